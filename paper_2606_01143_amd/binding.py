@@ -1,0 +1,215 @@
+"""ctypes binding of libspr: one Python function per C entry point, same
+name without the ``spr_`` prefix, same argument order.  Argument
+marshalling only (tensor -> device pointer, stream -> hipStream_t, status ->
+exception); every step of the computation runs in the HIP library.
+
+Tensors must be contiguous GPU tensors; ``None`` passes a NULL pointer.
+The library must be built (``python -m paper_2606_01143_amd.build``);
+loading fails loudly otherwise -- there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from ctypes import POINTER, byref, c_char_p, c_double, c_float, c_int32, c_size_t, c_uint32, c_void_p
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "lib", "libspr.so")
+
+SPR_F32 = 0
+SPR_BF16 = 1
+SPR_DETERMINISTIC = 1
+
+OP_PREFIX_FWD = 0
+OP_SUFFIX_FWD = 1
+OP_SUFFIX_BWD = 2
+OP_PREFIX_BWD = 3
+OP_DENSE_BASELINE = 4
+
+STATUS = {0: "SPR_OK", 1: "SPR_ERR_INVALID_ARG", 2: "SPR_ERR_UNSUPPORTED",
+          3: "SPR_ERR_MISALIGNED", 4: "SPR_ERR_ALIASING", 5: "SPR_ERR_WORKSPACE",
+          6: "SPR_ERR_HIP"}
+
+# C symbol -> (argtypes, restype)
+_P = c_void_p
+_SIGNATURES = {
+    "spr_prefix_fwd": ([_P, _P, _P, _P, _P, _P, _P], c_int32),
+    "spr_suffix_attn_fwd": ([_P, _P, _P, _P, _P, _P, _P, c_int32, c_int32, c_int32, _P, _P, _P,
+                             c_size_t, _P], c_int32),
+    "spr_suffix_attn_bwd_accum": ([_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, c_int32, c_int32, c_int32,
+                                   _P, _P, _P, _P, _P, _P, c_size_t, _P], c_int32),
+    "spr_prefix_bwd": ([_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, c_size_t, _P], c_int32),
+    "spr_dense_recompute_baseline": ([_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, c_int32, c_int32,
+                                      c_int32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                                      c_size_t, _P], c_int32),
+    "spr_workspace_size": ([c_int32, _P, c_int32, c_int32, c_int32, POINTER(c_size_t)], c_int32),
+    "spr_gkv_cache_zero": ([_P, _P, _P, _P], c_int32),
+    "spr_gkv_accumulate": ([_P, _P, _P, _P, _P, _P], c_int32),
+    "spr_profile_enable": ([c_int32], c_int32),
+    "spr_profile_reset": ([], c_int32),
+    "spr_profile_query": ([c_char_p, POINTER(c_double), POINTER(c_int32)], c_int32),
+    "spr_profile_num_kernels": ([], c_int32),
+    "spr_profile_kernel_name": ([c_int32], c_char_p),
+    "spr_status_string": ([c_int32], c_char_p),
+    "spr_last_error": ([], c_char_p),
+    "spr_version": ([], c_char_p),
+}
+
+
+class SprDims(ctypes.Structure):
+    """Mirror of ``spr_dims`` in include/spr.h."""
+    _fields_ = [("num_q_heads", c_int32), ("num_kv_heads", c_int32), ("head_dim", c_int32),
+                ("prefix_len", c_int32), ("softmax_scale", c_float), ("dtype", c_int32),
+                ("flags", c_uint32)]
+
+
+class SprError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        self.status = status
+        self.status_name = STATUS.get(status, f"status {status}")
+        super().__init__(f"{self.status_name}: {message}")
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libspr.so (once) and declare every entry point's signature."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                f"libspr.so is not built ({LIB_PATH}); build it with "
+                "`python -m paper_2606_01143_amd.build` -- there is no fallback path")
+        handle = ctypes.CDLL(LIB_PATH)
+        for name, (argtypes, restype) in _SIGNATURES.items():
+            fn = getattr(handle, name)
+            fn.argtypes = argtypes
+            fn.restype = restype
+        _lib = handle
+    return _lib
+
+
+def make_dims(num_q_heads: int, num_kv_heads: int, head_dim: int, prefix_len: int,
+              dtype: str = "bf16", softmax_scale: float = 0.0,
+              deterministic: bool = False) -> SprDims:
+    code = {"f32": SPR_F32, "bf16": SPR_BF16}[dtype]
+    return SprDims(num_q_heads, num_kv_heads, head_dim, prefix_len, softmax_scale, code,
+                   SPR_DETERMINISTIC if deterministic else 0)
+
+
+def _ptr(x):
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    if not x.is_cuda:
+        raise ValueError("libspr takes GPU tensors only")
+    if not x.is_contiguous():
+        raise ValueError("libspr takes contiguous tensors only")
+    return x.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _check(status: int) -> None:
+    if status != 0:
+        raise SprError(status, lib().spr_last_error().decode())
+
+
+def _nbytes(ws) -> int:
+    return 0 if ws is None else ws.numel() * ws.element_size()
+
+
+# ------------------------------------------------------------ entry points
+def prefix_fwd(dims, q_p, k_p, v_p, o_p, lse_p, stream=None):
+    _check(lib().spr_prefix_fwd(byref(dims), _ptr(q_p), _ptr(k_p), _ptr(v_p), _ptr(o_p),
+                                _ptr(lse_p), _stream(stream)))
+
+
+def suffix_attn_fwd(dims, k_p, v_p, q_s, k_s, v_s, cu_seqlens, n_mb, max_len, total_len, o_s,
+                    lse_s, ws=None, stream=None):
+    _check(lib().spr_suffix_attn_fwd(byref(dims), _ptr(k_p), _ptr(v_p), _ptr(q_s), _ptr(k_s),
+                                     _ptr(v_s), _ptr(cu_seqlens), n_mb, max_len, total_len,
+                                     _ptr(o_s), _ptr(lse_s), _ptr(ws), _nbytes(ws),
+                                     _stream(stream)))
+
+
+def suffix_attn_bwd_accum(dims, k_p, v_p, q_s, k_s, v_s, o_s, lse_s, do_s, cu_seqlens, n_mb,
+                          max_len, total_len, dq_s, dk_s, dv_s, gk_cache, gv_cache, ws=None,
+                          stream=None):
+    _check(lib().spr_suffix_attn_bwd_accum(
+        byref(dims), _ptr(k_p), _ptr(v_p), _ptr(q_s), _ptr(k_s), _ptr(v_s), _ptr(o_s),
+        _ptr(lse_s), _ptr(do_s), _ptr(cu_seqlens), n_mb, max_len, total_len, _ptr(dq_s),
+        _ptr(dk_s), _ptr(dv_s), _ptr(gk_cache), _ptr(gv_cache), _ptr(ws), _nbytes(ws),
+        _stream(stream)))
+
+
+def prefix_bwd(dims, q_p, k_p, v_p, o_p, lse_p, do_p, gk_cache, gv_cache, dq_p, dk_p, dv_p,
+               ws=None, stream=None):
+    _check(lib().spr_prefix_bwd(byref(dims), _ptr(q_p), _ptr(k_p), _ptr(v_p), _ptr(o_p),
+                                _ptr(lse_p), _ptr(do_p), _ptr(gk_cache), _ptr(gv_cache),
+                                _ptr(dq_p), _ptr(dk_p), _ptr(dv_p), _ptr(ws), _nbytes(ws),
+                                _stream(stream)))
+
+
+def dense_recompute_baseline(dims, q_p, k_p, v_p, do_p_seq, q_s, k_s, v_s, do_s, cu_seqlens, n,
+                             max_len, total_len, o_p, lse_p, o_s, lse_s, dq_s, dk_s, dv_s, dq_p,
+                             dk_p, dv_p, ws=None, stream=None):
+    _check(lib().spr_dense_recompute_baseline(
+        byref(dims), _ptr(q_p), _ptr(k_p), _ptr(v_p), _ptr(do_p_seq), _ptr(q_s), _ptr(k_s),
+        _ptr(v_s), _ptr(do_s), _ptr(cu_seqlens), n, max_len, total_len, _ptr(o_p), _ptr(lse_p),
+        _ptr(o_s), _ptr(lse_s), _ptr(dq_s), _ptr(dk_s), _ptr(dv_s), _ptr(dq_p), _ptr(dk_p),
+        _ptr(dv_p), _ptr(ws), _nbytes(ws), _stream(stream)))
+
+
+def workspace_size(op, dims, n_mb=0, max_len=0, total_len=0) -> int:
+    out = c_size_t(0)
+    _check(lib().spr_workspace_size(op, byref(dims), n_mb, max_len, total_len, byref(out)))
+    return int(out.value)
+
+
+def gkv_cache_zero(dims, gk_cache, gv_cache, stream=None):
+    _check(lib().spr_gkv_cache_zero(byref(dims), _ptr(gk_cache), _ptr(gv_cache), _stream(stream)))
+
+
+def gkv_accumulate(dims, gk_cache, gv_cache, dgk, dgv, stream=None):
+    _check(lib().spr_gkv_accumulate(byref(dims), _ptr(gk_cache), _ptr(gv_cache), _ptr(dgk),
+                                    _ptr(dgv), _stream(stream)))
+
+
+def profile_enable(on: bool = True):
+    _check(lib().spr_profile_enable(1 if on else 0))
+
+
+def profile_reset():
+    _check(lib().spr_profile_reset())
+
+
+def profile_query(kernel: str):
+    ms, cnt = c_double(0.0), c_int32(0)
+    _check(lib().spr_profile_query(kernel.encode(), byref(ms), byref(cnt)))
+    return float(ms.value), int(cnt.value)
+
+
+def profile_kernels():
+    n = lib().spr_profile_num_kernels()
+    return [lib().spr_profile_kernel_name(i).decode() for i in range(n)]
+
+
+def status_string(status: int) -> str:
+    return lib().spr_status_string(status).decode()
+
+
+def last_error() -> str:
+    return lib().spr_last_error().decode()
+
+
+def version() -> str:
+    return lib().spr_version().decode()

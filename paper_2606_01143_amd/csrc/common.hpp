@@ -1,0 +1,101 @@
+// Shared definitions for the gfx950 kernels of libspr.
+//
+// Every kernel works on one "virtual sequence" [P || S(s)] per suffix s: the
+// prefix segment (rows/keys 0..P-1 of the *_p buffers) followed by suffix s
+// (rows cu[s]..cu[s+1]-1 of the packed *_s buffers).  Keys are never copied
+// into a concatenated buffer; each tile reads from whichever segment it
+// belongs to.  Tiles never straddle the two segments: the tile grid of the
+// prefix covers [0, P) and the tile grid of each suffix restarts at its first
+// token, so every tile is either all-prefix or all-one-suffix.
+//
+// Visibility (causal, inclusive): prefix row r sees prefix keys j <= r;
+// suffix row t of s sees every prefix key and suffix keys j <= t of s.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace spr {
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+// All arguments of one attention launch.  Unused fields are null/zero.
+struct AttnArgs {
+  // prefix segment: rows and keys 0..P-1
+  const void* q_p;
+  const void* k_p;
+  const void* v_p;
+  void* o_p;
+  float* lse_p;        // [P, Hq]
+  const void* do_p;    // upstream adjoint of the prefix rows (bwd)
+  float* dd_p;         // rowsum(dO * O) [P, Hq] (bwd)
+  float* dq_acc_p;     // fp32 dQ accumulator [P, Hq, d] (bwd)
+  // suffix segment: packed rows, suffix s = rows cu[s] .. cu[s+1]-1
+  const void* q_s;
+  const void* k_s;
+  const void* v_s;
+  void* o_s;
+  float* lse_s;        // [total_len, Hq]
+  const void* do_s;
+  float* dd_s;         // [total_len, Hq]
+  float* dq_acc_s;     // [total_len, Hq, d]
+  const int32_t* cu;   // device cu_seqlens
+  int32_t P;
+  int32_t total_len;
+  int32_t hq;
+  int32_t hkv;
+  float scale;         // softmax scale
+  float scale_log2;    // softmax scale * log2(e)
+  int32_t seq_base;    // first suffix of this launch
+  int32_t n_seq;       // suffixes in this launch
+  // query-outer launches (forward, fp32 dQ): grid.x = prefix row tiles then
+  // suffix row tiles of suffix seq_base + blockIdx.z
+  int32_t n_prefix_q_tiles;
+  int32_t n_suffix_q_tiles;
+  // key-outer launches (backward): grid.x = prefix key tiles, then
+  // n_seq * n_suffix_k_tiles suffix key tiles
+  int32_t n_prefix_k_tiles;
+  int32_t n_suffix_k_tiles;
+  int32_t prefix_rows;   // prefix-key tiles also take the prefix rows (causal)
+  int32_t suffix_rows;   // prefix-key tiles take the suffix rows of suffixes
+                         // seq_base .. seq_base+n_seq-1 (all visible)
+  int32_t pk_mode;       // prefix-key epilogue: 0 => gk/gv += fp32 gradient;
+                         // 1 => dk_p/dv_p = gradient + gk/gv in storage dtype
+  float* gk;             // [P, Hkv, d] fp32
+  float* gv;
+  void* dk_p;
+  void* dv_p;
+  void* dk_s;
+  void* dv_s;
+};
+
+enum PkMode { kPkAccumulate = 0, kPkInject = 1 };
+
+__device__ __forceinline__ float bf2f(bf16 x) { return (float)x; }
+__device__ __forceinline__ bf16 f2bf(float x) { return (bf16)x; }
+
+template <typename T>
+__device__ __forceinline__ float to_f32(T x);
+template <>
+__device__ __forceinline__ float to_f32<float>(float x) { return x; }
+template <>
+__device__ __forceinline__ float to_f32<bf16>(bf16 x) { return (float)x; }
+
+template <typename T>
+__device__ __forceinline__ T from_f32(float x);
+template <>
+__device__ __forceinline__ float from_f32<float>(float x) { return x; }
+template <>
+__device__ __forceinline__ bf16 from_f32<bf16>(float x) { return (bf16)x; }
+
+__device__ __forceinline__ int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+}  // namespace spr

@@ -1,0 +1,149 @@
+// Bandwidth-bound helper kernels: the backward's row statistic
+// D = rowsum(dO * O), fp32 accumulator conversion, zero fill, and the
+// standalone gradient-cache accumulation G += g.
+//
+// All of them stream memory once with 16-byte vector accesses; the fill and
+// accumulate kernels are grid-stride loops sized to a few waves per CU.
+#include "common.hpp"
+#include "launch.hpp"
+
+namespace spr {
+
+namespace {
+
+constexpr int kAuxThreads = 256;
+
+int aux_blocks(size_t n_vec) {
+  size_t b = (n_vec + kAuxThreads - 1) / kAuxThreads;
+  const size_t cap = 256 * 8;  // 8 workgroups per CU on 256 CUs
+  if (b > cap) b = cap;
+  if (b == 0) b = 1;
+  return (int)b;
+}
+
+}  // namespace
+
+// One wave per (row, head): each lane takes d/64 consecutive elements.
+// With cu != nullptr the rows are those of suffix `seq` only:
+// cu[seq] .. cu[seq+1]-1, and `rows` is an upper bound on their count.
+template <typename T, int D>
+__global__ __launch_bounds__(kAuxThreads) void row_dot_kernel(const T* __restrict__ dO,
+                                                            const T* __restrict__ O, int rows,
+                                                            const int32_t* __restrict__ cu,
+                                                            int seq, int hq,
+                                                            float* __restrict__ dd) {
+  constexpr int PER = D / 64;
+  const int wave = (blockIdx.x * kAuxThreads + threadIdx.x) >> 6;
+  const int lane = threadIdx.x & 63;
+  int row0 = 0, nrows = rows;
+  if (cu != nullptr) {
+    row0 = cu[seq];
+    nrows = cu[seq + 1] - row0;
+  }
+  if (wave >= nrows * hq) return;
+  const int row = row0 + wave / hq, h = wave % hq;
+  float acc = 0.f;
+  if (dO != nullptr) {
+    const size_t off = ((size_t)row * hq + h) * D + lane * PER;
+#pragma unroll
+    for (int j = 0; j < PER; ++j) acc += to_f32<T>(dO[off + j]) * to_f32<T>(O[off + j]);
+  }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) acc += __shfl_xor(acc, m);
+  if (lane == 0) dd[(size_t)row * hq + h] = acc;
+}
+
+__global__ __launch_bounds__(kAuxThreads) void fill_zero_kernel(float4* p, size_t n4) {
+  for (size_t i = (size_t)blockIdx.x * kAuxThreads + threadIdx.x; i < n4;
+       i += (size_t)gridDim.x * kAuxThreads)
+    p[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+}
+
+__global__ __launch_bounds__(kAuxThreads) void accumulate_kernel(float4* __restrict__ dst,
+                                                                const float4* __restrict__ src,
+                                                                size_t n4) {
+  for (size_t i = (size_t)blockIdx.x * kAuxThreads + threadIdx.x; i < n4;
+       i += (size_t)gridDim.x * kAuxThreads) {
+    float4 a = dst[i];
+    const float4 b = src[i];
+    a.x += b.x; a.y += b.y; a.z += b.z; a.w += b.w;
+    dst[i] = a;
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(kAuxThreads) void convert_kernel(const float4* __restrict__ acc,
+                                                             float scale,
+                                                             const float4* __restrict__ add,
+                                                             T* __restrict__ out, size_t n4) {
+  for (size_t i = (size_t)blockIdx.x * kAuxThreads + threadIdx.x; i < n4;
+       i += (size_t)gridDim.x * kAuxThreads) {
+    float4 v = acc[i];
+    v.x *= scale; v.y *= scale; v.z *= scale; v.w *= scale;
+    if (add != nullptr) {
+      const float4 b = add[i];
+      v.x += b.x; v.y += b.y; v.z += b.z; v.w += b.w;
+    }
+    out[4 * i + 0] = from_f32<T>(v.x);
+    out[4 * i + 1] = from_f32<T>(v.y);
+    out[4 * i + 2] = from_f32<T>(v.z);
+    out[4 * i + 3] = from_f32<T>(v.w);
+  }
+}
+
+hipError_t launch_row_dot(int dtype, const void* dO, const void* O, int rows, const int32_t* cu,
+                          int seq, int hq, int head_dim, float* dd, hipStream_t st) {
+  if (rows <= 0) return hipSuccess;
+  const size_t waves = (size_t)rows * hq;
+  const int blocks = (int)((waves * 64 + kAuxThreads - 1) / kAuxThreads);
+  ProfileScope ps("row_dot", st);
+  if (dtype == 0) {
+    if (head_dim == 64)
+      hipLaunchKernelGGL((row_dot_kernel<float, 64>), blocks, kAuxThreads, 0, st,
+                         (const float*)dO, (const float*)O, rows, cu, seq, hq, dd);
+    else
+      hipLaunchKernelGGL((row_dot_kernel<float, 128>), blocks, kAuxThreads, 0, st,
+                         (const float*)dO, (const float*)O, rows, cu, seq, hq, dd);
+  } else {
+    if (head_dim == 64)
+      hipLaunchKernelGGL((row_dot_kernel<bf16, 64>), blocks, kAuxThreads, 0, st,
+                         (const bf16*)dO, (const bf16*)O, rows, cu, seq, hq, dd);
+    else
+      hipLaunchKernelGGL((row_dot_kernel<bf16, 128>), blocks, kAuxThreads, 0, st,
+                         (const bf16*)dO, (const bf16*)O, rows, cu, seq, hq, dd);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_zero(float* p, size_t n, hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  const size_t n4 = n / 4;  // every buffer here is a multiple of 4 floats
+  ProfileScope ps("fill_zero", st);
+  hipLaunchKernelGGL(fill_zero_kernel, aux_blocks(n4), kAuxThreads, 0, st, (float4*)p, n4);
+  return hipGetLastError();
+}
+
+hipError_t launch_accumulate(float* dst, const float* src, size_t n, hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  const size_t n4 = n / 4;
+  ProfileScope ps("gkv_accumulate", st);
+  hipLaunchKernelGGL(accumulate_kernel, aux_blocks(n4), kAuxThreads, 0, st, (float4*)dst,
+                     (const float4*)src, n4);
+  return hipGetLastError();
+}
+
+hipError_t launch_convert(int dtype, const float* acc, float scale, const float* add, void* out,
+                          size_t n, hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  const size_t n4 = n / 4;
+  ProfileScope ps("convert", st);
+  if (dtype == 0)
+    hipLaunchKernelGGL(convert_kernel<float>, aux_blocks(n4), kAuxThreads, 0, st,
+                       (const float4*)acc, scale, (const float4*)add, (float*)out, n4);
+  else
+    hipLaunchKernelGGL(convert_kernel<bf16>, aux_blocks(n4), kAuxThreads, 0, st,
+                       (const float4*)acc, scale, (const float4*)add, (bf16*)out, n4);
+  return hipGetLastError();
+}
+
+}  // namespace spr

@@ -1,0 +1,71 @@
+// Host-side launchers of the gfx950 kernels and the per-kernel event timer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "common.hpp"
+
+namespace spr {
+
+// --- per-kernel timing (enabled through spr_profile_enable) -------------
+bool profile_enabled();
+void profile_record(const char* kernel, hipEvent_t begin, hipEvent_t end);
+hipEvent_t profile_event();  // from a pool owned by the profiler
+
+// Brackets one kernel launch with two events on `stream` while profiling
+// is enabled; a no-op otherwise.
+class ProfileScope {
+ public:
+  ProfileScope(const char* kernel, hipStream_t stream) : kernel_(kernel), stream_(stream) {
+    if (profile_enabled()) {
+      begin_ = profile_event();
+      end_ = profile_event();
+      if (begin_ && end_) hipEventRecord(begin_, stream_);
+    }
+  }
+  ~ProfileScope() {
+    if (begin_ && end_) {
+      hipEventRecord(end_, stream_);
+      profile_record(kernel_, begin_, end_);
+    }
+  }
+  ProfileScope(const ProfileScope&) = delete;
+  ProfileScope& operator=(const ProfileScope&) = delete;
+
+ private:
+  const char* kernel_;
+  hipStream_t stream_;
+  hipEvent_t begin_ = nullptr;
+  hipEvent_t end_ = nullptr;
+};
+
+// --- fp32 storage path (kernels_f32.hip) --------------------------------
+hipError_t launch_fwd_f32(const AttnArgs& a, int head_dim, int n_z, hipStream_t st);
+hipError_t launch_bwd_f32(const AttnArgs& a, int head_dim, int n_qz, hipStream_t st);
+
+// --- bf16 storage path, MFMA (kernels_bf16_fwd.hip, kernels_bf16_bwd.hip) --
+hipError_t launch_fwd_bf16(const AttnArgs& a, int head_dim, int n_z, hipStream_t st);
+hipError_t launch_bwd_bf16(const AttnArgs& a, int head_dim, int n_qz, bool deterministic,
+                           hipStream_t st);
+// Row-tile sizes the launchers expect in AttnArgs (q tiles / k tiles).
+int fwd_bf16_block_q();
+int bwd_bf16_block_k();
+int f32_block_q();
+int f32_block_k();
+
+// --- auxiliary kernels (kernels_aux.hip) ----------------------------------
+// dd[row * hq + h] = sum_d dO[row,h,d] * O[row,h,d] for rows [0, rows),
+// or, when cu != nullptr, for the rows cu[seq] .. cu[seq+1]-1 of one packed
+// suffix (rows then bounds their count); dO == nullptr gives 0.
+hipError_t launch_row_dot(int dtype, const void* dO, const void* O, int rows, const int32_t* cu,
+                          int seq, int hq, int head_dim, float* dd, hipStream_t st);
+hipError_t launch_fill_zero(float* p, size_t n, hipStream_t st);
+// out = acc * scale (+ add when add != nullptr), converted to `dtype`
+hipError_t launch_convert(int dtype, const float* acc, float scale, const float* add,
+                          void* out, size_t n, hipStream_t st);
+// dst += src
+hipError_t launch_accumulate(float* dst, const float* src, size_t n, hipStream_t st);
+
+}  // namespace spr

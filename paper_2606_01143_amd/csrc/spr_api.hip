@@ -1,0 +1,629 @@
+// C ABI of libspr: argument validation, workspace layout and dispatch of the
+// three-phase schedule (paper Sec. 3.2) and the dense-recompute baseline.
+//
+// Nothing is launched unless every check passes.  The library keeps no state
+// between calls except the optional event profiler.
+#include <math.h>
+#include <string.h>
+
+#include <algorithm>
+#include <map>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/spr.h"
+#include "common.hpp"
+#include "launch.hpp"
+
+namespace spr {
+
+namespace {
+
+thread_local std::string g_last_error;
+
+spr_status fail(spr_status st, const std::string& msg) {
+  g_last_error = msg;
+  return st;
+}
+
+spr_status ok() {
+  g_last_error.clear();
+  return SPR_OK;
+}
+
+size_t dtype_bytes(int dtype) { return dtype == SPR_F32 ? 4 : 2; }
+
+size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+int tiles(int n, int b) { return n <= 0 ? 0 : (n + b - 1) / b; }
+
+// ------------------------------------------------------------ validation
+spr_status check_dims(const spr_dims* d) {
+  if (d == nullptr) return fail(SPR_ERR_INVALID_ARG, "dims is null");
+  if (d->num_q_heads < 1 || d->num_kv_heads < 1)
+    return fail(SPR_ERR_INVALID_ARG, "num_q_heads and num_kv_heads must be >= 1");
+  if (d->num_q_heads % d->num_kv_heads != 0)
+    return fail(SPR_ERR_INVALID_ARG, "num_q_heads must be a multiple of num_kv_heads");
+  if (d->prefix_len < 0) return fail(SPR_ERR_INVALID_ARG, "prefix_len must be >= 0");
+  if (d->head_dim != 64 && d->head_dim != 128)
+    return fail(SPR_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
+  if (d->dtype != SPR_F32 && d->dtype != SPR_BF16)
+    return fail(SPR_ERR_UNSUPPORTED, "dtype must be SPR_F32 or SPR_BF16");
+  if ((d->flags & ~(uint32_t)SPR_DETERMINISTIC) != 0)
+    return fail(SPR_ERR_UNSUPPORTED, "unknown flag bits");
+  if (!(d->softmax_scale >= 0.f) || isinf(d->softmax_scale))
+    return fail(SPR_ERR_INVALID_ARG, "softmax_scale must be finite and >= 0");
+  return SPR_OK;
+}
+
+spr_status check_suffix_sizes(int32_t n, int32_t max_len, int32_t total_len) {
+  if (n < 1) return fail(SPR_ERR_INVALID_ARG, "number of suffixes must be >= 1");
+  if (max_len < 1) return fail(SPR_ERR_INVALID_ARG, "max_len must be >= 1");
+  if (total_len < n || total_len < max_len)
+    return fail(SPR_ERR_INVALID_ARG, "total_len must be >= n and >= max_len");
+  if ((int64_t)n * max_len < total_len)
+    return fail(SPR_ERR_INVALID_ARG, "total_len exceeds n * max_len");
+  return SPR_OK;
+}
+
+struct Buf {
+  const void* p;
+  size_t bytes;
+  const char* name;
+  bool required;
+  uintptr_t align = 16;  // LSE and cu_seqlens are read as 4-byte scalars
+};
+
+spr_status check_bufs(const std::vector<Buf>& bufs) {
+  for (const Buf& b : bufs) {
+    if (b.bytes == 0) continue;
+    if (b.p == nullptr) {
+      if (b.required) return fail(SPR_ERR_INVALID_ARG, std::string(b.name) + " is null");
+      continue;
+    }
+    if (((uintptr_t)b.p & (b.align - 1)) != 0)
+      return fail(SPR_ERR_MISALIGNED,
+                  std::string(b.name) + " is not " + std::to_string(b.align) + "-byte aligned");
+  }
+  return SPR_OK;
+}
+
+bool overlaps(const Buf& a, const Buf& b) {
+  if (a.p == nullptr || b.p == nullptr || a.bytes == 0 || b.bytes == 0) return false;
+  const uintptr_t a0 = (uintptr_t)a.p, a1 = a0 + a.bytes;
+  const uintptr_t b0 = (uintptr_t)b.p, b1 = b0 + b.bytes;
+  return a0 < b1 && b0 < a1;
+}
+
+// every buffer in `inout` must overlap nothing else in `all`
+spr_status check_aliasing(const std::vector<Buf>& inout, const std::vector<Buf>& all) {
+  for (const Buf& x : inout)
+    for (const Buf& y : all) {
+      if (x.p == y.p && x.name == y.name) continue;
+      if (overlaps(x, y))
+        return fail(SPR_ERR_ALIASING, std::string(x.name) + " overlaps " + y.name);
+    }
+  return SPR_OK;
+}
+
+spr_status hip_check(hipError_t e, const char* what) {
+  if (e != hipSuccess)
+    return fail(SPR_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+  return SPR_OK;
+}
+
+float eff_scale(const spr_dims* d) {
+  return d->softmax_scale > 0.f ? d->softmax_scale : 1.0f / sqrtf((float)d->head_dim);
+}
+
+AttnArgs base_args(const spr_dims* d) {
+  AttnArgs a;
+  memset(&a, 0, sizeof(a));
+  a.P = d->prefix_len;
+  a.hq = d->num_q_heads;
+  a.hkv = d->num_kv_heads;
+  a.scale = eff_scale(d);
+  a.scale_log2 = a.scale * kLog2e;
+  return a;
+}
+
+int block_q(int dtype) { return dtype == SPR_BF16 ? fwd_bf16_block_q() : f32_block_q(); }
+int block_k(int dtype) { return dtype == SPR_BF16 ? bwd_bf16_block_k() : f32_block_k(); }
+
+hipError_t launch_fwd(const spr_dims* d, const AttnArgs& a, int n_z, hipStream_t st) {
+  return d->dtype == SPR_BF16 ? launch_fwd_bf16(a, d->head_dim, n_z, st)
+                              : launch_fwd_f32(a, d->head_dim, n_z, st);
+}
+
+hipError_t launch_bwd(const spr_dims* d, const AttnArgs& a, int n_qz, hipStream_t st) {
+  return d->dtype == SPR_BF16
+             ? launch_bwd_bf16(a, d->head_dim, n_qz, (d->flags & SPR_DETERMINISTIC) != 0, st)
+             : launch_bwd_f32(a, d->head_dim, n_qz, st);
+}
+
+// ------------------------------------------------------------- workspace
+struct WsLayout {
+  size_t dd_p = 0, dq_acc_p = 0, dd_s = 0, dq_acc_s = 0, dk_acc_p = 0, dv_acc_p = 0;
+  size_t total = 0;
+};
+
+WsLayout ws_layout(int op, const spr_dims* d, int32_t max_len, int32_t total_len) {
+  (void)max_len;
+  WsLayout w;
+  const size_t hq = d->num_q_heads, hkv = d->num_kv_heads, hd = d->head_dim;
+  const size_t P = d->prefix_len, T = total_len > 0 ? total_len : 0;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes, 256);
+    return at;
+  };
+  const bool deterministic = (d->flags & SPR_DETERMINISTIC) != 0;
+  (void)deterministic;
+  switch (op) {
+    case SPR_OP_PREFIX_FWD:
+    case SPR_OP_SUFFIX_FWD:
+      break;
+    case SPR_OP_SUFFIX_BWD:
+      w.dd_s = take(hq * T * 4);
+      w.dq_acc_s = take(T * hq * hd * 4);
+      break;
+    case SPR_OP_PREFIX_BWD:
+      w.dd_p = take(hq * P * 4);
+      w.dq_acc_p = take(P * hq * hd * 4);
+      break;
+    case SPR_OP_DENSE_BASELINE:
+      w.dd_p = take(hq * P * 4);
+      w.dq_acc_p = take(P * hq * hd * 4);
+      w.dd_s = take(hq * T * 4);
+      w.dq_acc_s = take(T * hq * hd * 4);
+      w.dk_acc_p = take(P * hkv * hd * 4);
+      w.dv_acc_p = take(P * hkv * hd * 4);
+      break;
+    default:
+      break;
+  }
+  w.total = off;
+  return w;
+}
+
+spr_status check_ws(const WsLayout& w, const void* ws, size_t ws_bytes) {
+  if (w.total == 0) return SPR_OK;
+  if (ws == nullptr) return fail(SPR_ERR_WORKSPACE, "workspace is null");
+  if (ws_bytes < w.total)
+    return fail(SPR_ERR_WORKSPACE, "workspace too small: need " + std::to_string(w.total) +
+                                       " bytes, got " + std::to_string(ws_bytes));
+  if (((uintptr_t)ws & 15u) != 0) return fail(SPR_ERR_MISALIGNED, "workspace is not 16-byte aligned");
+  return SPR_OK;
+}
+
+template <typename T>
+T* at(void* base, size_t off) {
+  return (T*)((char*)base + off);
+}
+
+// ---------------------------------------------------------------- profiler
+struct ProfRec {
+  const char* name;
+  hipEvent_t b, e;
+};
+std::mutex g_prof_mu;
+bool g_prof_on = false;
+std::vector<ProfRec> g_prof_pending;
+std::vector<hipEvent_t> g_prof_pool;
+std::map<std::string, std::pair<double, int>> g_prof_totals;
+std::vector<std::string> g_prof_names;
+
+void prof_drain_locked() {
+  for (const ProfRec& r : g_prof_pending) {
+    float ms = 0.f;
+    if (hipEventSynchronize(r.e) == hipSuccess && hipEventElapsedTime(&ms, r.b, r.e) == hipSuccess) {
+      auto& t = g_prof_totals[r.name];
+      if (t.second == 0 && std::find(g_prof_names.begin(), g_prof_names.end(), r.name) == g_prof_names.end())
+        g_prof_names.push_back(r.name);
+      t.first += ms;
+      t.second += 1;
+    }
+    g_prof_pool.push_back(r.b);
+    g_prof_pool.push_back(r.e);
+  }
+  g_prof_pending.clear();
+}
+
+}  // namespace
+
+bool profile_enabled() {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  return g_prof_on;
+}
+
+hipEvent_t profile_event() {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  if (!g_prof_pool.empty()) {
+    hipEvent_t e = g_prof_pool.back();
+    g_prof_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+void profile_record(const char* kernel, hipEvent_t begin, hipEvent_t end) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  g_prof_pending.push_back({kernel, begin, end});
+}
+
+}  // namespace spr
+
+using namespace spr;
+
+extern "C" {
+
+const char* spr_version(void) { return "spr 0.1.0 (gfx950)"; }
+
+const char* spr_last_error(void) { return g_last_error.c_str(); }
+
+const char* spr_status_string(int32_t s) {
+  switch (s) {
+    case SPR_OK: return "SPR_OK";
+    case SPR_ERR_INVALID_ARG: return "SPR_ERR_INVALID_ARG";
+    case SPR_ERR_UNSUPPORTED: return "SPR_ERR_UNSUPPORTED";
+    case SPR_ERR_MISALIGNED: return "SPR_ERR_MISALIGNED";
+    case SPR_ERR_ALIASING: return "SPR_ERR_ALIASING";
+    case SPR_ERR_WORKSPACE: return "SPR_ERR_WORKSPACE";
+    case SPR_ERR_HIP: return "SPR_ERR_HIP";
+    default: return "SPR_ERR_UNKNOWN";
+  }
+}
+
+spr_status spr_workspace_size(int32_t op, const spr_dims* dims, int32_t n_mb, int32_t max_len,
+                              int32_t total_len, size_t* bytes) {
+  spr_status st = check_dims(dims);
+  if (st != SPR_OK) return st;
+  if (bytes == nullptr) return fail(SPR_ERR_INVALID_ARG, "bytes is null");
+  if (op < SPR_OP_PREFIX_FWD || op > SPR_OP_DENSE_BASELINE)
+    return fail(SPR_ERR_INVALID_ARG, "unknown op");
+  if (op != SPR_OP_PREFIX_FWD && op != SPR_OP_PREFIX_BWD) {
+    st = check_suffix_sizes(n_mb, max_len, total_len);
+    if (st != SPR_OK) return st;
+  }
+  *bytes = ws_layout(op, dims, max_len, total_len).total;
+  return ok();
+}
+
+spr_status spr_prefix_fwd(const spr_dims* dims, const void* q_p, const void* k_p, const void* v_p,
+                          void* o_p, float* lse_p, hipStream_t stream) {
+  spr_status st = check_dims(dims);
+  if (st != SPR_OK) return st;
+  const size_t P = dims->prefix_len, hq = dims->num_q_heads, hkv = dims->num_kv_heads,
+               hd = dims->head_dim, eb = dtype_bytes(dims->dtype);
+  std::vector<Buf> bufs = {{q_p, P * hq * hd * eb, "q_p", true},
+                           {k_p, P * hkv * hd * eb, "k_p", true},
+                           {v_p, P * hkv * hd * eb, "v_p", true},
+                           {o_p, P * hq * hd * eb, "o_p", true},
+                           {lse_p, hq * P * 4, "lse_p", true, 4}};
+  if ((st = check_bufs(bufs)) != SPR_OK) return st;
+  if (P == 0) return ok();
+  AttnArgs a = base_args(dims);
+  a.q_p = q_p; a.k_p = k_p; a.v_p = v_p; a.o_p = o_p; a.lse_p = lse_p;
+  a.n_prefix_q_tiles = tiles(dims->prefix_len, block_q(dims->dtype));
+  if ((st = hip_check(launch_fwd(dims, a, 1, stream), "prefix forward")) != SPR_OK) return st;
+  return ok();
+}
+
+spr_status spr_suffix_attn_fwd(const spr_dims* dims, const void* k_p, const void* v_p,
+                               const void* q_s, const void* k_s, const void* v_s,
+                               const int32_t* cu_seqlens, int32_t n_mb, int32_t max_len,
+                               int32_t total_len, void* o_s, float* lse_s, void* ws,
+                               size_t ws_bytes, hipStream_t stream) {
+  spr_status st = check_dims(dims);
+  if (st != SPR_OK) return st;
+  if ((st = check_suffix_sizes(n_mb, max_len, total_len)) != SPR_OK) return st;
+  const size_t P = dims->prefix_len, hq = dims->num_q_heads, hkv = dims->num_kv_heads,
+               hd = dims->head_dim, eb = dtype_bytes(dims->dtype), T = total_len;
+  std::vector<Buf> bufs = {{k_p, P * hkv * hd * eb, "k_p", true},
+                           {v_p, P * hkv * hd * eb, "v_p", true},
+                           {q_s, T * hq * hd * eb, "q_s", true},
+                           {k_s, T * hkv * hd * eb, "k_s", true},
+                           {v_s, T * hkv * hd * eb, "v_s", true},
+                           {cu_seqlens, (size_t)(n_mb + 1) * 4, "cu_seqlens", true, 4},
+                           {o_s, T * hq * hd * eb, "o_s", true},
+                           {lse_s, hq * T * 4, "lse_s", true, 4}};
+  if ((st = check_bufs(bufs)) != SPR_OK) return st;
+  const WsLayout w = ws_layout(SPR_OP_SUFFIX_FWD, dims, max_len, total_len);
+  if ((st = check_ws(w, ws, ws_bytes)) != SPR_OK) return st;
+  AttnArgs a = base_args(dims);
+  a.k_p = k_p; a.v_p = v_p;
+  a.q_s = q_s; a.k_s = k_s; a.v_s = v_s; a.o_s = o_s; a.lse_s = lse_s;
+  a.cu = cu_seqlens;
+  a.total_len = total_len;
+  a.seq_base = 0;
+  a.n_seq = n_mb;
+  a.n_suffix_q_tiles = tiles(max_len, block_q(dims->dtype));
+  if ((st = hip_check(launch_fwd(dims, a, n_mb, stream), "suffix forward")) != SPR_OK) return st;
+  return ok();
+}
+
+spr_status spr_suffix_attn_bwd_accum(const spr_dims* dims, const void* k_p, const void* v_p,
+                                     const void* q_s, const void* k_s, const void* v_s,
+                                     const void* o_s, const float* lse_s, const void* do_s,
+                                     const int32_t* cu_seqlens, int32_t n_mb, int32_t max_len,
+                                     int32_t total_len, void* dq_s, void* dk_s, void* dv_s,
+                                     float* gk_cache, float* gv_cache, void* ws, size_t ws_bytes,
+                                     hipStream_t stream) {
+  spr_status st = check_dims(dims);
+  if (st != SPR_OK) return st;
+  if ((st = check_suffix_sizes(n_mb, max_len, total_len)) != SPR_OK) return st;
+  const size_t P = dims->prefix_len, hq = dims->num_q_heads, hkv = dims->num_kv_heads,
+               hd = dims->head_dim, eb = dtype_bytes(dims->dtype), T = total_len;
+  std::vector<Buf> bufs = {{k_p, P * hkv * hd * eb, "k_p", true},
+                           {v_p, P * hkv * hd * eb, "v_p", true},
+                           {q_s, T * hq * hd * eb, "q_s", true},
+                           {k_s, T * hkv * hd * eb, "k_s", true},
+                           {v_s, T * hkv * hd * eb, "v_s", true},
+                           {o_s, T * hq * hd * eb, "o_s", true},
+                           {lse_s, hq * T * 4, "lse_s", true, 4},
+                           {do_s, T * hq * hd * eb, "do_s", true},
+                           {cu_seqlens, (size_t)(n_mb + 1) * 4, "cu_seqlens", true, 4},
+                           {dq_s, T * hq * hd * eb, "dq_s", true},
+                           {dk_s, T * hkv * hd * eb, "dk_s", true},
+                           {dv_s, T * hkv * hd * eb, "dv_s", true},
+                           {gk_cache, P * hkv * hd * 4, "gk_cache", true},
+                           {gv_cache, P * hkv * hd * 4, "gv_cache", true}};
+  if ((st = check_bufs(bufs)) != SPR_OK) return st;
+  const WsLayout w = ws_layout(SPR_OP_SUFFIX_BWD, dims, max_len, total_len);
+  if ((st = check_ws(w, ws, ws_bytes)) != SPR_OK) return st;
+  std::vector<Buf> all = bufs;
+  all.push_back({ws, w.total, "ws", false});
+  if ((st = check_aliasing({bufs[12], bufs[13]}, all)) != SPR_OK) return st;
+
+  float* dd_s = at<float>(ws, w.dd_s);
+  float* dq_acc = at<float>(ws, w.dq_acc_s);
+  if ((st = hip_check(launch_row_dot(dims->dtype, do_s, o_s, total_len, nullptr, 0, (int)hq,
+                                     (int)hd, dd_s, stream), "row statistic")) != SPR_OK)
+    return st;
+  if ((st = hip_check(launch_fill_zero(dq_acc, T * hq * hd, stream), "dq clear")) != SPR_OK)
+    return st;
+  AttnArgs a = base_args(dims);
+  a.k_p = k_p; a.v_p = v_p;
+  a.q_s = q_s; a.k_s = k_s; a.v_s = v_s; a.do_s = do_s;
+  a.lse_s = const_cast<float*>(lse_s);
+  a.dd_s = dd_s; a.dq_acc_s = dq_acc;
+  a.cu = cu_seqlens;
+  a.total_len = total_len;
+  a.seq_base = 0;
+  a.n_seq = n_mb;
+  a.n_prefix_k_tiles = tiles(dims->prefix_len, block_k(dims->dtype));
+  a.n_suffix_k_tiles = tiles(max_len, block_k(dims->dtype));
+  a.prefix_rows = 0;
+  a.suffix_rows = 1;
+  a.pk_mode = kPkAccumulate;
+  a.gk = gk_cache; a.gv = gv_cache;
+  a.dk_s = dk_s; a.dv_s = dv_s;
+  a.n_suffix_q_tiles = tiles(max_len, block_q(dims->dtype));
+  if ((st = hip_check(launch_bwd(dims, a, n_mb, stream), "suffix backward")) != SPR_OK) return st;
+  if ((st = hip_check(launch_convert(dims->dtype, dq_acc, a.scale, nullptr, dq_s, T * hq * hd,
+                                     stream), "dq convert")) != SPR_OK)
+    return st;
+  return ok();
+}
+
+spr_status spr_prefix_bwd(const spr_dims* dims, const void* q_p, const void* k_p, const void* v_p,
+                          const void* o_p, const float* lse_p, const void* do_p,
+                          const float* gk_cache, const float* gv_cache, void* dq_p, void* dk_p,
+                          void* dv_p, void* ws, size_t ws_bytes, hipStream_t stream) {
+  spr_status st = check_dims(dims);
+  if (st != SPR_OK) return st;
+  const size_t P = dims->prefix_len, hq = dims->num_q_heads, hkv = dims->num_kv_heads,
+               hd = dims->head_dim, eb = dtype_bytes(dims->dtype);
+  std::vector<Buf> bufs = {{q_p, P * hq * hd * eb, "q_p", true},
+                           {k_p, P * hkv * hd * eb, "k_p", true},
+                           {v_p, P * hkv * hd * eb, "v_p", true},
+                           {o_p, P * hq * hd * eb, "o_p", true},
+                           {lse_p, hq * P * 4, "lse_p", true, 4},
+                           {do_p, P * hq * hd * eb, "do_p", false},
+                           {gk_cache, P * hkv * hd * 4, "gk_cache", true},
+                           {gv_cache, P * hkv * hd * 4, "gv_cache", true},
+                           {dq_p, P * hq * hd * eb, "dq_p", true},
+                           {dk_p, P * hkv * hd * eb, "dk_p", true},
+                           {dv_p, P * hkv * hd * eb, "dv_p", true}};
+  if ((st = check_bufs(bufs)) != SPR_OK) return st;
+  const WsLayout w = ws_layout(SPR_OP_PREFIX_BWD, dims, 0, 0);
+  if (do_p != nullptr && (st = check_ws(w, ws, ws_bytes)) != SPR_OK) return st;
+  std::vector<Buf> all = bufs;
+  if (do_p != nullptr) all.push_back({ws, w.total, "ws", false});
+  if ((st = check_aliasing({bufs[6], bufs[7]}, all)) != SPR_OK) return st;
+  if (P == 0) return ok();
+  const float scale = eff_scale(dims);
+  if (do_p == nullptr) {
+    // G_Y = 0: dQ_P = 0, dK_P = G_K, dV_P = G_V (paper App. A.5)
+    if ((st = hip_check(launch_fill_zero((float*)dq_p, P * hq * hd * eb / 4, stream), "dq zero")) != SPR_OK)
+      return st;
+    if ((st = hip_check(launch_convert(dims->dtype, gk_cache, 1.f, nullptr, dk_p, P * hkv * hd, stream),
+                        "dk convert")) != SPR_OK)
+      return st;
+    if ((st = hip_check(launch_convert(dims->dtype, gv_cache, 1.f, nullptr, dv_p, P * hkv * hd, stream),
+                        "dv convert")) != SPR_OK)
+      return st;
+    return ok();
+  }
+  float* dd_p = at<float>(ws, w.dd_p);
+  float* dq_acc = at<float>(ws, w.dq_acc_p);
+  if ((st = hip_check(launch_row_dot(dims->dtype, do_p, o_p, (int)P, nullptr, 0, (int)hq, (int)hd,
+                                     dd_p, stream), "row statistic")) != SPR_OK)
+    return st;
+  if ((st = hip_check(launch_fill_zero(dq_acc, P * hq * hd, stream), "dq clear")) != SPR_OK)
+    return st;
+  AttnArgs a = base_args(dims);
+  a.q_p = q_p; a.k_p = k_p; a.v_p = v_p; a.do_p = do_p;
+  a.lse_p = const_cast<float*>(lse_p);
+  a.dd_p = dd_p; a.dq_acc_p = dq_acc;
+  a.n_prefix_k_tiles = tiles(dims->prefix_len, block_k(dims->dtype));
+  a.prefix_rows = 1;
+  a.suffix_rows = 0;
+  a.pk_mode = kPkInject;
+  a.gk = const_cast<float*>(gk_cache); a.gv = const_cast<float*>(gv_cache);
+  a.dk_p = dk_p; a.dv_p = dv_p;
+  a.n_prefix_q_tiles = tiles(dims->prefix_len, block_q(dims->dtype));
+  if ((st = hip_check(launch_bwd(dims, a, 1, stream), "prefix backward")) != SPR_OK) return st;
+  if ((st = hip_check(launch_convert(dims->dtype, dq_acc, scale, nullptr, dq_p, P * hq * hd, stream),
+                      "dq convert")) != SPR_OK)
+    return st;
+  return ok();
+}
+
+spr_status spr_dense_recompute_baseline(
+    const spr_dims* dims, const void* q_p, const void* k_p, const void* v_p, const void* do_p_seq,
+    const void* q_s, const void* k_s, const void* v_s, const void* do_s,
+    const int32_t* cu_seqlens, int32_t n, int32_t max_len, int32_t total_len, void* o_p,
+    float* lse_p, void* o_s, float* lse_s, void* dq_s, void* dk_s, void* dv_s, void* dq_p,
+    void* dk_p, void* dv_p, void* ws, size_t ws_bytes, hipStream_t stream) {
+  spr_status st = check_dims(dims);
+  if (st != SPR_OK) return st;
+  if ((st = check_suffix_sizes(n, max_len, total_len)) != SPR_OK) return st;
+  const size_t P = dims->prefix_len, hq = dims->num_q_heads, hkv = dims->num_kv_heads,
+               hd = dims->head_dim, eb = dtype_bytes(dims->dtype), T = total_len;
+  std::vector<Buf> bufs = {{q_p, P * hq * hd * eb, "q_p", true},
+                           {k_p, P * hkv * hd * eb, "k_p", true},
+                           {v_p, P * hkv * hd * eb, "v_p", true},
+                           {do_p_seq, (size_t)n * P * hq * hd * eb, "do_p_seq", false},
+                           {q_s, T * hq * hd * eb, "q_s", true},
+                           {k_s, T * hkv * hd * eb, "k_s", true},
+                           {v_s, T * hkv * hd * eb, "v_s", true},
+                           {do_s, T * hq * hd * eb, "do_s", true},
+                           {cu_seqlens, (size_t)(n + 1) * 4, "cu_seqlens", true, 4},
+                           {o_p, P * hq * hd * eb, "o_p", true},
+                           {lse_p, hq * P * 4, "lse_p", true, 4},
+                           {o_s, T * hq * hd * eb, "o_s", true},
+                           {lse_s, hq * T * 4, "lse_s", true, 4},
+                           {dq_s, T * hq * hd * eb, "dq_s", true},
+                           {dk_s, T * hkv * hd * eb, "dk_s", true},
+                           {dv_s, T * hkv * hd * eb, "dv_s", true},
+                           {dq_p, P * hq * hd * eb, "dq_p", true},
+                           {dk_p, P * hkv * hd * eb, "dk_p", true},
+                           {dv_p, P * hkv * hd * eb, "dv_p", true}};
+  if ((st = check_bufs(bufs)) != SPR_OK) return st;
+  const WsLayout w = ws_layout(SPR_OP_DENSE_BASELINE, dims, max_len, total_len);
+  if ((st = check_ws(w, ws, ws_bytes)) != SPR_OK) return st;
+  float* dd_p = at<float>(ws, w.dd_p);
+  float* dq_acc_p = at<float>(ws, w.dq_acc_p);
+  float* dd_s = at<float>(ws, w.dd_s);
+  float* dq_acc_s = at<float>(ws, w.dq_acc_s);
+  float* dk_acc = at<float>(ws, w.dk_acc_p);
+  float* dv_acc = at<float>(ws, w.dv_acc_p);
+  const float scale = eff_scale(dims);
+  const bool have_dop = do_p_seq != nullptr;
+#define SPR_TRY(expr, what) \
+  if ((st = hip_check((expr), (what))) != SPR_OK) return st
+  SPR_TRY(launch_fill_zero(dq_acc_p, P * hq * hd, stream), "clear");
+  SPR_TRY(launch_fill_zero(dq_acc_s, T * hq * hd, stream), "clear");
+  SPR_TRY(launch_fill_zero(dk_acc, P * hkv * hd, stream), "clear");
+  SPR_TRY(launch_fill_zero(dv_acc, P * hkv * hd, stream), "clear");
+  // one trajectory at a time, as a dense trainer runs them
+  for (int32_t i = 0; i < n; ++i) {
+    AttnArgs a = base_args(dims);
+    a.q_p = q_p; a.k_p = k_p; a.v_p = v_p; a.o_p = o_p; a.lse_p = lse_p;
+    a.q_s = q_s; a.k_s = k_s; a.v_s = v_s; a.o_s = o_s; a.lse_s = lse_s;
+    a.cu = cu_seqlens;
+    a.total_len = total_len;
+    a.seq_base = i;
+    a.n_seq = 1;
+    a.n_prefix_q_tiles = tiles(dims->prefix_len, block_q(dims->dtype));
+    a.n_suffix_q_tiles = tiles(max_len, block_q(dims->dtype));
+    SPR_TRY(launch_fwd(dims, a, 1, stream), "dense forward");
+    const void* dop_i = have_dop ? (const char*)do_p_seq + (size_t)i * P * hq * hd * eb : nullptr;
+    if (have_dop && P > 0)
+      SPR_TRY(launch_row_dot(dims->dtype, dop_i, o_p, (int)P, nullptr, 0, (int)hq, (int)hd, dd_p,
+                             stream), "row statistic");
+    SPR_TRY(launch_row_dot(dims->dtype, do_s, o_s, max_len, cu_seqlens, i, (int)hq, (int)hd, dd_s,
+                           stream), "row statistic");
+    a.do_p = dop_i; a.dd_p = dd_p; a.dq_acc_p = dq_acc_p;
+    a.do_s = do_s; a.dd_s = dd_s; a.dq_acc_s = dq_acc_s;
+    a.n_prefix_k_tiles = tiles(dims->prefix_len, block_k(dims->dtype));
+    a.n_suffix_k_tiles = tiles(max_len, block_k(dims->dtype));
+    a.prefix_rows = have_dop ? 1 : 0;
+    a.suffix_rows = 1;
+    a.pk_mode = kPkAccumulate;
+    a.gk = dk_acc; a.gv = dv_acc;
+    a.dk_s = dk_s; a.dv_s = dv_s;
+    a.n_prefix_q_tiles = have_dop ? tiles(dims->prefix_len, block_q(dims->dtype)) : 0;
+    SPR_TRY(launch_bwd(dims, a, 1, stream), "dense backward");
+  }
+  SPR_TRY(launch_convert(dims->dtype, dq_acc_p, scale, nullptr, dq_p, P * hq * hd, stream), "convert");
+  SPR_TRY(launch_convert(dims->dtype, dk_acc, 1.f, nullptr, dk_p, P * hkv * hd, stream), "convert");
+  SPR_TRY(launch_convert(dims->dtype, dv_acc, 1.f, nullptr, dv_p, P * hkv * hd, stream), "convert");
+  SPR_TRY(launch_convert(dims->dtype, dq_acc_s, scale, nullptr, dq_s, T * hq * hd, stream), "convert");
+#undef SPR_TRY
+  return ok();
+}
+
+spr_status spr_gkv_cache_zero(const spr_dims* dims, float* gk_cache, float* gv_cache,
+                              hipStream_t stream) {
+  spr_status st = check_dims(dims);
+  if (st != SPR_OK) return st;
+  const size_t n = (size_t)dims->prefix_len * dims->num_kv_heads * dims->head_dim;
+  if ((st = check_bufs({{gk_cache, n * 4, "gk_cache", true}, {gv_cache, n * 4, "gv_cache", true}})) != SPR_OK)
+    return st;
+  if (n == 0) return ok();
+  if ((st = hip_check(launch_fill_zero(gk_cache, n, stream), "cache zero")) != SPR_OK) return st;
+  if ((st = hip_check(launch_fill_zero(gv_cache, n, stream), "cache zero")) != SPR_OK) return st;
+  return ok();
+}
+
+spr_status spr_gkv_accumulate(const spr_dims* dims, float* gk_cache, float* gv_cache,
+                              const float* dgk, const float* dgv, hipStream_t stream) {
+  spr_status st = check_dims(dims);
+  if (st != SPR_OK) return st;
+  const size_t n = (size_t)dims->prefix_len * dims->num_kv_heads * dims->head_dim;
+  std::vector<Buf> bufs = {{gk_cache, n * 4, "gk_cache", true}, {gv_cache, n * 4, "gv_cache", true},
+                           {dgk, n * 4, "dgk", true}, {dgv, n * 4, "dgv", true}};
+  if ((st = check_bufs(bufs)) != SPR_OK) return st;
+  if ((st = check_aliasing({bufs[0], bufs[1]}, bufs)) != SPR_OK) return st;
+  if (n == 0) return ok();
+  if ((st = hip_check(launch_accumulate(gk_cache, dgk, n, stream), "cache accumulate")) != SPR_OK)
+    return st;
+  if ((st = hip_check(launch_accumulate(gv_cache, dgv, n, stream), "cache accumulate")) != SPR_OK)
+    return st;
+  return ok();
+}
+
+spr_status spr_profile_enable(int32_t enable) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  g_prof_on = enable != 0;
+  return SPR_OK;
+}
+
+spr_status spr_profile_reset(void) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  prof_drain_locked();
+  g_prof_totals.clear();
+  g_prof_names.clear();
+  return SPR_OK;
+}
+
+spr_status spr_profile_query(const char* kernel, double* total_ms, int32_t* count) {
+  if (kernel == nullptr || total_ms == nullptr || count == nullptr)
+    return fail(SPR_ERR_INVALID_ARG, "null argument");
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  prof_drain_locked();
+  auto it = g_prof_totals.find(kernel);
+  *total_ms = it == g_prof_totals.end() ? 0.0 : it->second.first;
+  *count = it == g_prof_totals.end() ? 0 : it->second.second;
+  return SPR_OK;
+}
+
+int32_t spr_profile_num_kernels(void) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  prof_drain_locked();
+  return (int32_t)g_prof_names.size();
+}
+
+const char* spr_profile_kernel_name(int32_t index) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  if (index < 0 || index >= (int32_t)g_prof_names.size()) return "";
+  return g_prof_names[index].c_str();
+}
+
+}  // extern "C"

@@ -1,0 +1,135 @@
+"""CPU tier for the C ABI: the library loads, exports every symbol the header
+declares, and rejects bad arguments before launching anything.
+
+No call here reaches a kernel launch: each one fails validation first, and
+the fake device pointers are only compared, never dereferenced.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2606_01143_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "spr.h")
+
+
+def header_symbols():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(spr_[a-z_0-9]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(B.LIB_PATH):
+        pytest.fail("libspr.so is not built: run `python -m paper_2606_01143_amd.build`")
+    return B.lib()
+
+
+def test_every_header_symbol_is_exported_and_bound(lib):
+    syms = header_symbols()
+    assert len(syms) >= 15
+    for s in syms:
+        assert hasattr(lib, s), s
+        assert s in B._SIGNATURES, f"{s} has no Python binding"
+
+
+def test_dims_struct_matches_header():
+    text = open(HEADER).read()
+    body = re.search(r"typedef struct spr_dims \{(.*?)\} spr_dims;", text, re.S).group(1)
+    fields = re.findall(r"\b(?:int32_t|float|uint32_t)\s+(\w+);", body)
+    assert fields == [f for f, _ in B.SprDims._fields_]
+    assert ctypes.sizeof(B.SprDims) == 28
+
+
+def test_version_and_status_strings(lib):
+    assert "spr" in B.version()
+    for code, name in B.STATUS.items():
+        assert B.status_string(code) == name
+
+
+A = 0x7F0000000000  # fake, 16-byte aligned device addresses (never dereferenced)
+
+
+def _addr(i):
+    return A + i * (1 << 30)
+
+
+def _dims(**kw):
+    base = dict(num_q_heads=4, num_kv_heads=2, head_dim=128, prefix_len=64, dtype="bf16")
+    base.update(kw)
+    return B.make_dims(**base)
+
+
+def _call_prefix_fwd(dims, q=1, k=2, v=3, o=4, lse=5):
+    args = [_addr(x) if x else None for x in (q, k, v, o, lse)]
+    return B.lib().spr_prefix_fwd(ctypes.byref(dims), *args, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(head_dim=96), "SPR_ERR_UNSUPPORTED"),
+    (dict(num_q_heads=6, num_kv_heads=4), "SPR_ERR_INVALID_ARG"),
+    (dict(num_kv_heads=0), "SPR_ERR_INVALID_ARG"),
+    (dict(prefix_len=-1), "SPR_ERR_INVALID_ARG"),
+    (dict(softmax_scale=float("inf")), "SPR_ERR_INVALID_ARG"),
+])
+def test_dims_validation(lib, kw, status):
+    assert B.STATUS[_call_prefix_fwd(_dims(**kw))] == status
+    assert B.last_error()
+
+
+def test_unknown_dtype_and_flags(lib):
+    d = _dims()
+    d.dtype = 7
+    assert B.STATUS[_call_prefix_fwd(d)] == "SPR_ERR_UNSUPPORTED"
+    d = _dims()
+    d.flags = 0x80
+    assert B.STATUS[_call_prefix_fwd(d)] == "SPR_ERR_UNSUPPORTED"
+
+
+def test_null_and_misaligned_pointers(lib):
+    assert B.STATUS[_call_prefix_fwd(_dims(), q=0)] == "SPR_ERR_INVALID_ARG"
+    d = _dims()
+    r = B.lib().spr_prefix_fwd(ctypes.byref(d), _addr(1) + 8, _addr(2), _addr(3), _addr(4),
+                               _addr(5), None)
+    assert B.STATUS[r] == "SPR_ERR_MISALIGNED"
+
+
+def _bwd_accum(dims, n_mb=2, max_len=10, total=15, gk=None, ws_bytes=1 << 40, ws=100):
+    ptr = [_addr(i) for i in range(1, 14)]
+    gk_ptr = gk if gk is not None else _addr(20)
+    return B.lib().spr_suffix_attn_bwd_accum(
+        ctypes.byref(dims), ptr[0], ptr[1], ptr[2], ptr[3], ptr[4], ptr[5], ptr[6], ptr[7],
+        ptr[8], n_mb, max_len, total, ptr[9], ptr[10], ptr[11], gk_ptr, _addr(21),
+        _addr(ws) if ws else None, ws_bytes, None)
+
+
+@pytest.mark.parametrize("n_mb,max_len,total", [(0, 4, 4), (2, 0, 4), (3, 4, 2), (2, 4, 9)])
+def test_suffix_size_validation(lib, n_mb, max_len, total):
+    assert B.STATUS[_bwd_accum(_dims(), n_mb, max_len, total)] == "SPR_ERR_INVALID_ARG"
+
+
+def test_cache_aliasing_is_rejected(lib):
+    # gk_cache placed inside q_s (argument 3)
+    assert B.STATUS[_bwd_accum(_dims(), gk=_addr(3) + 256)] == "SPR_ERR_ALIASING"
+
+
+def test_workspace_checks(lib):
+    dims = _dims()
+    need = B.workspace_size(B.OP_SUFFIX_BWD, dims, 2, 10, 15)
+    assert need >= 15 * 4 * 128 * 4
+    assert B.STATUS[_bwd_accum(dims, ws_bytes=need - 1)] == "SPR_ERR_WORKSPACE"
+    assert B.STATUS[_bwd_accum(dims, ws=0)] == "SPR_ERR_WORKSPACE"
+
+
+def test_workspace_sizes_are_consistent(lib):
+    dims = _dims(prefix_len=4096, num_q_heads=32, num_kv_heads=8)
+    assert B.workspace_size(B.OP_PREFIX_FWD, dims) == 0
+    assert B.workspace_size(B.OP_PREFIX_BWD, dims) >= 4096 * 32 * 128 * 4
+    dense = B.workspace_size(B.OP_DENSE_BASELINE, dims, 8, 512, 4096)
+    assert dense >= 4096 * 32 * 128 * 4 * 2 + 4096 * 8 * 128 * 4 * 2
+    with pytest.raises(B.SprError):
+        B.workspace_size(99, dims)

@@ -1,0 +1,193 @@
+"""GPU parity: every libspr entry point against the fp64 oracle.
+
+The schedule (prefix_fwd, suffix_attn_fwd, suffix_attn_bwd_accum,
+prefix_bwd) is compared with the oracle's three-phase reference fed the same
+G_Y; the dense-recompute baseline with the oracle's dense definition.  Gates
+(max-abs-relative per tensor): 1e-4 for fp32 storage, 2e-2 for bf16.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import dense_group_reference, three_phase_reference, max_abs_rel, paper_pass_fraction
+from synthetic import GroupShape, make_group
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+SCHED_KEYS = ["o_p", "lse_p", "o_s", "lse_s", "dq_p", "dk_p", "dv_p", "dq_s", "dk_s", "dv_s",
+              "g_k", "g_v"]
+DENSE_KEYS = ["o_p", "lse_p", "o_s", "lse_s", "dq_p", "dk_p", "dv_p", "dq_s", "dk_s", "dv_s"]
+
+
+def _announce(msg):
+    sys.stderr.write(f"\n[gpu-case] {msg}\n")
+    sys.stderr.flush()
+
+
+# A reference tensor can be identically zero (P = 1: the lone prefix row's
+# softmax is one-hot, so dS_11 = 0 and dQ_P = 0); its error is then measured
+# against an absolute scale floor.  Inputs are N(0,1), so every non-degenerate
+# tensor's scale is far above the floor.
+SCALE_FLOOR = 1e-3
+
+
+def _errors(gpu, ref, keys):
+    errs = {}
+    for k in keys:
+        r = ref[k]
+        if k.startswith("lse"):
+            r = r.T  # oracle LSE is [Hq, T]; the library's is [T, Hq]
+        errs[k] = max_abs_rel(gpu[k], r, floor=SCALE_FLOOR)
+    return errs
+
+
+def _assert_close(gpu, ref, keys, tol, what):
+    errs = _errors(gpu, ref, keys)
+    bad = {k: v for k, v in errs.items() if not v <= tol}
+    assert not bad, f"{what}: {bad} (all: {errs})"
+    return errs
+
+
+def _group(shape, seed, **kw):
+    from paper_2606_01143_amd.group import DeviceGroup
+    inp = make_group(shape, seed=seed)
+    return inp, DeviceGroup(inp, **kw)
+
+
+SHAPES = [
+    # the tiny fp32 group: 2/2 heads, d=64, P=128, N=4 x 32
+    ("tiny_f32", GroupShape(2, 2, 64, 128, (32,) * 4, "f32")),
+    ("f32_gqa_d128_ragged", GroupShape(4, 2, 128, 75, (33, 70, 5), "f32")),
+    ("f32_d64_p0", GroupShape(4, 4, 64, 0, (50, 17), "f32")),
+    ("bf16_gqa4_d128_ragged", GroupShape(8, 2, 128, 200, (70, 129, 33), "bf16")),
+    ("bf16_gqa8_d128", GroupShape(8, 1, 128, 300, (64, 1, 150), "bf16")),
+    ("bf16_d64", GroupShape(4, 2, 64, 130, (65, 63, 128), "bf16")),
+    ("bf16_p0", GroupShape(4, 2, 128, 0, (90, 40), "bf16")),
+    ("bf16_n1", GroupShape(4, 1, 128, 257, (100,), "bf16")),
+    ("bf16_p1_s1", GroupShape(2, 1, 128, 1, (1, 2), "bf16")),
+]
+
+
+@pytest.mark.parametrize("name,shape", SHAPES, ids=[s[0] for s in SHAPES])
+def test_schedule_matches_oracle(gpu, name, shape):
+    _announce(f"schedule {name} {shape}")
+    inp, grp = _group(shape, seed=0)
+    grp.run_schedule()
+    got = grp.fetch("schedule")
+    ref = three_phase_reference(inp)
+    _assert_close(got, ref, SCHED_KEYS, TOL[shape.dtype], f"schedule {name}")
+
+
+@pytest.mark.parametrize("name,shape", SHAPES, ids=[s[0] for s in SHAPES])
+def test_dense_baseline_matches_oracle(gpu, name, shape):
+    _announce(f"dense {name} {shape}")
+    inp, grp = _group(shape, seed=1)
+    grp.run_dense()
+    got = grp.fetch("dense")
+    ref = dense_group_reference(inp)
+    _assert_close(got, ref, DENSE_KEYS, TOL[shape.dtype], f"dense {name}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_suffix_only_loss_exact_cache_injection(gpu, dtype):
+    """G_Y = NULL: dQ_P = 0 exactly and dK_P/dV_P are the cache rounded once."""
+    import torch
+    shape = GroupShape(4, 2, 128 if dtype == "bf16" else 64, 96, (40, 77), dtype)
+    _announce(f"suffix-only {shape}")
+    inp, grp = _group(shape, seed=2)
+    grp.run_schedule(use_gy=False)
+    out = grp.out
+    assert torch.count_nonzero(out["dq_p"]).item() == 0
+    assert torch.equal(out["dk_p"], grp.gk.to(out["dk_p"].dtype))
+    assert torch.equal(out["dv_p"], grp.gv.to(out["dv_p"].dtype))
+    ref = three_phase_reference(inp, g_y=np.zeros_like(inp["g_y"]))
+    _assert_close(grp.fetch("schedule"), ref, SCHED_KEYS, TOL[dtype], "suffix-only")
+
+
+def test_cache_is_bitwise_reproducible(gpu):
+    import torch
+    shape = GroupShape(8, 2, 128, 256, (100, 60, 128), "bf16")
+    _announce(f"determinism {shape}")
+    inp, grp = _group(shape, seed=3)
+    grp.run_schedule()
+    gk1, gv1 = grp.gk.clone(), grp.gv.clone()
+    dk1, dv1 = grp.out["dk_s"].clone(), grp.out["dv_s"].clone()
+    for _ in range(2):
+        grp.run_schedule()
+        assert torch.equal(grp.gk, gk1) and torch.equal(grp.gv, gv1)
+        assert torch.equal(grp.out["dk_s"], dk1) and torch.equal(grp.out["dv_s"], dv1)
+
+
+def test_microbatch_split_and_order_invariance(gpu):
+    """Any split of the suffixes into packed microbatches, in any order, gives
+    the same group gradients (paper Sec. 4.2; Prop. 1)."""
+    shape = GroupShape(8, 2, 128, 192, (70, 20, 129, 64), "bf16")
+    _announce(f"microbatch splits {shape}")
+    splits = [[(0, 1), (1, 2), (2, 3), (3, 4)], [(0, 4)], [(2, 4), (0, 2)],
+              [(3, 4), (1, 3), (0, 1)]]
+    inp, grp = _group(shape, seed=4, microbatch_splits=splits)
+    ref = three_phase_reference(inp)
+    base = None
+    for mbs in splits:
+        grp.run_schedule(microbatches=mbs)
+        got = grp.fetch("schedule")
+        _assert_close(got, ref, SCHED_KEYS, TOL["bf16"], f"split {mbs}")
+        if base is None:
+            base = got
+        else:
+            errs = {k: max_abs_rel(got[k], base[k]) for k in SCHED_KEYS}
+            assert max(errs.values()) <= 1e-2, errs
+
+
+def test_schedule_equals_dense_baseline_on_gpu(gpu):
+    shape = GroupShape(8, 2, 128, 320, (128, 96, 200), "bf16")
+    _announce(f"schedule vs dense {shape}")
+    inp, grp = _group(shape, seed=5)
+    grp.run_schedule()
+    grp.run_dense()
+    s, d = grp.fetch("schedule"), grp.fetch("dense")
+    errs = {k: max_abs_rel(s[k], d[k]) for k in DENSE_KEYS}
+    assert max(errs.values()) <= TOL["bf16"], errs
+    # The paper's element-wise BF16 rule (Sec. 5.2) was set for parameters
+    # after an optimizer step; on raw bf16 gradient tensors it is reported,
+    # with only a loose sanity bound.
+    fracs = {k: paper_pass_fraction(s[k], d[k]) for k in DENSE_KEYS}
+    _announce(f"paper element-wise rule pass fractions: {fracs}")
+    assert min(fracs.values()) >= 0.9, fracs
+
+
+def _head_subset(inp, kv):
+    """Inputs of one kv head and its G query heads (heads are independent)."""
+    shp = inp["shape"]
+    g = shp.group
+    qh = slice(kv * g, (kv + 1) * g)
+    sub = dict(inp)
+    for k in ("q_p", "q_s", "do_s", "g_y"):
+        sub[k] = inp[k][:, qh]
+    sub["do_p"] = inp["do_p"][:, :, qh]
+    for k in ("k_p", "v_p", "k_s", "v_s"):
+        sub[k] = inp[k][:, kv:kv + 1]
+    sub["shape"] = GroupShape(g, 1, shp.head_dim, shp.prefix_len, shp.suffix_lens, shp.dtype)
+    return sub, qh
+
+
+@pytest.mark.parametrize("kv", [0, 5])
+def test_llama3_8b_full_size_on_one_kv_group(gpu, kv):
+    """Llama3-8B attention at full size (GQA 32/8, d=128, P=4096, N=8 x 512),
+    checked against the oracle on one kv head and its 4 q heads."""
+    from synthetic import NAMED_SHAPES
+    shape = NAMED_SHAPES["llama3_8b_p4096_n8_s512"]
+    _announce(f"full-size llama3 kv={kv}")
+    inp, grp = _group(shape, seed=0)
+    grp.run_schedule()
+    got = grp.fetch("schedule")
+    sub, qh = _head_subset(inp, kv)
+    ref = three_phase_reference(sub)
+    q_keys = ["o_p", "o_s", "dq_p", "dq_s"]
+    kv_keys = ["dk_p", "dv_p", "dk_s", "dv_s", "g_k", "g_v"]
+    sel = {k: got[k][:, qh] for k in q_keys}
+    sel.update({k: got[k][:, qh] for k in ("lse_p", "lse_s")})
+    sel.update({k: got[k][:, kv:kv + 1] for k in kv_keys})
+    _assert_close(sel, ref, SCHED_KEYS, TOL["bf16"], f"llama3 full kv={kv}")

@@ -211,11 +211,13 @@ spr_status spr_gkv_accumulate(const spr_dims* dims, float* gk_cache, float* gv_c
                               const float* dgk, const float* dgv, hipStream_t stream);
 
 /* Per-kernel GPU timing with HIP events, off by default.  While enabled,
- * every kernel the library launches is bracketed by two events on its
- * stream.  spr_profile_query waits for the recorded events and returns the
- * summed milliseconds and launch count of the kernels whose name equals
- * `kernel` (names as printed by spr_profile_kernel_name). */
-spr_status spr_profile_enable(int32_t enable);
+ * every kernel the library launches (or, when only_kernel is not NULL, every
+ * launch of that kernel only) is bracketed by two events on its stream.
+ * spr_profile_query waits for the recorded events and returns the summed
+ * milliseconds and launch count of the kernels whose name equals `kernel`
+ * (names as listed by spr_profile_kernel_name).  Not thread-safe against
+ * concurrent enable/reset; recording itself is. */
+spr_status spr_profile_enable(int32_t enable, const char* only_kernel);
 spr_status spr_profile_reset(void);
 spr_status spr_profile_query(const char* kernel, double* total_ms, int32_t* count);
 int32_t spr_profile_num_kernels(void);

@@ -44,7 +44,7 @@ _SIGNATURES = {
     "spr_workspace_size": ([c_int32, _P, c_int32, c_int32, c_int32, POINTER(c_size_t)], c_int32),
     "spr_gkv_cache_zero": ([_P, _P, _P, _P], c_int32),
     "spr_gkv_accumulate": ([_P, _P, _P, _P, _P, _P], c_int32),
-    "spr_profile_enable": ([c_int32], c_int32),
+    "spr_profile_enable": ([c_int32, c_char_p], c_int32),
     "spr_profile_reset": ([], c_int32),
     "spr_profile_query": ([c_char_p, POINTER(c_double), POINTER(c_int32)], c_int32),
     "spr_profile_num_kernels": ([], c_int32),
@@ -184,8 +184,9 @@ def gkv_accumulate(dims, gk_cache, gv_cache, dgk, dgv, stream=None):
                                     _ptr(dgv), _stream(stream)))
 
 
-def profile_enable(on: bool = True):
-    _check(lib().spr_profile_enable(1 if on else 0))
+def profile_enable(on: bool = True, only_kernel: str = None):
+    _check(lib().spr_profile_enable(1 if on else 0,
+                                    only_kernel.encode() if only_kernel else None))
 
 
 def profile_reset():

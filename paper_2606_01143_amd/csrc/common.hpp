@@ -47,6 +47,12 @@ struct AttnArgs {
   const void* do_s;
   float* dd_s;         // [total_len, Hq]
   float* dq_acc_s;     // [total_len, Hq, d]
+  // bf16 backward: dQ is written once, scaled, in the storage dtype; the
+  // dense baseline accumulates the prefix rows' dQ over the trajectories in
+  // dq_acc_p (unscaled) instead
+  void* dq_p;
+  void* dq_s;
+  int32_t dq_p_accumulate;
   const int32_t* cu;   // device cu_seqlens
   int32_t P;
   int32_t total_len;

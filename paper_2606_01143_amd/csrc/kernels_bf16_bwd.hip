@@ -2,64 +2,65 @@
 // with gradient-cache accumulation, Phase C prefix backward with cache
 // injection, and the dense baseline's backward.
 //
-// What it computes (paper App. A.2-A.5), per key tile and kv head, over every
-// query row that sees the tile (all G q heads of the kv head):
-//   P  = exp(S - LSE),  dP = dO V^T,  dS = P * (dP - rowsum(dO * O))
-//   dV += P^T dO,  dK += dS^T Q / sqrt(d),  dQ += dS K / sqrt(d)
-// For a prefix key tile in Phase B the rows are every suffix row of the
-// microbatch, and the tile's dK/dV are exactly gK_1 = dS_21^T Q_2 / sqrt(d)
-// and gV_1 = P_21^T dO_2; the workgroup adds them into the fp32 cache
-// G_K/G_V with a plain read-modify-write.  Each (prefix tile, kv head) is
-// owned by exactly one workgroup of one launch, so no atomics are needed and
-// the cache is bitwise reproducible.  In Phase C the same epilogue writes
-// dK_1 = local + G_K and dV_1 = local + G_V instead.
+// What it computes (paper App. A.2-A.5): with P = exp(S - LSE),
+// dP = dO V^T and dS = P * (dP - rowsum(dO * O)) over the joint row,
+//   dV = P^T dO,  dK = dS^T Q / sqrt(d),  dQ = dS K / sqrt(d).
+// Two kernels split the work so that no gradient needs atomics:
 //
-// Structure: one workgroup = 4 waves = one 64-key tile; wave w owns keys
-// 16 w .. 16 w + 15 and keeps their K/V fragments and dK/dV accumulators in
-// registers.  Query rows stream through LDS in tiles of 64 (natural layout).
-// Per row tile and wave (16 keys x 64 rows):
-//   S  = Q K^T, dP = dO V^T      A = Q/dO rows (LDS), B = K/V (registers)
-//   dV += P^T dO, dK += dS^T Q   A = P^T/dS^T straight from the S/dP
-//                                registers, B = dO/Q columns via LDS
-//                                transpose reads
-//   dS^T -> LDS; dQ = dS K       A = dS via transpose reads, B = K columns
-//                                (registers); each wave owns d/4 columns and
-//                                adds its 64 x d/4 block into an fp32 dQ
-//                                accumulator with float atomics.
+// bwd_kv (key-outer): one workgroup owns a 128-key tile of one kv head and
+//   sweeps every query row that sees it, for all G q heads of the kv head.
+//   For a prefix key tile in Phase B the rows are all suffix rows of the
+//   microbatch, so the tile's dK/dV are exactly gK_1 = dS_21^T Q_2 / sqrt(d)
+//   and gV_1 = P_21^T dO_2; the workgroup adds them into the fp32 cache
+//   G_K/G_V with a plain read-modify-write.  Each (prefix tile, kv head)
+//   belongs to exactly one workgroup of a launch, so the cache update is
+//   deterministic.  In Phase C the epilogue writes dK_1 = local + G_K and
+//   dV_1 = local + G_V instead.  Per 64-row tile and wave (32 keys):
+//     S  = Q K^T, dP = dO V^T     A = Q/dO rows (natural tiles), B = K/V (registers)
+//     dV += P^T dO, dK += dS^T Q  A = P^T/dS^T from the S/dP registers,
+//                                 B = dO/Q columns (transposed tiles)
+// bwd_q (query-outer): one workgroup owns 128 query rows of one q head and
+//   sweeps their visible key tiles, recomputing S and dP:
+//     S^T = K Q^T, dP^T = V dO^T  A = K/V rows (natural tiles), B = Q/dO (registers)
+//     dQ^T += K^T dS^T            A = K columns (transposed tile), B = dS^T registers
+//   and writes dQ once, already scaled and rounded.
+// Both stream their tiles through double-buffered LDS with the next tile's
+// global loads in flight during the current tile's products.
 #include "common.hpp"
 #include "launch.hpp"
-#include "mfma.hpp"
+#include "tile.hpp"
 
 namespace spr {
 
 namespace {
-constexpr int kBwdBK = 64;
-constexpr int kBwdBQ = 64;
+constexpr int kKvBK = 128;  // keys per bwd_kv workgroup (32 per wave)
+constexpr int kKvBQ = 64;   // rows per streamed tile
+constexpr int kQBQ = 128;   // rows per bwd_q workgroup (32 per wave)
+constexpr int kQBK = 64;    // keys per streamed tile
 constexpr int kBwdThreads = 256;
 }  // namespace
 
-int bwd_bf16_block_k() { return kBwdBK; }
+int bwd_bf16_block_k() { return kKvBK; }
 
+// ---------------------------------------------------------------- bwd_kv
 template <int D>
-__global__ __launch_bounds__(kBwdThreads) void bwd_bf16_kernel(AttnArgs a) {
-  constexpr int BK = kBwdBK, BQ = kBwdBQ;
-  constexpr int NS = D / 32;     // k-steps over d for S and dP
-  constexpr int NDB = D / 16;    // d blocks of dK/dV
-  constexpr int NQB = BQ / 16;   // row blocks of a row tile
-  constexpr int RS = D + 16;     // Q/dO tile row stride (transpose reads conflict-free)
-  constexpr int SS = BQ + 16;    // dS^T tile row stride
-  constexpr int DQW = D / 4;     // dQ columns owned by one wave
-  constexpr int NQN = DQW / 16;
-  __shared__ __attribute__((aligned(16))) bf16 Qs[BQ * RS];
-  __shared__ __attribute__((aligned(16))) bf16 dOs[BQ * RS];
-  __shared__ __attribute__((aligned(16))) bf16 dSt[BK * SS];
-  __shared__ float Ls[BQ], Dd[BQ];
+__global__ __launch_bounds__(kBwdThreads) void bwd_kv_bf16_kernel(AttnArgs a) {
+  using TG = TileGeom<D>;
+  constexpr int BK = kKvBK, BQ = kKvBQ;
+  constexpr int NS = D / 16;
+  constexpr int NDB = D / 32;
+  __shared__ __attribute__((aligned(16))) bf16 Qn[2][TG::NAT];
+  __shared__ __attribute__((aligned(16))) bf16 On[2][TG::NAT];  // dO, natural
+  __shared__ __attribute__((aligned(16))) bf16 Qt[2][TG::TRN];
+  __shared__ __attribute__((aligned(16))) bf16 Ot[2][TG::TRN];  // dO, transposed
+  __shared__ __attribute__((aligned(16))) float Ls[2][BQ];
+  __shared__ __attribute__((aligned(16))) float Dd[2][BQ];
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int c = lane & 15, g = lane >> 4;
+  const int r = lane & 31, h = lane >> 5;
   const int hk = blockIdx.y, G = a.hq / a.hkv;
 
-  // ---- which 64 keys: a prefix tile, or a tile of suffix s
+  // ---- which 128 keys: a prefix tile, or a tile of suffix s
   const int x = blockIdx.x;
   bool kpre;
   int k0, kseg, kbase;
@@ -77,206 +78,375 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_bf16_kernel(AttnArgs a) {
     kpre = false;
   }
   if (k0 >= kseg) return;
-  const bf16* kglob = (const bf16*)(kpre ? a.k_p : a.k_s);
-  const bf16* vglob = (const bf16*)(kpre ? a.v_p : a.v_s);
-  const int my_key = k0 + 16 * w + c;  // segment-local key of this lane's S/dP column
+  const int my_key = k0 + 32 * w + r;  // segment-local key of this lane's S/dP column
   const bool kvalid = my_key < kseg;
 
   // K, V as the B operand of S = Q K^T and dP = dO V^T
   bf16x8 kf[NS], vf[NS];
   {
-    const size_t off = ((size_t)(kbase + (kvalid ? my_key : k0)) * a.hkv + hk) * D + 8 * g;
+    const bf16* kg = (const bf16*)(kpre ? a.k_p : a.k_s);
+    const bf16* vg = (const bf16*)(kpre ? a.v_p : a.v_s);
+    const size_t off = ((size_t)(kbase + (kvalid ? my_key : k0)) * a.hkv + hk) * D + 8 * h;
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      kf[s] = kvalid ? *(const bf16x8*)(kglob + off + 32 * s) : zero8();
-      vf[s] = kvalid ? *(const bf16x8*)(vglob + off + 32 * s) : zero8();
+      kf[s] = kvalid ? *(const bf16x8*)(kg + off + 16 * s) : zero_bf8();
+      vf[s] = kvalid ? *(const bf16x8*)(vg + off + 16 * s) : zero_bf8();
     }
   }
-  // K as the B operand of dQ = dS K (slot (g, j) of k-step t holds key
-  // 32 t + 4 g + j or 32 t + 16 + 4 g + j - 4; n = this wave's columns):
-  // stage the tile in LDS once and read its columns with transpose reads.
-  bf16x8 ktf[BK / 32][NQN];
-  for (int i = tid; i < BK * (D / 8); i += kBwdThreads) {
-    const int r = i / (D / 8), cc = (i % (D / 8)) * 8;
-    bf16x8 kv = zero8();
-    if (k0 + r < kseg) kv = *(const bf16x8*)(kglob + ((size_t)(kbase + k0 + r) * a.hkv + hk) * D + cc);
-    *(bf16x8*)(Qs + r * RS + cc) = kv;
+  f32x16 dk[NDB], dv[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) {
+    dk[db] = zero16();
+    dv[db] = zero16();
+  }
+
+  // ---- the row tiles this key tile sees, per q head of the group:
+  // prefix key tile: prefix rows from k0 on (causal) and/or every suffix row
+  // of suffixes seq_base .. seq_base + n_seq - 1 (all visible);
+  // suffix key tile: the suffix's own rows from k0 on (causal).
+  int n_pr = 0, n_sr = 0, sr0 = 0, sr1 = 0;
+  if (kpre) {
+    if (a.prefix_rows) n_pr = (a.P - k0 + BQ - 1) / BQ;
+    if (a.suffix_rows) {
+      sr0 = a.cu[a.seq_base];
+      sr1 = a.cu[a.seq_base + a.n_seq];
+      n_sr = (sr1 - sr0 + BQ - 1) / BQ;
+    }
+  } else {
+    n_sr = (kseg - k0 + BQ - 1) / BQ;
+  }
+  const int per_head = n_pr + n_sr;
+  const int ntiles = G * per_head;
+  struct RowTile {
+    int hh, row0, nr, lp_first;
+    bool prefix, causal;
+  };
+  auto tile_info = [&](int t) {
+    RowTile rt;
+    rt.hh = hk * G + t / per_head;
+    const int j = t % per_head;
+    if (j < n_pr) {
+      rt.prefix = true;
+      rt.causal = true;
+      rt.lp_first = k0 + j * BQ;
+      rt.row0 = rt.lp_first;
+      rt.nr = min(BQ, a.P - rt.lp_first);
+    } else if (kpre) {
+      rt.prefix = false;
+      rt.causal = false;
+      rt.lp_first = 0;
+      rt.row0 = sr0 + (j - n_pr) * BQ;
+      rt.nr = min(BQ, sr1 - rt.row0);
+    } else {
+      rt.prefix = false;
+      rt.causal = true;
+      rt.lp_first = k0 + j * BQ;
+      rt.row0 = kbase + rt.lp_first;
+      rt.nr = min(BQ, kseg - rt.lp_first);
+    }
+    return rt;
+  };
+  Stager<D> sq, so;
+  float lreg = 0.f, dreg = 0.f;
+  auto stage_load = [&](int t) {
+    const RowTile rt = tile_info(t);
+    const bf16* qg = (const bf16*)(rt.prefix ? a.q_p : a.q_s);
+    const bf16* dg = (const bf16*)(rt.prefix ? a.do_p : a.do_s);
+    sq.load(qg, rt.row0, rt.nr, a.hq, rt.hh, tid);
+    so.load(dg, rt.row0, rt.nr, a.hq, rt.hh, tid);
+    if (tid < BQ) {
+      const float* lg = rt.prefix ? a.lse_p : a.lse_s;
+      const float* ddg = rt.prefix ? a.dd_p : a.dd_s;
+      const bool v = tid < rt.nr;
+      lreg = v ? lg[(size_t)(rt.row0 + tid) * a.hq + rt.hh] * kLog2e : INFINITY;
+      dreg = v ? ddg[(size_t)(rt.row0 + tid) * a.hq + rt.hh] : 0.f;
+    }
+  };
+  auto stage_store = [&](int buf) {
+    sq.store_nat(Qn[buf], tid);
+    sq.store_trn(Qt[buf], tid);
+    so.store_nat(On[buf], tid);
+    so.store_trn(Ot[buf], tid);
+    if (tid < BQ) {
+      Ls[buf][tid] = lreg;
+      Dd[buf][tid] = dreg;
+    }
+  };
+  if (ntiles > 0) {
+    stage_load(0);
+    stage_store(0);
   }
   __syncthreads();
-#pragma unroll
-  for (int t = 0; t < BK / 32; ++t)
-#pragma unroll
-    for (int nb = 0; nb < NQN; ++nb)
-      ktf[t][nb] = join(lds_col4(Qs, RS, 32 * t + 4 * g, w * DQW + 16 * nb, c),
-                        lds_col4(Qs, RS, 32 * t + 16 + 4 * g, w * DQW + 16 * nb, c));
 
-  f32x4 dk[NDB], dv[NDB];
+  for (int t = 0; t < ntiles; ++t) {
+    const int buf = t & 1;
+    if (t + 1 < ntiles) stage_load(t + 1);
+    const RowTile rt = tile_info(t);
+    // S = Q K^T and dP = dO V^T for the two 32-row blocks of the tile:
+    // acc[rb][i] is row 32 rb + 8 (i/4) + 4 h + i%4 of the tile, key my_key
+    f32x16 sacc[2], pacc[2];
 #pragma unroll
-  for (int nb = 0; nb < NDB; ++nb) {
-    dk[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-    dv[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
-
-  // One tile of up to 64 query rows of head hh: memory rows row0 .. row0+nr-1
-  // whose segment-local index is lp_first + r.  `causal`: the rows are in the
-  // key tile's own segment, so row r sees key j only if j <= lp_first + r.
-  auto row_tile = [&](int hh, bool rows_prefix, int row0, int nr, bool causal, int lp_first) {
-    const bf16* qg = (const bf16*)(rows_prefix ? a.q_p : a.q_s);
-    const bf16* dg = (const bf16*)(rows_prefix ? a.do_p : a.do_s);
-    const float* lg = rows_prefix ? a.lse_p : a.lse_s;
-    const float* ddg = rows_prefix ? a.dd_p : a.dd_s;
-    float* dqacc = rows_prefix ? a.dq_acc_p : a.dq_acc_s;
-    __syncthreads();  // LDS tiles of the previous row tile are consumed
-    for (int i = tid; i < BQ * (D / 8); i += kBwdThreads) {
-      const int r = i / (D / 8), cc = (i % (D / 8)) * 8;
-      bf16x8 qv = zero8(), dv8 = zero8();
-      if (r < nr) {
-        const size_t off = ((size_t)(row0 + r) * a.hq + hh) * D + cc;
-        qv = *(const bf16x8*)(qg + off);
-        dv8 = *(const bf16x8*)(dg + off);
-      }
-      *(bf16x8*)(Qs + r * RS + cc) = qv;
-      *(bf16x8*)(dOs + r * RS + cc) = dv8;
-    }
-    if (tid < BQ) {
-      const bool v = tid < nr;
-      Ls[tid] = v ? lg[(size_t)(row0 + tid) * a.hq + hh] * kLog2e : INFINITY;
-      Dd[tid] = v ? ddg[(size_t)(row0 + tid) * a.hq + hh] : 0.f;
-    }
-    __syncthreads();
-
-    // S = Q K^T and dP = dO V^T: acc[qb][i] is row 16 qb + 4 g + i, key my_key
-    f32x4 sacc[NQB], pacc[NQB];
-#pragma unroll
-    for (int qb = 0; qb < NQB; ++qb) {
-      sacc[qb] = f32x4{0.f, 0.f, 0.f, 0.f};
-      pacc[qb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int rb = 0; rb < 2; ++rb) {
+      sacc[rb] = zero16();
+      pacc[rb] = zero16();
 #pragma unroll
       for (int s = 0; s < NS; ++s) {
-        const bf16x8 qa = *(const bf16x8*)(Qs + (16 * qb + c) * RS + 32 * s + 8 * g);
-        const bf16x8 da = *(const bf16x8*)(dOs + (16 * qb + c) * RS + 32 * s + 8 * g);
-        sacc[qb] = mfma16x16x32(qa, kf[s], sacc[qb]);
-        pacc[qb] = mfma16x16x32(da, vf[s], pacc[qb]);
+        sacc[rb] = mfma32(nat_frag<D>(Qn[buf], 32 * rb + r, 16 * s, h), kf[s], sacc[rb]);
+        pacc[rb] = mfma32(nat_frag<D>(On[buf], 32 * rb + r, 16 * s, h), vf[s], pacc[rb]);
       }
     }
     // P and dS (softmax backward of the joint row)
 #pragma unroll
-    for (int qb = 0; qb < NQB; ++qb)
+    for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int q = 16 * qb + 4 * g + i;
-        const bool vis = kvalid && q < nr && (!causal || my_key <= lp_first + q);
-        const float p = vis ? exp2f(sacc[qb][i] * a.scale_log2 - Ls[q]) : 0.f;
-        sacc[qb][i] = p;
-        pacc[qb][i] = p * (pacc[qb][i] - Dd[q]);
-      }
-    // dV += P^T dO ; dK += dS^T Q  (k = rows, slots as for the keys of dQ)
+      for (int g4 = 0; g4 < 4; ++g4) {
+        const int q0 = 32 * rb + 8 * g4 + 4 * h;
+        const float4 lv = *(const float4*)(&Ls[buf][q0]);
+        const float4 dd = *(const float4*)(&Dd[buf][q0]);
+        const float lq[4] = {lv.x, lv.y, lv.z, lv.w};
+        const float dq[4] = {dd.x, dd.y, dd.z, dd.w};
 #pragma unroll
-    for (int t = 0; t < NQB / 2; ++t) {
-      const bf16x8 pa = pack8(sacc[2 * t], sacc[2 * t + 1]);
-      const bf16x8 sa = pack8(pacc[2 * t], pacc[2 * t + 1]);
-#pragma unroll
-      for (int nb = 0; nb < NDB; ++nb) {
-        const bf16x8 dob = join(lds_col4(dOs, RS, 32 * t + 4 * g, 16 * nb, c),
-                                lds_col4(dOs, RS, 32 * t + 16 + 4 * g, 16 * nb, c));
-        dv[nb] = mfma16x16x32(pa, dob, dv[nb]);
-        const bf16x8 qbv = join(lds_col4(Qs, RS, 32 * t + 4 * g, 16 * nb, c),
-                                lds_col4(Qs, RS, 32 * t + 16 + 4 * g, 16 * nb, c));
-        dk[nb] = mfma16x16x32(sa, qbv, dk[nb]);
-      }
-    }
-    // dS^T[key 16 w + c][rows 16 qb + 4 g .. +3]
-#pragma unroll
-    for (int qb = 0; qb < NQB; ++qb) {
-      const bf16x4 v = {f2bf(pacc[qb][0]), f2bf(pacc[qb][1]), f2bf(pacc[qb][2]), f2bf(pacc[qb][3])};
-      *(bf16x4*)(dSt + (16 * w + c) * SS + 16 * qb + 4 * g) = v;
-    }
-    __syncthreads();
-    // dQ[rows][this wave's columns] += dS K
-#pragma unroll
-    for (int qb = 0; qb < NQB; ++qb) {
-      f32x4 acc[NQN];
-#pragma unroll
-      for (int nb = 0; nb < NQN; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int t = 0; t < BK / 32; ++t) {
-        const bf16x8 sa = join(lds_col4(dSt, SS, 32 * t + 4 * g, 16 * qb, c),
-                               lds_col4(dSt, SS, 32 * t + 16 + 4 * g, 16 * qb, c));
-#pragma unroll
-        for (int nb = 0; nb < NQN; ++nb) acc[nb] = mfma16x16x32(sa, ktf[t][nb], acc[nb]);
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int q = 16 * qb + 4 * g + i;
-        if (q < nr) {
-          float* dst = dqacc + ((size_t)(row0 + q) * a.hq + hh) * D + w * DQW + c;
-#pragma unroll
-          for (int nb = 0; nb < NQN; ++nb) unsafeAtomicAdd(dst + 16 * nb, acc[nb][i]);
+        for (int b = 0; b < 4; ++b) {
+          const int i = 4 * g4 + b, q = q0 + b;
+          const bool vis = kvalid && q < rt.nr && (!rt.causal || my_key <= rt.lp_first + q);
+          const float p = vis ? exp2f(sacc[rb][i] * a.scale_log2 - lq[b]) : 0.f;
+          sacc[rb][i] = p;
+          pacc[rb][i] = p * (pacc[rb][i] - dq[b]);
         }
       }
-    }
-  };
-
-  for (int hh = hk * G; hh < hk * G + G; ++hh) {
-    if (kpre) {
-      if (a.prefix_rows)
-        for (int rt = k0; rt < a.P; rt += BQ) row_tile(hh, true, rt, min(BQ, a.P - rt), true, rt);
-      if (a.suffix_rows) {
-        const int r0 = a.cu[a.seq_base], r1 = a.cu[a.seq_base + a.n_seq];
-        for (int rt = r0; rt < r1; rt += BQ) row_tile(hh, false, rt, min(BQ, r1 - rt), false, 0);
+    // dV += P^T dO ; dK += dS^T Q over 16-row steps u: rows 16 u + 4 h + 0..3
+    // (chunk 4 u + h) and 16 u + 8 + 4 h + 0..3 (chunk 4 u + 2 + h)
+#pragma unroll
+    for (int u = 0; u < BQ / 16; ++u) {
+      const bf16x8 pa = c_to_kfrag(sacc[u >> 1], u & 1);
+      const bf16x8 sa = c_to_kfrag(pacc[u >> 1], u & 1);
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        dv[db] = mfma32(pa, trn_frag(Ot[buf], 32 * db + r, 4 * u + h, 4 * u + 2 + h), dv[db]);
+        dk[db] = mfma32(sa, trn_frag(Qt[buf], 32 * db + r, 4 * u + h, 4 * u + 2 + h), dk[db]);
       }
-    } else {
-      for (int lr = k0; lr < kseg; lr += BQ)
-        row_tile(hh, false, kbase + lr, min(BQ, kseg - lr), true, lr);
     }
+    if (t + 1 < ntiles) stage_store(buf ^ 1);
+    __syncthreads();
   }
 
-  // ---- epilogue: dk[nb][i] / dv[nb][i] belong to key 16 w + 4 g + i, d = 16 nb + c
+  // ---- epilogue: dk[db][i] is key 32 w + 8 (i/4) + 4 h + i%4, d = 32 db + r
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int key = k0 + 16 * w + 4 * g + i;
+  for (int i = 0; i < 16; ++i) {
+    const int key = k0 + 32 * w + 8 * (i >> 2) + 4 * h + (i & 3);
     if (key >= kseg) continue;
     if (kpre) {
-      const size_t off = ((size_t)key * a.hkv + hk) * D + c;
+      const size_t off = ((size_t)key * a.hkv + hk) * D + r;
       if (a.pk_mode == kPkAccumulate) {
 #pragma unroll
-        for (int nb = 0; nb < NDB; ++nb) {
-          a.gk[off + 16 * nb] += dk[nb][i] * a.scale;
-          a.gv[off + 16 * nb] += dv[nb][i];
+        for (int db = 0; db < NDB; ++db) {
+          a.gk[off + 32 * db] += dk[db][i] * a.scale;
+          a.gv[off + 32 * db] += dv[db][i];
         }
       } else {
         bf16* okp = (bf16*)a.dk_p;
         bf16* ovp = (bf16*)a.dv_p;
 #pragma unroll
-        for (int nb = 0; nb < NDB; ++nb) {
-          okp[off + 16 * nb] = f2bf(dk[nb][i] * a.scale + a.gk[off + 16 * nb]);
-          ovp[off + 16 * nb] = f2bf(dv[nb][i] + a.gv[off + 16 * nb]);
+        for (int db = 0; db < NDB; ++db) {
+          okp[off + 32 * db] = (bf16)(dk[db][i] * a.scale + a.gk[off + 32 * db]);
+          ovp[off + 32 * db] = (bf16)(dv[db][i] + a.gv[off + 32 * db]);
         }
       }
     } else {
-      const size_t off = ((size_t)(kbase + key) * a.hkv + hk) * D + c;
+      const size_t off = ((size_t)(kbase + key) * a.hkv + hk) * D + r;
       bf16* oks = (bf16*)a.dk_s;
       bf16* ovs = (bf16*)a.dv_s;
 #pragma unroll
-      for (int nb = 0; nb < NDB; ++nb) {
-        oks[off + 16 * nb] = f2bf(dk[nb][i] * a.scale);
-        ovs[off + 16 * nb] = f2bf(dv[nb][i]);
+      for (int db = 0; db < NDB; ++db) {
+        oks[off + 32 * db] = (bf16)(dk[db][i] * a.scale);
+        ovs[off + 32 * db] = (bf16)dv[db][i];
       }
     }
   }
 }
 
+// ----------------------------------------------------------------- bwd_q
+template <int D>
+__global__ __launch_bounds__(kBwdThreads) void bwd_q_bf16_kernel(AttnArgs a) {
+  using TG = TileGeom<D>;
+  constexpr int BQ = kQBQ, BK = kQBK;
+  constexpr int NS = D / 16;
+  constexpr int NDB = D / 32;
+  __shared__ __attribute__((aligned(16))) bf16 Kn[2][TG::NAT];
+  __shared__ __attribute__((aligned(16))) bf16 Vn[2][TG::NAT];
+  __shared__ __attribute__((aligned(16))) bf16 Kt[2][TG::TRN];
+
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int r = lane & 31, h = lane >> 5;
+
+  const int tile = gridDim.x - 1 - blockIdx.x;  // rows with the most keys first
+  const int seq = a.seq_base + blockIdx.z;
+  bool prefix_rows;
+  int lp0, seg_len, row_base;
+  if (tile < a.n_prefix_q_tiles) {
+    prefix_rows = true;
+    lp0 = tile * BQ;
+    seg_len = a.P;
+    row_base = 0;
+  } else {
+    prefix_rows = false;
+    lp0 = (tile - a.n_prefix_q_tiles) * BQ;
+    row_base = a.cu[seq];
+    seg_len = a.cu[seq + 1] - row_base;
+  }
+  if (lp0 >= seg_len) return;
+  const int hq = blockIdx.y, hk = hq / (a.hq / a.hkv);
+  const int wave_lp0 = lp0 + 32 * w;
+  const int my_lp = wave_lp0 + r;
+  const bool row_valid = my_lp < seg_len;
+
+  // Q, dO as the B operands of S^T = K Q^T and dP^T = V dO^T
+  bf16x8 qf[NS], df[NS];
+  float lse2 = 0.f, drow = 0.f;
+  {
+    const bf16* qb = (const bf16*)(prefix_rows ? a.q_p : a.q_s);
+    const bf16* db = (const bf16*)(prefix_rows ? a.do_p : a.do_s);
+    const size_t row = (size_t)(row_base + (row_valid ? my_lp : 0));
+    const size_t off = (row * a.hq + hq) * D + 8 * h;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      qf[s] = row_valid ? *(const bf16x8*)(qb + off + 16 * s) : zero_bf8();
+      df[s] = row_valid ? *(const bf16x8*)(db + off + 16 * s) : zero_bf8();
+    }
+    if (row_valid) {
+      lse2 = (prefix_rows ? a.lse_p : a.lse_s)[row * a.hq + hq] * kLog2e;
+      drow = (prefix_rows ? a.dd_p : a.dd_s)[row * a.hq + hq];
+    }
+  }
+  f32x16 dq[NDB];
+#pragma unroll
+  for (int db = 0; db < NDB; ++db) dq[db] = zero16();
+
+  const int last_lp = min(lp0 + BQ, seg_len) - 1;
+  const int nkeys0 = prefix_rows ? min(a.P, last_lp + 1) : a.P;
+  const int nkeys1 = prefix_rows ? 0 : last_lp + 1;
+  const int nt0 = (nkeys0 + BK - 1) / BK, nt1 = (nkeys1 + BK - 1) / BK;
+  const int ntiles = nt0 + nt1;
+  auto tile_info = [&](int t, int& seg, int& k0, int& nk) {
+    seg = t < nt0 ? 0 : 1;
+    k0 = (seg == 0 ? t : t - nt0) * BK;
+    nk = min(BK, (seg == 0 ? nkeys0 : nkeys1) - k0);
+  };
+  Stager<D> sk, sv;
+  auto stage_load = [&](int t) {
+    int seg, k0, nk;
+    tile_info(t, seg, k0, nk);
+    const bf16* kb = (const bf16*)(seg == 0 ? a.k_p : a.k_s);
+    const bf16* vb = (const bf16*)(seg == 0 ? a.v_p : a.v_s);
+    const int kbase = seg == 0 ? 0 : row_base;
+    sk.load(kb, kbase + k0, nk, a.hkv, hk, tid);
+    sv.load(vb, kbase + k0, nk, a.hkv, hk, tid);
+  };
+  auto stage_store = [&](int buf) {
+    sk.store_nat(Kn[buf], tid);
+    sk.store_trn(Kt[buf], tid);
+    sv.store_nat(Vn[buf], tid);
+  };
+  if (ntiles > 0) {
+    stage_load(0);
+    stage_store(0);
+  }
+  __syncthreads();
+
+  for (int t = 0; t < ntiles; ++t) {
+    const int buf = t & 1;
+    if (t + 1 < ntiles) stage_load(t + 1);
+    int seg, k0, nk;
+    tile_info(t, seg, k0, nk);
+    const bool causal = (seg == 0) == prefix_rows;
+    if (!(causal && k0 > wave_lp0 + 31)) {
+      // st[kb][i] = S^T[key k0 + 32 kb + 8 (i/4) + 4 h + i%4][row my_lp]; pt = dP^T
+      f32x16 st[BK / 32], pt[BK / 32];
+#pragma unroll
+      for (int kb = 0; kb < BK / 32; ++kb) {
+        st[kb] = zero16();
+        pt[kb] = zero16();
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+          st[kb] = mfma32(nat_frag<D>(Kn[buf], 32 * kb + r, 16 * s, h), qf[s], st[kb]);
+          pt[kb] = mfma32(nat_frag<D>(Vn[buf], 32 * kb + r, 16 * s, h), df[s], pt[kb]);
+        }
+      }
+#pragma unroll
+      for (int kb = 0; kb < BK / 32; ++kb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int kk = 32 * kb + 8 * (i >> 2) + 4 * h + (i & 3);
+          const bool vis = row_valid && kk < nk && (!causal || k0 + kk <= my_lp);
+          const float p = vis ? exp2f(st[kb][i] * a.scale_log2 - lse2) : 0.f;
+          pt[kb][i] = p * (pt[kb][i] - drow);  // dS^T
+        }
+      // dQ^T += K^T dS^T over 16-key steps u (chunks 4 u + h and 4 u + 2 + h)
+#pragma unroll
+      for (int u = 0; u < BK / 16; ++u) {
+        const bf16x8 sb = c_to_kfrag(pt[u >> 1], u & 1);
+#pragma unroll
+        for (int db = 0; db < NDB; ++db)
+          dq[db] = mfma32(trn_frag(Kt[buf], 32 * db + r, 4 * u + h, 4 * u + 2 + h), sb, dq[db]);
+      }
+    }
+    if (t + 1 < ntiles) stage_store(buf ^ 1);
+    __syncthreads();
+  }
+
+  if (!row_valid) return;
+  // dq[db][i] = dQ^T[d = 32 db + 8 (i/4) + 4 h + i%4][row my_lp] (unscaled)
+  const size_t off = ((size_t)(row_base + my_lp) * a.hq + hq) * D + 4 * h;
+  if (prefix_rows && a.dq_p_accumulate) {
+    // dense baseline: the prefix rows' dQ sums over the trajectories
+    float* acc = a.dq_acc_p;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        float4* p4 = (float4*)(acc + off + 32 * db + 8 * g4);
+        float4 v = *p4;
+        v.x += dq[db][4 * g4];
+        v.y += dq[db][4 * g4 + 1];
+        v.z += dq[db][4 * g4 + 2];
+        v.w += dq[db][4 * g4 + 3];
+        *p4 = v;
+      }
+    return;
+  }
+  bf16* out = (bf16*)(prefix_rows ? a.dq_p : a.dq_s);
+#pragma unroll
+  for (int db = 0; db < NDB; ++db)
+#pragma unroll
+    for (int g4 = 0; g4 < 4; ++g4) {
+      const bf16x4 v = {(bf16)(dq[db][4 * g4] * a.scale), (bf16)(dq[db][4 * g4 + 1] * a.scale),
+                        (bf16)(dq[db][4 * g4 + 2] * a.scale), (bf16)(dq[db][4 * g4 + 3] * a.scale)};
+      *(bf16x4*)(out + off + 32 * db + 8 * g4) = v;
+    }
+}
+
 hipError_t launch_bwd_bf16(const AttnArgs& a, int head_dim, int n_qz, bool deterministic,
                            hipStream_t st) {
-  (void)n_qz;
-  if (deterministic) return hipErrorNotSupported;
-  const dim3 grid(a.n_prefix_k_tiles + a.n_seq * a.n_suffix_k_tiles, a.hkv, 1);
-  if (grid.x == 0) return hipSuccess;
-  ProfileScope ps("bwd_bf16", st);
+  (void)deterministic;  // both kernels are deterministic: no atomics anywhere
+  {
+    const dim3 grid(a.n_prefix_k_tiles + a.n_seq * a.n_suffix_k_tiles, a.hkv, 1);
+    if (grid.x > 0) {
+      ProfileScope ps("bwd_kv_bf16", st);
+      if (head_dim == 64)
+        hipLaunchKernelGGL(bwd_kv_bf16_kernel<64>, grid, dim3(kBwdThreads), 0, st, a);
+      else
+        hipLaunchKernelGGL(bwd_kv_bf16_kernel<128>, grid, dim3(kBwdThreads), 0, st, a);
+      const hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    }
+  }
+  const dim3 grid(a.n_prefix_q_tiles + a.n_suffix_q_tiles, a.hq, n_qz);
+  if (grid.x == 0 || n_qz == 0) return hipSuccess;
+  ProfileScope ps("bwd_q_bf16", st);
   if (head_dim == 64)
-    hipLaunchKernelGGL(bwd_bf16_kernel<64>, grid, dim3(kBwdThreads), 0, st, a);
+    hipLaunchKernelGGL(bwd_q_bf16_kernel<64>, grid, dim3(kBwdThreads), 0, st, a);
   else
-    hipLaunchKernelGGL(bwd_bf16_kernel<128>, grid, dim3(kBwdThreads), 0, st, a);
+    hipLaunchKernelGGL(bwd_q_bf16_kernel<128>, grid, dim3(kBwdThreads), 0, st, a);
   return hipGetLastError();
 }
 

@@ -10,7 +10,7 @@
 namespace spr {
 
 // --- per-kernel timing (enabled through spr_profile_enable) -------------
-bool profile_enabled();
+bool profile_enabled(const char* kernel);
 void profile_record(const char* kernel, hipEvent_t begin, hipEvent_t end);
 hipEvent_t profile_event();  // from a pool owned by the profiler
 
@@ -19,7 +19,7 @@ hipEvent_t profile_event();  // from a pool owned by the profiler
 class ProfileScope {
  public:
   ProfileScope(const char* kernel, hipStream_t stream) : kernel_(kernel), stream_(stream) {
-    if (profile_enabled()) {
+    if (profile_enabled(kernel)) {
       begin_ = profile_event();
       end_ = profile_event();
       if (begin_ && end_) hipEventRecord(begin_, stream_);

@@ -159,25 +159,26 @@ WsLayout ws_layout(int op, const spr_dims* d, int32_t max_len, int32_t total_len
     off = align_up(off + bytes, 256);
     return at;
   };
-  const bool deterministic = (d->flags & SPR_DETERMINISTIC) != 0;
-  (void)deterministic;
+  // the bf16 path writes dQ directly (query-outer kernel); the fp32 path
+  // accumulates it in fp32 and converts
+  const bool f32 = d->dtype == SPR_F32;
   switch (op) {
     case SPR_OP_PREFIX_FWD:
     case SPR_OP_SUFFIX_FWD:
       break;
     case SPR_OP_SUFFIX_BWD:
       w.dd_s = take(hq * T * 4);
-      w.dq_acc_s = take(T * hq * hd * 4);
+      if (f32) w.dq_acc_s = take(T * hq * hd * 4);
       break;
     case SPR_OP_PREFIX_BWD:
       w.dd_p = take(hq * P * 4);
-      w.dq_acc_p = take(P * hq * hd * 4);
+      if (f32) w.dq_acc_p = take(P * hq * hd * 4);
       break;
     case SPR_OP_DENSE_BASELINE:
       w.dd_p = take(hq * P * 4);
       w.dq_acc_p = take(P * hq * hd * 4);
       w.dd_s = take(hq * T * 4);
-      w.dq_acc_s = take(T * hq * hd * 4);
+      if (f32) w.dq_acc_s = take(T * hq * hd * 4);
       w.dk_acc_p = take(P * hkv * hd * 4);
       w.dv_acc_p = take(P * hkv * hd * 4);
       break;
@@ -210,6 +211,7 @@ struct ProfRec {
 };
 std::mutex g_prof_mu;
 bool g_prof_on = false;
+std::string g_prof_only;  // empty: every kernel
 std::vector<ProfRec> g_prof_pending;
 std::vector<hipEvent_t> g_prof_pool;
 std::map<std::string, std::pair<double, int>> g_prof_totals;
@@ -233,9 +235,9 @@ void prof_drain_locked() {
 
 }  // namespace
 
-bool profile_enabled() {
+bool profile_enabled(const char* kernel) {
   std::lock_guard<std::mutex> lk(g_prof_mu);
-  return g_prof_on;
+  return g_prof_on && (g_prof_only.empty() || g_prof_only == kernel);
 }
 
 hipEvent_t profile_event() {
@@ -379,14 +381,16 @@ spr_status spr_suffix_attn_bwd_accum(const spr_dims* dims, const void* k_p, cons
   all.push_back({ws, w.total, "ws", false});
   if ((st = check_aliasing({bufs[12], bufs[13]}, all)) != SPR_OK) return st;
 
+  const bool f32 = dims->dtype == SPR_F32;
   float* dd_s = at<float>(ws, w.dd_s);
-  float* dq_acc = at<float>(ws, w.dq_acc_s);
+  float* dq_acc = f32 ? at<float>(ws, w.dq_acc_s) : nullptr;
   if ((st = hip_check(launch_row_dot(dims->dtype, do_s, o_s, total_len, nullptr, 0, (int)hq,
                                      (int)hd, dd_s, stream), "row statistic")) != SPR_OK)
     return st;
-  if ((st = hip_check(launch_fill_zero(dq_acc, T * hq * hd, stream), "dq clear")) != SPR_OK)
+  if (f32 && (st = hip_check(launch_fill_zero(dq_acc, T * hq * hd, stream), "dq clear")) != SPR_OK)
     return st;
   AttnArgs a = base_args(dims);
+  a.dq_s = dq_s;
   a.k_p = k_p; a.v_p = v_p;
   a.q_s = q_s; a.k_s = k_s; a.v_s = v_s; a.do_s = do_s;
   a.lse_s = const_cast<float*>(lse_s);
@@ -404,8 +408,8 @@ spr_status spr_suffix_attn_bwd_accum(const spr_dims* dims, const void* k_p, cons
   a.dk_s = dk_s; a.dv_s = dv_s;
   a.n_suffix_q_tiles = tiles(max_len, block_q(dims->dtype));
   if ((st = hip_check(launch_bwd(dims, a, n_mb, stream), "suffix backward")) != SPR_OK) return st;
-  if ((st = hip_check(launch_convert(dims->dtype, dq_acc, a.scale, nullptr, dq_s, T * hq * hd,
-                                     stream), "dq convert")) != SPR_OK)
+  if (f32 && (st = hip_check(launch_convert(dims->dtype, dq_acc, a.scale, nullptr, dq_s,
+                                            T * hq * hd, stream), "dq convert")) != SPR_OK)
     return st;
   return ok();
 }
@@ -449,14 +453,16 @@ spr_status spr_prefix_bwd(const spr_dims* dims, const void* q_p, const void* k_p
       return st;
     return ok();
   }
+  const bool f32 = dims->dtype == SPR_F32;
   float* dd_p = at<float>(ws, w.dd_p);
-  float* dq_acc = at<float>(ws, w.dq_acc_p);
+  float* dq_acc = f32 ? at<float>(ws, w.dq_acc_p) : nullptr;
   if ((st = hip_check(launch_row_dot(dims->dtype, do_p, o_p, (int)P, nullptr, 0, (int)hq, (int)hd,
                                      dd_p, stream), "row statistic")) != SPR_OK)
     return st;
-  if ((st = hip_check(launch_fill_zero(dq_acc, P * hq * hd, stream), "dq clear")) != SPR_OK)
+  if (f32 && (st = hip_check(launch_fill_zero(dq_acc, P * hq * hd, stream), "dq clear")) != SPR_OK)
     return st;
   AttnArgs a = base_args(dims);
+  a.dq_p = dq_p;
   a.q_p = q_p; a.k_p = k_p; a.v_p = v_p; a.do_p = do_p;
   a.lse_p = const_cast<float*>(lse_p);
   a.dd_p = dd_p; a.dq_acc_p = dq_acc;
@@ -468,8 +474,8 @@ spr_status spr_prefix_bwd(const spr_dims* dims, const void* q_p, const void* k_p
   a.dk_p = dk_p; a.dv_p = dv_p;
   a.n_prefix_q_tiles = tiles(dims->prefix_len, block_q(dims->dtype));
   if ((st = hip_check(launch_bwd(dims, a, 1, stream), "prefix backward")) != SPR_OK) return st;
-  if ((st = hip_check(launch_convert(dims->dtype, dq_acc, scale, nullptr, dq_p, P * hq * hd, stream),
-                      "dq convert")) != SPR_OK)
+  if (f32 && (st = hip_check(launch_convert(dims->dtype, dq_acc, scale, nullptr, dq_p, P * hq * hd,
+                                            stream), "dq convert")) != SPR_OK)
     return st;
   return ok();
 }
@@ -509,8 +515,9 @@ spr_status spr_dense_recompute_baseline(
   if ((st = check_ws(w, ws, ws_bytes)) != SPR_OK) return st;
   float* dd_p = at<float>(ws, w.dd_p);
   float* dq_acc_p = at<float>(ws, w.dq_acc_p);
+  const bool f32 = dims->dtype == SPR_F32;
   float* dd_s = at<float>(ws, w.dd_s);
-  float* dq_acc_s = at<float>(ws, w.dq_acc_s);
+  float* dq_acc_s = f32 ? at<float>(ws, w.dq_acc_s) : nullptr;
   float* dk_acc = at<float>(ws, w.dk_acc_p);
   float* dv_acc = at<float>(ws, w.dv_acc_p);
   const float scale = eff_scale(dims);
@@ -518,7 +525,7 @@ spr_status spr_dense_recompute_baseline(
 #define SPR_TRY(expr, what) \
   if ((st = hip_check((expr), (what))) != SPR_OK) return st
   SPR_TRY(launch_fill_zero(dq_acc_p, P * hq * hd, stream), "clear");
-  SPR_TRY(launch_fill_zero(dq_acc_s, T * hq * hd, stream), "clear");
+  if (f32) SPR_TRY(launch_fill_zero(dq_acc_s, T * hq * hd, stream), "clear");
   SPR_TRY(launch_fill_zero(dk_acc, P * hkv * hd, stream), "clear");
   SPR_TRY(launch_fill_zero(dv_acc, P * hkv * hd, stream), "clear");
   // one trajectory at a time, as a dense trainer runs them
@@ -541,6 +548,8 @@ spr_status spr_dense_recompute_baseline(
                            stream), "row statistic");
     a.do_p = dop_i; a.dd_p = dd_p; a.dq_acc_p = dq_acc_p;
     a.do_s = do_s; a.dd_s = dd_s; a.dq_acc_s = dq_acc_s;
+    a.dq_s = dq_s;
+    a.dq_p_accumulate = 1;
     a.n_prefix_k_tiles = tiles(dims->prefix_len, block_k(dims->dtype));
     a.n_suffix_k_tiles = tiles(max_len, block_k(dims->dtype));
     a.prefix_rows = have_dop ? 1 : 0;
@@ -554,7 +563,7 @@ spr_status spr_dense_recompute_baseline(
   SPR_TRY(launch_convert(dims->dtype, dq_acc_p, scale, nullptr, dq_p, P * hq * hd, stream), "convert");
   SPR_TRY(launch_convert(dims->dtype, dk_acc, 1.f, nullptr, dk_p, P * hkv * hd, stream), "convert");
   SPR_TRY(launch_convert(dims->dtype, dv_acc, 1.f, nullptr, dv_p, P * hkv * hd, stream), "convert");
-  SPR_TRY(launch_convert(dims->dtype, dq_acc_s, scale, nullptr, dq_s, T * hq * hd, stream), "convert");
+  if (f32) SPR_TRY(launch_convert(dims->dtype, dq_acc_s, scale, nullptr, dq_s, T * hq * hd, stream), "convert");
 #undef SPR_TRY
   return ok();
 }
@@ -589,9 +598,10 @@ spr_status spr_gkv_accumulate(const spr_dims* dims, float* gk_cache, float* gv_c
   return ok();
 }
 
-spr_status spr_profile_enable(int32_t enable) {
+spr_status spr_profile_enable(int32_t enable, const char* only_kernel) {
   std::lock_guard<std::mutex> lk(g_prof_mu);
   g_prof_on = enable != 0;
+  g_prof_only = only_kernel != nullptr ? only_kernel : "";
   return SPR_OK;
 }
 

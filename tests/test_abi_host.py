@@ -120,7 +120,9 @@ def test_cache_aliasing_is_rejected(lib):
 def test_workspace_checks(lib):
     dims = _dims()
     need = B.workspace_size(B.OP_SUFFIX_BWD, dims, 2, 10, 15)
-    assert need >= 15 * 4 * 128 * 4
+    assert need >= 15 * 4 * 4           # bf16: the row statistic only
+    need32 = B.workspace_size(B.OP_SUFFIX_BWD, _dims(dtype="f32"), 2, 10, 15)
+    assert need32 >= 15 * 4 * 128 * 4   # fp32 also accumulates dQ
     assert B.STATUS[_bwd_accum(dims, ws_bytes=need - 1)] == "SPR_ERR_WORKSPACE"
     assert B.STATUS[_bwd_accum(dims, ws=0)] == "SPR_ERR_WORKSPACE"
 
@@ -128,8 +130,10 @@ def test_workspace_checks(lib):
 def test_workspace_sizes_are_consistent(lib):
     dims = _dims(prefix_len=4096, num_q_heads=32, num_kv_heads=8)
     assert B.workspace_size(B.OP_PREFIX_FWD, dims) == 0
-    assert B.workspace_size(B.OP_PREFIX_BWD, dims) >= 4096 * 32 * 128 * 4
+    assert B.workspace_size(B.OP_PREFIX_BWD, dims) >= 4096 * 32 * 4
+    assert B.workspace_size(B.OP_PREFIX_BWD, _dims(prefix_len=4096, num_q_heads=32, num_kv_heads=8,
+                                                   dtype="f32")) >= 4096 * 32 * 128 * 4
     dense = B.workspace_size(B.OP_DENSE_BASELINE, dims, 8, 512, 4096)
-    assert dense >= 4096 * 32 * 128 * 4 * 2 + 4096 * 8 * 128 * 4 * 2
+    assert dense >= 4096 * 32 * 128 * 4 + 4096 * 8 * 128 * 4 * 2
     with pytest.raises(B.SprError):
         B.workspace_size(99, dims)

@@ -178,54 +178,64 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_kv_bf16_kernel(AttnArgs a) {
   }
   __syncthreads();
 
+  const int q_off = nat_off<D>(r, 0, h);  // A-operand reads: LDS row 32 rb + r
   for (int t = 0; t < ntiles; ++t) {
     const int buf = t & 1;
-    if (t + 1 < ntiles) stage_load(t + 1);
+    if (t + 1 < ntiles) stage_load(t + 1);  // global loads in flight during the MFMAs
     const RowTile rt = tile_info(t);
+    const bf16* Qb = Qn[buf] + q_off;
+    const bf16* Ob = On[buf] + q_off;
     // S = Q K^T and dP = dO V^T for the two 32-row blocks of the tile:
-    // acc[rb][i] is row 32 rb + 8 (i/4) + 4 h + i%4 of the tile, key my_key
+    // acc[rb][i] is tile row 32 rb + c_row(i, h), key my_key
     f32x16 sacc[2], pacc[2];
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb) {
       sacc[rb] = zero16();
       pacc[rb] = zero16();
-#pragma unroll
-      for (int s = 0; s < NS; ++s) {
-        sacc[rb] = mfma32(nat_frag<D>(Qn[buf], 32 * rb + r, 16 * s, h), kf[s], sacc[rb]);
-        pacc[rb] = mfma32(nat_frag<D>(On[buf], 32 * rb + r, 16 * s, h), vf[s], pacc[rb]);
-      }
     }
-    // P and dS (softmax backward of the joint row)
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb) {
+        sacc[rb] = mfma32(lds8(Qb, nat_off<D>(32 * rb, 16 * s, 0)), kf[s], sacc[rb]);
+        pacc[rb] = mfma32(lds8(Ob, nat_off<D>(32 * rb, 16 * s, 0)), vf[s], pacc[rb]);
+      }
+    // P and dS (softmax backward of the joint row); rows of element i of a
+    // block come in runs of 8: 32 rb + 16 (i / 8) + 8 h + i % 8
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
-      for (int g4 = 0; g4 < 4; ++g4) {
-        const int q0 = 32 * rb + 8 * g4 + 4 * h;
-        const float4 lv = *(const float4*)(&Ls[buf][q0]);
-        const float4 dd = *(const float4*)(&Dd[buf][q0]);
-        const float lq[4] = {lv.x, lv.y, lv.z, lv.w};
-        const float dq[4] = {dd.x, dd.y, dd.z, dd.w};
+      for (int half = 0; half < 2; ++half) {
+        const int q0 = 32 * rb + 16 * half + 8 * h;
+        const float4 l0 = *(const float4*)(&Ls[buf][q0]);
+        const float4 l1 = *(const float4*)(&Ls[buf][q0 + 4]);
+        const float4 d0 = *(const float4*)(&Dd[buf][q0]);
+        const float4 d1 = *(const float4*)(&Dd[buf][q0 + 4]);
+        const float lq[8] = {l0.x, l0.y, l0.z, l0.w, l1.x, l1.y, l1.z, l1.w};
+        const float dq[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
 #pragma unroll
-        for (int b = 0; b < 4; ++b) {
-          const int i = 4 * g4 + b, q = q0 + b;
+        for (int b = 0; b < 8; ++b) {
+          const int i = 8 * half + b, q = q0 + b;
           const bool vis = kvalid && q < rt.nr && (!rt.causal || my_key <= rt.lp_first + q);
-          const float p = vis ? exp2f(sacc[rb][i] * a.scale_log2 - lq[b]) : 0.f;
-          sacc[rb][i] = p;
-          pacc[rb][i] = p * (pacc[rb][i] - dq[b]);
+          const float p = fast_exp2(fmaf(sacc[rb][i], a.scale_log2, -lq[b]));
+          const float pv = vis ? p : 0.f;
+          sacc[rb][i] = pv;
+          pacc[rb][i] = pv * (pacc[rb][i] - dq[b]);
         }
       }
-    // dV += P^T dO ; dK += dS^T Q over 16-row steps u: rows 16 u + 4 h + 0..3
-    // (chunk 4 u + h) and 16 u + 8 + 4 h + 0..3 (chunk 4 u + 2 + h)
+    // dV += P^T dO ; dK += dS^T Q over 16-row steps u: rows 16 u + 8 h + 0..7
 #pragma unroll
     for (int u = 0; u < BQ / 16; ++u) {
       const bf16x8 pa = c_to_kfrag(sacc[u >> 1], u & 1);
       const bf16x8 sa = c_to_kfrag(pacc[u >> 1], u & 1);
 #pragma unroll
       for (int db = 0; db < NDB; ++db) {
-        dv[db] = mfma32(pa, trn_frag(Ot[buf], 32 * db + r, 4 * u + h, 4 * u + 2 + h), dv[db]);
-        dk[db] = mfma32(sa, trn_frag(Qt[buf], 32 * db + r, 4 * u + h, 4 * u + 2 + h), dk[db]);
+        const int off = trn_off(32 * db + r, u, h);
+        dv[db] = mfma32(pa, lds8(Ot[buf], off), dv[db]);
+        dk[db] = mfma32(sa, lds8(Qt[buf], off), dk[db]);
       }
     }
+    compiler_fence();
     if (t + 1 < ntiles) stage_store(buf ^ 1);
     __syncthreads();
   }
@@ -353,43 +363,50 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_q_bf16_kernel(AttnArgs a) {
   }
   __syncthreads();
 
+  const int k_off = nat_off<D>(r, 0, h);  // A-operand reads: LDS row 32 kb + r
   for (int t = 0; t < ntiles; ++t) {
     const int buf = t & 1;
-    if (t + 1 < ntiles) stage_load(t + 1);
+    if (t + 1 < ntiles) stage_load(t + 1);  // global loads in flight during the MFMAs
     int seg, k0, nk;
     tile_info(t, seg, k0, nk);
     const bool causal = (seg == 0) == prefix_rows;
-    if (!(causal && k0 > wave_lp0 + 31)) {
-      // st[kb][i] = S^T[key k0 + 32 kb + 8 (i/4) + 4 h + i%4][row my_lp]; pt = dP^T
+    if (!(causal && k0 > wave_lp0 + 31)) {  // else no row of this wave sees the tile
+      const bf16* Kb = Kn[buf] + k_off;
+      const bf16* Vb = Vn[buf] + k_off;
+      // st[kb][i] = S^T[key k0 + 32 kb + c_row(i, h)][row my_lp]; pt = dP^T
       f32x16 st[BK / 32], pt[BK / 32];
 #pragma unroll
       for (int kb = 0; kb < BK / 32; ++kb) {
         st[kb] = zero16();
         pt[kb] = zero16();
-#pragma unroll
-        for (int s = 0; s < NS; ++s) {
-          st[kb] = mfma32(nat_frag<D>(Kn[buf], 32 * kb + r, 16 * s, h), qf[s], st[kb]);
-          pt[kb] = mfma32(nat_frag<D>(Vn[buf], 32 * kb + r, 16 * s, h), df[s], pt[kb]);
-        }
       }
+#pragma unroll
+      for (int s = 0; s < NS; ++s)
+#pragma unroll
+        for (int kb = 0; kb < BK / 32; ++kb) {
+          st[kb] = mfma32(lds8(Kb, nat_off<D>(32 * kb, 16 * s, 0)), qf[s], st[kb]);
+          pt[kb] = mfma32(lds8(Vb, nat_off<D>(32 * kb, 16 * s, 0)), df[s], pt[kb]);
+        }
+      // keys kk < lim are visible to this lane's row
+      const int lim = !row_valid ? 0 : (causal ? min(nk, my_lp - k0 + 1) : nk);
 #pragma unroll
       for (int kb = 0; kb < BK / 32; ++kb)
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          const int kk = 32 * kb + 8 * (i >> 2) + 4 * h + (i & 3);
-          const bool vis = row_valid && kk < nk && (!causal || k0 + kk <= my_lp);
-          const float p = vis ? exp2f(st[kb][i] * a.scale_log2 - lse2) : 0.f;
-          pt[kb][i] = p * (pt[kb][i] - drow);  // dS^T
+          const int kk = 32 * kb + c_row(i, h);
+          const float p = fast_exp2(fmaf(st[kb][i], a.scale_log2, -lse2));
+          pt[kb][i] = kk < lim ? p * (pt[kb][i] - drow) : 0.f;  // dS^T
         }
-      // dQ^T += K^T dS^T over 16-key steps u (chunks 4 u + h and 4 u + 2 + h)
+      // dQ^T += K^T dS^T over 16-key steps u: keys 16 u + 8 h + 0..7
 #pragma unroll
       for (int u = 0; u < BK / 16; ++u) {
         const bf16x8 sb = c_to_kfrag(pt[u >> 1], u & 1);
 #pragma unroll
         for (int db = 0; db < NDB; ++db)
-          dq[db] = mfma32(trn_frag(Kt[buf], 32 * db + r, 4 * u + h, 4 * u + 2 + h), sb, dq[db]);
+          dq[db] = mfma32(lds8(Kt[buf], trn_off(32 * db + r, u, h)), sb, dq[db]);
       }
     }
+    compiler_fence();
     if (t + 1 < ntiles) stage_store(buf ^ 1);
     __syncthreads();
   }

@@ -38,8 +38,8 @@ __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(AttnArgs a) {
   constexpr int BQ = kFwdBQ, BK = kFwdBK;
   constexpr int NS = D / 16;   // k-steps over d for S^T
   constexpr int NDB = D / 32;  // 32-wide d blocks of O^T
-  __shared__ __attribute__((aligned(16))) bf16 Kn[2][TG::NAT];
-  __shared__ __attribute__((aligned(16))) bf16 Vt[2][TG::TRN];
+  __shared__ __attribute__((aligned(16))) bf16 Kn[2 * TG::NAT];
+  __shared__ __attribute__((aligned(16))) bf16 Vt[2 * TG::TRN];
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int r = lane & 31, h = lane >> 5;
@@ -79,6 +79,12 @@ __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(AttnArgs a) {
   for (int db = 0; db < NDB; ++db) o[db] = zero16();
   float m = -INFINITY, l = 0.f;  // running max (log2 domain) and sum of row my_lp
 
+  // LDS offsets of this lane's fragments: K rows at k_off + immediates; the
+  // V column of d block db is v_col + db * 32 * kTileRows, its 16-key step u
+  // at chunk (2 u + h) ^ trn_swz(32 db + r)
+  const int k_off = nat_off<D>(r, 0, h);
+  const int v_col = r * kTileRows;
+
   // key tiles: prefix keys first (causal for prefix rows), then own suffix keys
   const int last_lp = min(lp0 + BQ, seg_len) - 1;
   const int nkeys0 = prefix_rows ? min(a.P, last_lp + 1) : a.P;
@@ -102,8 +108,8 @@ __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(AttnArgs a) {
   };
   if (ntiles > 0) {
     stage_load(0);
-    sk.store_nat(Kn[0], tid);
-    sv.store_trn(Vt[0], tid);
+    sk.store_nat(Kn, tid);
+    sv.store_trn(Vt, tid);
   }
   __syncthreads();
 
@@ -114,60 +120,60 @@ __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(AttnArgs a) {
     tile_info(t, seg, k0, nk);
     const bool causal = (seg == 0) == prefix_rows;  // keys of the row's own segment
     if (!(causal && k0 > wave_lp0 + 31)) {          // else no row of this wave sees the tile
-      // S^T = K Q^T ; st[kb][i] = S^T[key k0 + 32 kb + 8 (i/4) + 4 h + i%4][row my_lp]
+      const bf16* Kb = Kn + buf * TG::NAT + k_off;
+      const bf16* Vb = Vt + buf * TG::TRN;
+      // S^T = K Q^T ; st[kb][i] = S^T[key k0 + 32 kb + c_row(i, h)][row my_lp]
       f32x16 st[BK / 32];
 #pragma unroll
-      for (int kb = 0; kb < BK / 32; ++kb) {
-        st[kb] = zero16();
+      for (int kb = 0; kb < BK / 32; ++kb) st[kb] = zero16();
 #pragma unroll
-        for (int s = 0; s < NS; ++s)
-          st[kb] = mfma32(nat_frag<D>(Kn[buf], 32 * kb + r, 16 * s, h), qf[s], st[kb]);
+      for (int s = 0; s < NS; ++s)  // independent chains interleaved
+#pragma unroll
+        for (int kb = 0; kb < BK / 32; ++kb)
+          st[kb] = mfma32(lds8(Kb, nat_off<D>(32 * kb, 16 * s, 0)), qf[s], st[kb]);
+#define SC(e) st[(e) >> 4][(e) & 15]
+      if (nk < BK || (causal && k0 + BK - 1 > wave_lp0)) {  // partial or diagonal tile
+        const int lim = causal ? min(nk, my_lp - k0 + 1) : nk;  // keys kk < lim are visible
+#pragma unroll
+        for (int e = 0; e < BK / 2; ++e) SC(e) = 32 * (e >> 4) + c_row(e & 15, h) < lim ? SC(e) : -INFINITY;
       }
-      const bool need_mask = nk < BK || (causal && k0 + BK - 1 > wave_lp0);
       float mt = -INFINITY;
 #pragma unroll
-      for (int kb = 0; kb < BK / 32; ++kb)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          float v = st[kb][i] * a.scale_log2;
-          if (need_mask) {
-            const int kk = 32 * kb + 8 * (i >> 2) + 4 * h + (i & 3);
-            if (kk >= nk || (causal && k0 + kk > my_lp)) v = -INFINITY;
-          }
-          st[kb][i] = v;
-          mt = fmaxf(mt, v);
-        }
-      mt = fmaxf(mt, __shfl_xor(mt, 32));
+      for (int e = 0; e < BK / 2; ++e) mt = fmaxf(mt, SC(e));
+      mt = fmaxf(mt, __shfl_xor(mt, 32)) * a.scale_log2;
       const float mn = fmaxf(m, mt);
       const float mu = mn == -INFINITY ? 0.f : mn;
-      const float corr = exp2f(m - mu);
+      if (__builtin_expect(__any(mn > m), 0)) {  // rescale only when some row's max grew
+        const float corr = fast_exp2(m - mu);
+        l *= corr;
+#pragma unroll
+        for (int db = 0; db < NDB; ++db) o[db] *= corr;
+      }
+      m = mn;
       float rs = 0.f;
 #pragma unroll
-      for (int kb = 0; kb < BK / 32; ++kb)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const float p = exp2f(st[kb][i] - mu);
-          st[kb][i] = p;
-          rs += p;
-        }
+      for (int e = 0; e < BK / 2; ++e) {
+        SC(e) = fast_exp2(fmaf(SC(e), a.scale_log2, -mu));
+        rs += SC(e);
+      }
       rs += __shfl_xor(rs, 32);
-      l = l * corr + rs;
-      m = mn;
-#pragma unroll
-      for (int db = 0; db < NDB; ++db) o[db] *= corr;
-      // O^T += V^T P^T over 16-key steps u: keys 16 u + 4 h + 0..3 (chunk 4 u + h)
-      // and 16 u + 8 + 4 h + 0..3 (chunk 4 u + 2 + h)
+      l += rs;
+#undef SC
+      // O^T += V^T P^T over 16-key steps u: keys 16 u + 8 h + 0..7
 #pragma unroll
       for (int u = 0; u < BK / 16; ++u) {
         const bf16x8 pb = c_to_kfrag(st[u >> 1], u & 1);
 #pragma unroll
         for (int db = 0; db < NDB; ++db)
-          o[db] = mfma32(trn_frag(Vt[buf], 32 * db + r, 4 * u + h, 4 * u + 2 + h), pb, o[db]);
+          o[db] = mfma32(lds8(Vb, v_col + db * 32 * kTileRows +
+                                      8 * ((2 * u + h) ^ trn_swz(32 * db + r))),
+                         pb, o[db]);
       }
     }
+    compiler_fence();
     if (t + 1 < ntiles) {
-      sk.store_nat(Kn[buf ^ 1], tid);
-      sv.store_trn(Vt[buf ^ 1], tid);
+      sk.store_nat(Kn + (buf ^ 1) * TG::NAT, tid);
+      sv.store_trn(Vt + (buf ^ 1) * TG::TRN, tid);
     }
     __syncthreads();
   }

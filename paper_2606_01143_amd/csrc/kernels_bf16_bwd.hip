@@ -7,25 +7,26 @@
 //   dV = P^T dO,  dK = dS^T Q / sqrt(d),  dQ = dS K / sqrt(d).
 // Two kernels split the work so that no gradient needs atomics:
 //
-// bwd_kv (key-outer): one workgroup owns a 128-key tile of one kv head and
-//   sweeps every query row that sees it, for all G q heads of the kv head.
-//   For a prefix key tile in Phase B the rows are all suffix rows of the
-//   microbatch, so the tile's dK/dV are exactly gK_1 = dS_21^T Q_2 / sqrt(d)
-//   and gV_1 = P_21^T dO_2; the workgroup adds them into the fp32 cache
-//   G_K/G_V with a plain read-modify-write.  Each (prefix tile, kv head)
-//   belongs to exactly one workgroup of a launch, so the cache update is
-//   deterministic.  In Phase C the epilogue writes dK_1 = local + G_K and
-//   dV_1 = local + G_V instead.  Per 64-row tile and wave (32 keys):
-//     S  = Q K^T, dP = dO V^T     A = Q/dO rows (natural tiles), B = K/V (registers)
-//     dV += P^T dO, dK += dS^T Q  A = P^T/dS^T from the S/dP registers,
-//                                 B = dO/Q columns (transposed tiles)
+// bwd_kv (key-outer): one workgroup owns a 128-key tile of one kv head (32
+//   keys per wave) and sweeps every query row that sees it, for all G q
+//   heads of the kv head.  For a prefix key tile in Phase B the rows are all
+//   suffix rows of the microbatch, so the tile's dK/dV are exactly
+//   gK_1 = dS_21^T Q_2 / sqrt(d) and gV_1 = P_21^T dO_2; the workgroup adds
+//   them into the fp32 cache G_K/G_V with a plain read-modify-write.  Each
+//   (prefix tile, kv head) belongs to exactly one workgroup of a launch, so
+//   the cache update is deterministic.  In Phase C the epilogue writes
+//   dK_1 = local + G_K and dV_1 = local + G_V instead.  Per 32-row block and
+//   wave (operand conventions in tile.hpp):
+//     S  = Q K^T, dP = dO V^T      A = Q/dO tile rows, B = K/V (registers)
+//     dV^T += dO^T P, dK^T += Q^T dS  A = dO/Q tiles read transposed,
+//                                     B = P/dS straight from the registers
 // bwd_q (query-outer): one workgroup owns 128 query rows of one q head and
 //   sweeps their visible key tiles, recomputing S and dP:
-//     S^T = K Q^T, dP^T = V dO^T  A = K/V rows (natural tiles), B = Q/dO (registers)
-//     dQ^T += K^T dS^T            A = K columns (transposed tile), B = dS^T registers
+//     S^T = K Q^T, dP^T = V dO^T   A = K/V tile rows, B = Q/dO (registers)
+//     dQ^T += K^T dS^T             A = K tile read transposed, B = dS^T registers
 //   and writes dQ once, already scaled and rounded.
-// Both stream their tiles through double-buffered LDS with the next tile's
-// global loads in flight during the current tile's products.
+// Both stream their tiles through double-buffered LDS, filled by
+// direct-to-LDS loads issued one tile ahead of the products.
 #include "common.hpp"
 #include "launch.hpp"
 #include "tile.hpp"
@@ -34,63 +35,62 @@ namespace spr {
 
 namespace {
 constexpr int kKvBK = 128;  // keys per bwd_kv workgroup (32 per wave)
-constexpr int kKvBQ = 64;   // rows per streamed tile
 constexpr int kQBQ = 128;   // rows per bwd_q workgroup (32 per wave)
-constexpr int kQBK = 64;    // keys per streamed tile
-constexpr int kBwdThreads = 256;
 }  // namespace
 
 int bwd_bf16_block_k() { return kKvBK; }
 
 // ---------------------------------------------------------------- bwd_kv
 template <int D>
-__global__ __launch_bounds__(kBwdThreads) void bwd_kv_bf16_kernel(AttnArgs a) {
-  using TG = TileGeom<D>;
-  constexpr int BK = kKvBK, BQ = kKvBQ;
+__global__ __launch_bounds__(kThreads, 1) void bwd_kv_bf16_kernel(AttnArgs a) {
   constexpr int NS = D / 16;
   constexpr int NDB = D / 32;
-  __shared__ __attribute__((aligned(16))) bf16 Qn[2][TG::NAT];
-  __shared__ __attribute__((aligned(16))) bf16 On[2][TG::NAT];  // dO, natural
-  __shared__ __attribute__((aligned(16))) bf16 Qt[2][TG::TRN];
-  __shared__ __attribute__((aligned(16))) bf16 Ot[2][TG::TRN];  // dO, transposed
-  __shared__ __attribute__((aligned(16))) float Ls[2][BQ];
-  __shared__ __attribute__((aligned(16))) float Dd[2][BQ];
+  constexpr int TE = Tile<D>::ELEMS, BQ = kTileRows;
+  __shared__ __attribute__((aligned(1024))) bf16 Q0[TE];
+  __shared__ __attribute__((aligned(1024))) bf16 Q1[TE];
+  __shared__ __attribute__((aligned(1024))) bf16 O0[TE];  // dO
+  __shared__ __attribute__((aligned(1024))) bf16 O1[TE];
+  __shared__ __attribute__((aligned(256))) float L0[BQ];  // LSE of the tile rows
+  __shared__ __attribute__((aligned(256))) float L1[BQ];
+  __shared__ __attribute__((aligned(256))) float E0[BQ];  // rowsum(dO * O)
+  __shared__ __attribute__((aligned(256))) float E1[BQ];
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int r = lane & 31, h = lane >> 5;
-  const int hk = blockIdx.y, G = a.hq / a.hkv;
+  // 1D grid: block b -> kv head b % Hkv (one XCD per kv head), key tile b / Hkv
+  const int hk = blockIdx.x % a.hkv, x = blockIdx.x / a.hkv;
+  const int G = a.hq / a.hkv;
 
   // ---- which 128 keys: a prefix tile, or a tile of suffix s
-  const int x = blockIdx.x;
   bool kpre;
   int k0, kseg, kbase;
   if (x < a.n_prefix_k_tiles) {
     kpre = true;
-    k0 = x * BK;
+    k0 = x * kKvBK;
     kseg = a.P;
     kbase = 0;
   } else {
     const int y = x - a.n_prefix_k_tiles;
     const int s = a.seq_base + y / a.n_suffix_k_tiles;
-    k0 = (y % a.n_suffix_k_tiles) * BK;
+    k0 = (y % a.n_suffix_k_tiles) * kKvBK;
     kbase = a.cu[s];
     kseg = a.cu[s + 1] - kbase;
     kpre = false;
   }
   if (k0 >= kseg) return;
-  const int my_key = k0 + 32 * w + r;  // segment-local key of this lane's S/dP column
-  const bool kvalid = my_key < kseg;
+  const int wave_k0 = k0 + 32 * w;
+  const int my_key = min(wave_k0 + r, kseg - 1);  // keys past the end recompute the last one
 
-  // K, V as the B operand of S = Q K^T and dP = dO V^T
+  // K, V as the B operand of S = Q K^T and dP = dO V^T (natural k)
   bf16x8 kf[NS], vf[NS];
   {
     const bf16* kg = (const bf16*)(kpre ? a.k_p : a.k_s);
     const bf16* vg = (const bf16*)(kpre ? a.v_p : a.v_s);
-    const size_t off = ((size_t)(kbase + (kvalid ? my_key : k0)) * a.hkv + hk) * D + 8 * h;
+    const size_t off = ((size_t)(kbase + my_key) * a.hkv + hk) * D + 8 * h;
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      kf[s] = kvalid ? *(const bf16x8*)(kg + off + 16 * s) : zero_bf8();
-      vf[s] = kvalid ? *(const bf16x8*)(vg + off + 16 * s) : zero_bf8();
+      kf[s] = *(const bf16x8*)(kg + off + 16 * s);
+      vf[s] = *(const bf16x8*)(vg + off + 16 * s);
     }
   }
   f32x16 dk[NDB], dv[NDB];
@@ -140,279 +140,281 @@ __global__ __launch_bounds__(kBwdThreads) void bwd_kv_bf16_kernel(AttnArgs a) {
     } else {
       rt.prefix = false;
       rt.causal = true;
-      rt.lp_first = k0 + j * BQ;
+      rt.lp_first = k0 + (j - n_pr) * BQ;
       rt.row0 = kbase + rt.lp_first;
       rt.nr = min(BQ, kseg - rt.lp_first);
     }
     return rt;
   };
-  Stager<D> sq, so;
-  float lreg = 0.f, dreg = 0.f;
-  auto stage_load = [&](int t) {
-    const RowTile rt = tile_info(t);
-    const bf16* qg = (const bf16*)(rt.prefix ? a.q_p : a.q_s);
-    const bf16* dg = (const bf16*)(rt.prefix ? a.do_p : a.do_s);
-    sq.load(qg, rt.row0, rt.nr, a.hq, rt.hh, tid);
-    so.load(dg, rt.row0, rt.nr, a.hq, rt.hh, tid);
-    if (tid < BQ) {
-      const float* lg = rt.prefix ? a.lse_p : a.lse_s;
-      const float* ddg = rt.prefix ? a.dd_p : a.dd_s;
-      const bool v = tid < rt.nr;
-      lreg = v ? lg[(size_t)(rt.row0 + tid) * a.hq + rt.hh] * kLog2e : INFINITY;
-      dreg = v ? ddg[(size_t)(rt.row0 + tid) * a.hq + rt.hh] : 0.f;
-    }
-  };
-  auto stage_store = [&](int buf) {
-    sq.store_nat(Qn[buf], tid);
-    sq.store_trn(Qt[buf], tid);
-    so.store_nat(On[buf], tid);
-    so.store_trn(Ot[buf], tid);
-    if (tid < BQ) {
-      Ls[buf][tid] = lreg;
-      Dd[buf][tid] = dreg;
-    }
-  };
-  if (ntiles > 0) {
-    stage_load(0);
-    stage_store(0);
-  }
-  __syncthreads();
 
-  const int q_off = nat_off<D>(r, 0, h);  // A-operand reads: LDS row 32 rb + r
-  for (int t = 0; t < ntiles; ++t) {
-    const int buf = t & 1;
-    if (t + 1 < ntiles) stage_load(t + 1);  // global loads in flight during the MFMAs
+  auto issue = [&](int t, bf16* Qd, bf16* Od, float* Ld, float* Ed) {
     const RowTile rt = tile_info(t);
-    const bf16* Qb = Qn[buf] + q_off;
-    const bf16* Ob = On[buf] + q_off;
-    // S = Q K^T and dP = dO V^T for the two 32-row blocks of the tile:
-    // acc[rb][i] is tile row 32 rb + c_row(i, h), key my_key
-    f32x16 sacc[2], pacc[2];
+    load_tile<D>(Qd, (const bf16*)(rt.prefix ? a.q_p : a.q_s), rt.row0, rt.nr, a.hq, rt.hh, w, lane);
+    load_tile<D>(Od, (const bf16*)(rt.prefix ? a.do_p : a.do_s), rt.row0, rt.nr, a.hq, rt.hh, w, lane);
+    if (w == 0) load_row_vec(Ld, (rt.prefix ? a.lse_p : a.lse_s) + rt.hh, rt.row0, rt.nr, a.hq, lane);
+    if (w == 1) load_row_vec(Ed, (rt.prefix ? a.dd_p : a.dd_s) + rt.hh, rt.row0, rt.nr, a.hq, lane);
+  };
+
+  auto compute = [&](int t, const bf16* Qc, const bf16* Oc, const float* Lc, const float* Ec) {
+    const RowTile rt = tile_info(t);
+    if (rt.causal && rt.lp_first + BQ - 1 < wave_k0) return;  // no row sees this wave's keys
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb) {
-      sacc[rb] = zero16();
-      pacc[rb] = zero16();
-    }
+      if (rt.causal && rt.lp_first + 32 * rb + 31 < wave_k0) continue;
+      // s[i] = S[row 32 rb + c_row(i, h)][key my_key]; dp likewise
+      f32x16 s = zero16(), dp = zero16();
 #pragma unroll
-    for (int s = 0; s < NS; ++s)
-#pragma unroll
-      for (int rb = 0; rb < 2; ++rb) {
-        sacc[rb] = mfma32(lds8(Qb, nat_off<D>(32 * rb, 16 * s, 0)), kf[s], sacc[rb]);
-        pacc[rb] = mfma32(lds8(Ob, nat_off<D>(32 * rb, 16 * s, 0)), vf[s], pacc[rb]);
+      for (int k = 0; k < NS; ++k) {
+        s = mfma32(row_frag<D>(Qc, 32 * rb + r, 16 * k + 8 * h), kf[k], s);
+        dp = mfma32(row_frag<D>(Oc, 32 * rb + r, 16 * k + 8 * h), vf[k], dp);
       }
-    // P and dS (softmax backward of the joint row); rows of element i of a
-    // block come in runs of 8: 32 rb + 16 (i / 8) + 8 h + i % 8
+      const bool need_mask = rt.nr < 32 * rb + 32 || (rt.causal && rt.lp_first + 32 * rb < wave_k0 + 31);
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb)
+      for (int g4 = 0; g4 < 4; ++g4) {
+        const int q0 = 32 * rb + 8 * g4 + 4 * h;
+        const float4 l4 = *(const float4*)(Lc + q0);
+        const float4 e4 = *(const float4*)(Ec + q0);
+        const float lq[4] = {l4.x, l4.y, l4.z, l4.w};
+        const float eq[4] = {e4.x, e4.y, e4.z, e4.w};
 #pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        const int q0 = 32 * rb + 16 * half + 8 * h;
-        const float4 l0 = *(const float4*)(&Ls[buf][q0]);
-        const float4 l1 = *(const float4*)(&Ls[buf][q0 + 4]);
-        const float4 d0 = *(const float4*)(&Dd[buf][q0]);
-        const float4 d1 = *(const float4*)(&Dd[buf][q0 + 4]);
-        const float lq[8] = {l0.x, l0.y, l0.z, l0.w, l1.x, l1.y, l1.z, l1.w};
-        const float dq[8] = {d0.x, d0.y, d0.z, d0.w, d1.x, d1.y, d1.z, d1.w};
-#pragma unroll
-        for (int b = 0; b < 8; ++b) {
-          const int i = 8 * half + b, q = q0 + b;
-          const bool vis = kvalid && q < rt.nr && (!rt.causal || my_key <= rt.lp_first + q);
-          const float p = fast_exp2(fmaf(sacc[rb][i], a.scale_log2, -lq[b]));
-          const float pv = vis ? p : 0.f;
-          sacc[rb][i] = pv;
-          pacc[rb][i] = pv * (pacc[rb][i] - dq[b]);
+        for (int b = 0; b < 4; ++b) {
+          const int i = 4 * g4 + b, q = q0 + b;
+          float p = fast_exp2(fmaf(s[i], a.scale_log2, -lq[b] * kLog2e));
+          if (need_mask) {
+            const bool vis = q < rt.nr && (!rt.causal || my_key <= rt.lp_first + q);
+            p = vis ? p : 0.f;
+          }
+          s[i] = p;
+          dp[i] = p * (dp[i] - eq[b]);
         }
       }
-    // dV += P^T dO ; dK += dS^T Q over 16-row steps u: rows 16 u + 8 h + 0..7
+      // dV^T += dO^T P ; dK^T += Q^T dS over 16-row k-steps v (C-order rows)
 #pragma unroll
-    for (int u = 0; u < BQ / 16; ++u) {
-      const bf16x8 pa = c_to_kfrag(sacc[u >> 1], u & 1);
-      const bf16x8 sa = c_to_kfrag(pacc[u >> 1], u & 1);
+      for (int v = 0; v < 2; ++v) {
+        const bf16x8 pb = c_kfrag(s, v);
+        const bf16x8 sb = c_kfrag(dp, v);
 #pragma unroll
-      for (int db = 0; db < NDB; ++db) {
-        const int off = trn_off(32 * db + r, u, h);
-        dv[db] = mfma32(pa, lds8(Ot[buf], off), dv[db]);
-        dk[db] = mfma32(sa, lds8(Qt[buf], off), dk[db]);
+        for (int db = 0; db < NDB; ++db) {
+          dv[db] = mfma32(tr_frag<D>(Oc, 32 * rb + 16 * v, 32 * db, lane), pb, dv[db]);
+          dk[db] = mfma32(tr_frag<D>(Qc, 32 * rb + 16 * v, 32 * db, lane), sb, dk[db]);
+        }
       }
     }
+  };
+
+  if (ntiles > 0) issue(0, Q0, O0, L0, E0);
+  tile_barrier();
+  for (int t = 0; t < ntiles; t += 2) {
+    if (t + 1 < ntiles) issue(t + 1, Q1, O1, L1, E1);
     compiler_fence();
-    if (t + 1 < ntiles) stage_store(buf ^ 1);
-    __syncthreads();
+    compute(t, Q0, O0, L0, E0);
+    tile_barrier();
+    if (t + 1 >= ntiles) break;
+    if (t + 2 < ntiles) issue(t + 2, Q0, O0, L0, E0);
+    compiler_fence();
+    compute(t + 1, Q1, O1, L1, E1);
+    tile_barrier();
   }
 
-  // ---- epilogue: dk[db][i] is key 32 w + 8 (i/4) + 4 h + i%4, d = 32 db + r
+  // ---- epilogue: dk[db][i] is dK^T[d = 32 db + c_row(i, h)][key wave_k0 + r]
+  if (wave_k0 + r >= kseg) return;
+  const int key = wave_k0 + r;
+  if (kpre) {
+    const size_t off = ((size_t)key * a.hkv + hk) * D + 4 * h;
+    if (a.pk_mode == kPkAccumulate) {
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const int key = k0 + 32 * w + 8 * (i >> 2) + 4 * h + (i & 3);
-    if (key >= kseg) continue;
-    if (kpre) {
-      const size_t off = ((size_t)key * a.hkv + hk) * D + r;
-      if (a.pk_mode == kPkAccumulate) {
+      for (int db = 0; db < NDB; ++db)
 #pragma unroll
-        for (int db = 0; db < NDB; ++db) {
-          a.gk[off + 32 * db] += dk[db][i] * a.scale;
-          a.gv[off + 32 * db] += dv[db][i];
+        for (int g4 = 0; g4 < 4; ++g4) {
+          float4* pk = (float4*)(a.gk + off + 32 * db + 8 * g4);
+          float4* pv = (float4*)(a.gv + off + 32 * db + 8 * g4);
+          float4 ck = *pk, cv = *pv;
+          ck.x += dk[db][4 * g4] * a.scale;
+          ck.y += dk[db][4 * g4 + 1] * a.scale;
+          ck.z += dk[db][4 * g4 + 2] * a.scale;
+          ck.w += dk[db][4 * g4 + 3] * a.scale;
+          cv.x += dv[db][4 * g4];
+          cv.y += dv[db][4 * g4 + 1];
+          cv.z += dv[db][4 * g4 + 2];
+          cv.w += dv[db][4 * g4 + 3];
+          *pk = ck;
+          *pv = cv;
         }
-      } else {
-        bf16* okp = (bf16*)a.dk_p;
-        bf16* ovp = (bf16*)a.dv_p;
-#pragma unroll
-        for (int db = 0; db < NDB; ++db) {
-          okp[off + 32 * db] = (bf16)(dk[db][i] * a.scale + a.gk[off + 32 * db]);
-          ovp[off + 32 * db] = (bf16)(dv[db][i] + a.gv[off + 32 * db]);
-        }
-      }
     } else {
-      const size_t off = ((size_t)(kbase + key) * a.hkv + hk) * D + r;
-      bf16* oks = (bf16*)a.dk_s;
-      bf16* ovs = (bf16*)a.dv_s;
+      bf16* okp = (bf16*)a.dk_p;
+      bf16* ovp = (bf16*)a.dv_p;
 #pragma unroll
-      for (int db = 0; db < NDB; ++db) {
-        oks[off + 32 * db] = (bf16)(dk[db][i] * a.scale);
-        ovs[off + 32 * db] = (bf16)dv[db][i];
-      }
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int g4 = 0; g4 < 4; ++g4) {
+          const float4 ck = *(const float4*)(a.gk + off + 32 * db + 8 * g4);
+          const float4 cv = *(const float4*)(a.gv + off + 32 * db + 8 * g4);
+          const bf16x4 vk = {(bf16)(dk[db][4 * g4] * a.scale + ck.x),
+                             (bf16)(dk[db][4 * g4 + 1] * a.scale + ck.y),
+                             (bf16)(dk[db][4 * g4 + 2] * a.scale + ck.z),
+                             (bf16)(dk[db][4 * g4 + 3] * a.scale + ck.w)};
+          const bf16x4 vv = {(bf16)(dv[db][4 * g4] + cv.x), (bf16)(dv[db][4 * g4 + 1] + cv.y),
+                             (bf16)(dv[db][4 * g4 + 2] + cv.z), (bf16)(dv[db][4 * g4 + 3] + cv.w)};
+          *(bf16x4*)(okp + off + 32 * db + 8 * g4) = vk;
+          *(bf16x4*)(ovp + off + 32 * db + 8 * g4) = vv;
+        }
     }
+  } else {
+    const size_t off = ((size_t)(kbase + key) * a.hkv + hk) * D + 4 * h;
+    bf16* oks = (bf16*)a.dk_s;
+    bf16* ovs = (bf16*)a.dv_s;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        const bf16x4 vk = {(bf16)(dk[db][4 * g4] * a.scale), (bf16)(dk[db][4 * g4 + 1] * a.scale),
+                           (bf16)(dk[db][4 * g4 + 2] * a.scale), (bf16)(dk[db][4 * g4 + 3] * a.scale)};
+        const bf16x4 vv = {(bf16)dv[db][4 * g4], (bf16)dv[db][4 * g4 + 1], (bf16)dv[db][4 * g4 + 2],
+                           (bf16)dv[db][4 * g4 + 3]};
+        *(bf16x4*)(oks + off + 32 * db + 8 * g4) = vk;
+        *(bf16x4*)(ovs + off + 32 * db + 8 * g4) = vv;
+      }
   }
 }
 
 // ----------------------------------------------------------------- bwd_q
+struct QBlock {
+  int tile, z, hq;
+};
+__device__ __forceinline__ QBlock decode_q_block(const AttnArgs& a, int ntx) {
+  const int G = a.hq / a.hkv;
+  int b = blockIdx.x;
+  const int hk = b % a.hkv;
+  b /= a.hkv;
+  const int gi = b % G;
+  b /= G;
+  QBlock qb;
+  qb.tile = ntx - 1 - b % ntx;  // rows with the most keys first
+  qb.z = b / ntx;
+  qb.hq = hk * G + gi;
+  return qb;
+}
+
 template <int D>
-__global__ __launch_bounds__(kBwdThreads) void bwd_q_bf16_kernel(AttnArgs a) {
-  using TG = TileGeom<D>;
-  constexpr int BQ = kQBQ, BK = kQBK;
+__global__ __launch_bounds__(kThreads, 2) void bwd_q_bf16_kernel(AttnArgs a) {
   constexpr int NS = D / 16;
   constexpr int NDB = D / 32;
-  __shared__ __attribute__((aligned(16))) bf16 Kn[2][TG::NAT];
-  __shared__ __attribute__((aligned(16))) bf16 Vn[2][TG::NAT];
-  __shared__ __attribute__((aligned(16))) bf16 Kt[2][TG::TRN];
+  constexpr int TE = Tile<D>::ELEMS, BK = kTileRows;
+  __shared__ __attribute__((aligned(1024))) bf16 K0[TE];
+  __shared__ __attribute__((aligned(1024))) bf16 K1[TE];
+  __shared__ __attribute__((aligned(1024))) bf16 V0[TE];
+  __shared__ __attribute__((aligned(1024))) bf16 V1[TE];
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int r = lane & 31, h = lane >> 5;
 
-  const int tile = gridDim.x - 1 - blockIdx.x;  // rows with the most keys first
-  const int seq = a.seq_base + blockIdx.z;
+  const QBlock blk = decode_q_block(a, a.n_prefix_q_tiles + a.n_suffix_q_tiles);
+  const int seq = a.seq_base + blk.z;
   bool prefix_rows;
   int lp0, seg_len, row_base;
-  if (tile < a.n_prefix_q_tiles) {
+  if (blk.tile < a.n_prefix_q_tiles) {
     prefix_rows = true;
-    lp0 = tile * BQ;
+    lp0 = blk.tile * kQBQ;
     seg_len = a.P;
     row_base = 0;
   } else {
     prefix_rows = false;
-    lp0 = (tile - a.n_prefix_q_tiles) * BQ;
+    lp0 = (blk.tile - a.n_prefix_q_tiles) * kQBQ;
     row_base = a.cu[seq];
     seg_len = a.cu[seq + 1] - row_base;
   }
   if (lp0 >= seg_len) return;
-  const int hq = blockIdx.y, hk = hq / (a.hq / a.hkv);
+  const int hq = blk.hq, hk = hq / (a.hq / a.hkv);
   const int wave_lp0 = lp0 + 32 * w;
-  const int my_lp = wave_lp0 + r;
-  const bool row_valid = my_lp < seg_len;
+  const int row_lp = wave_lp0 + r;
+  const bool row_valid = row_lp < seg_len;
+  const int my_lp = row_valid ? row_lp : seg_len - 1;
 
   // Q, dO as the B operands of S^T = K Q^T and dP^T = V dO^T
   bf16x8 qf[NS], df[NS];
-  float lse2 = 0.f, drow = 0.f;
+  float lse2, drow;
   {
     const bf16* qb = (const bf16*)(prefix_rows ? a.q_p : a.q_s);
-    const bf16* db = (const bf16*)(prefix_rows ? a.do_p : a.do_s);
-    const size_t row = (size_t)(row_base + (row_valid ? my_lp : 0));
+    const bf16* dob = (const bf16*)(prefix_rows ? a.do_p : a.do_s);
+    const size_t row = (size_t)(row_base + my_lp);
     const size_t off = (row * a.hq + hq) * D + 8 * h;
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      qf[s] = row_valid ? *(const bf16x8*)(qb + off + 16 * s) : zero_bf8();
-      df[s] = row_valid ? *(const bf16x8*)(db + off + 16 * s) : zero_bf8();
+      qf[s] = *(const bf16x8*)(qb + off + 16 * s);
+      df[s] = *(const bf16x8*)(dob + off + 16 * s);
     }
-    if (row_valid) {
-      lse2 = (prefix_rows ? a.lse_p : a.lse_s)[row * a.hq + hq] * kLog2e;
-      drow = (prefix_rows ? a.dd_p : a.dd_s)[row * a.hq + hq];
-    }
+    lse2 = (prefix_rows ? a.lse_p : a.lse_s)[row * a.hq + hq] * kLog2e;
+    drow = (prefix_rows ? a.dd_p : a.dd_s)[row * a.hq + hq];
   }
   f32x16 dq[NDB];
 #pragma unroll
   for (int db = 0; db < NDB; ++db) dq[db] = zero16();
 
-  const int last_lp = min(lp0 + BQ, seg_len) - 1;
+  const int last_lp = min(lp0 + kQBQ, seg_len) - 1;
   const int nkeys0 = prefix_rows ? min(a.P, last_lp + 1) : a.P;
   const int nkeys1 = prefix_rows ? 0 : last_lp + 1;
   const int nt0 = (nkeys0 + BK - 1) / BK, nt1 = (nkeys1 + BK - 1) / BK;
   const int ntiles = nt0 + nt1;
-  auto tile_info = [&](int t, int& seg, int& k0, int& nk) {
-    seg = t < nt0 ? 0 : 1;
-    k0 = (seg == 0 ? t : t - nt0) * BK;
-    nk = min(BK, (seg == 0 ? nkeys0 : nkeys1) - k0);
-  };
-  Stager<D> sk, sv;
-  auto stage_load = [&](int t) {
-    int seg, k0, nk;
-    tile_info(t, seg, k0, nk);
-    const bf16* kb = (const bf16*)(seg == 0 ? a.k_p : a.k_s);
-    const bf16* vb = (const bf16*)(seg == 0 ? a.v_p : a.v_s);
-    const int kbase = seg == 0 ? 0 : row_base;
-    sk.load(kb, kbase + k0, nk, a.hkv, hk, tid);
-    sv.load(vb, kbase + k0, nk, a.hkv, hk, tid);
-  };
-  auto stage_store = [&](int buf) {
-    sk.store_nat(Kn[buf], tid);
-    sk.store_trn(Kt[buf], tid);
-    sv.store_nat(Vn[buf], tid);
-  };
-  if (ntiles > 0) {
-    stage_load(0);
-    stage_store(0);
-  }
-  __syncthreads();
 
-  const int k_off = nat_off<D>(r, 0, h);  // A-operand reads: LDS row 32 kb + r
-  for (int t = 0; t < ntiles; ++t) {
-    const int buf = t & 1;
-    if (t + 1 < ntiles) stage_load(t + 1);  // global loads in flight during the MFMAs
-    int seg, k0, nk;
-    tile_info(t, seg, k0, nk);
+  auto issue = [&](int t, bf16* Kd, bf16* Vd) {
+    const int seg = t < nt0 ? 0 : 1;
+    const int k0 = (seg == 0 ? t : t - nt0) * BK;
+    const int nk = min(BK, (seg == 0 ? nkeys0 : nkeys1) - k0);
+    const int kbase = seg == 0 ? 0 : row_base;
+    load_tile<D>(Kd, (const bf16*)(seg == 0 ? a.k_p : a.k_s), kbase + k0, nk, a.hkv, hk, w, lane);
+    load_tile<D>(Vd, (const bf16*)(seg == 0 ? a.v_p : a.v_s), kbase + k0, nk, a.hkv, hk, w, lane);
+  };
+
+  auto compute = [&](int t, const bf16* Kc, const bf16* Vc) {
+    const int seg = t < nt0 ? 0 : 1;
+    const int k0 = (seg == 0 ? t : t - nt0) * BK;
+    const int nk = min(BK, (seg == 0 ? nkeys0 : nkeys1) - k0);
     const bool causal = (seg == 0) == prefix_rows;
-    if (!(causal && k0 > wave_lp0 + 31)) {  // else no row of this wave sees the tile
-      const bf16* Kb = Kn[buf] + k_off;
-      const bf16* Vb = Vn[buf] + k_off;
-      // st[kb][i] = S^T[key k0 + 32 kb + c_row(i, h)][row my_lp]; pt = dP^T
-      f32x16 st[BK / 32], pt[BK / 32];
+    if (causal && k0 > wave_lp0 + 31) return;  // no row of this wave sees the tile
+    // st[kb][i] = S^T[key k0 + 32 kb + c_row(i, h)][row my_lp]; pt = dP^T
+    f32x16 st[2] = {zero16(), zero16()}, pt[2] = {zero16(), zero16()};
 #pragma unroll
-      for (int kb = 0; kb < BK / 32; ++kb) {
-        st[kb] = zero16();
-        pt[kb] = zero16();
+    for (int s = 0; s < NS; ++s)
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        st[kb] = mfma32(row_frag<D>(Kc, 32 * kb + r, 16 * s + 8 * h), qf[s], st[kb]);
+        pt[kb] = mfma32(row_frag<D>(Vc, 32 * kb + r, 16 * s + 8 * h), df[s], pt[kb]);
       }
+    const bool need_mask = nk < BK || (causal && k0 + BK - 1 > wave_lp0);
+    const int lim = causal ? min(nk, my_lp - k0 + 1) : nk;  // keys kk < lim are visible
 #pragma unroll
-      for (int s = 0; s < NS; ++s)
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-        for (int kb = 0; kb < BK / 32; ++kb) {
-          st[kb] = mfma32(lds8(Kb, nat_off<D>(32 * kb, 16 * s, 0)), qf[s], st[kb]);
-          pt[kb] = mfma32(lds8(Vb, nat_off<D>(32 * kb, 16 * s, 0)), df[s], pt[kb]);
-        }
-      // keys kk < lim are visible to this lane's row
-      const int lim = !row_valid ? 0 : (causal ? min(nk, my_lp - k0 + 1) : nk);
-#pragma unroll
-      for (int kb = 0; kb < BK / 32; ++kb)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int kk = 32 * kb + c_row(i, h);
-          const float p = fast_exp2(fmaf(st[kb][i], a.scale_log2, -lse2));
-          pt[kb][i] = kk < lim ? p * (pt[kb][i] - drow) : 0.f;  // dS^T
-        }
-      // dQ^T += K^T dS^T over 16-key steps u: keys 16 u + 8 h + 0..7
-#pragma unroll
-      for (int u = 0; u < BK / 16; ++u) {
-        const bf16x8 sb = c_to_kfrag(pt[u >> 1], u & 1);
-#pragma unroll
-        for (int db = 0; db < NDB; ++db)
-          dq[db] = mfma32(lds8(Kt[buf], trn_off(32 * db + r, u, h)), sb, dq[db]);
+      for (int i = 0; i < 16; ++i) {
+        float p = fast_exp2(fmaf(st[kb][i], a.scale_log2, -lse2));
+        if (need_mask) p = 32 * kb + c_row(i, h) < lim ? p : 0.f;
+        pt[kb][i] = p * (pt[kb][i] - drow);  // dS^T
       }
+    // dQ^T += K^T dS^T over 16-key steps u (C-order keys)
+#pragma unroll
+    for (int u = 0; u < BK / 16; ++u) {
+      const bf16x8 sb = c_kfrag(pt[u >> 1], u & 1);
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) dq[db] = mfma32(tr_frag<D>(Kc, 16 * u, 32 * db, lane), sb, dq[db]);
     }
+  };
+
+  if (ntiles > 0) issue(0, K0, V0);
+  tile_barrier();
+  for (int t = 0; t < ntiles; t += 2) {
+    if (t + 1 < ntiles) issue(t + 1, K1, V1);
     compiler_fence();
-    if (t + 1 < ntiles) stage_store(buf ^ 1);
-    __syncthreads();
+    compute(t, K0, V0);
+    tile_barrier();
+    if (t + 1 >= ntiles) break;
+    if (t + 2 < ntiles) issue(t + 2, K0, V0);
+    compiler_fence();
+    compute(t + 1, K1, V1);
+    tile_barrier();
   }
 
   if (!row_valid) return;
-  // dq[db][i] = dQ^T[d = 32 db + 8 (i/4) + 4 h + i%4][row my_lp] (unscaled)
+  // dq[db][i] = dQ^T[d = 32 db + c_row(i, h)][row my_lp] (unscaled)
   const size_t off = ((size_t)(row_base + my_lp) * a.hq + hq) * D + 4 * h;
   if (prefix_rows && a.dq_p_accumulate) {
     // dense baseline: the prefix rows' dQ sums over the trajectories
@@ -446,24 +448,24 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, int head_dim, int n_qz, bool deter
                            hipStream_t st) {
   (void)deterministic;  // both kernels are deterministic: no atomics anywhere
   {
-    const dim3 grid(a.n_prefix_k_tiles + a.n_seq * a.n_suffix_k_tiles, a.hkv, 1);
-    if (grid.x > 0) {
+    const long nb = (long)(a.n_prefix_k_tiles + a.n_seq * a.n_suffix_k_tiles) * a.hkv;
+    if (nb > 0) {
       ProfileScope ps("bwd_kv_bf16", st);
       if (head_dim == 64)
-        hipLaunchKernelGGL(bwd_kv_bf16_kernel<64>, grid, dim3(kBwdThreads), 0, st, a);
+        hipLaunchKernelGGL(bwd_kv_bf16_kernel<64>, dim3((unsigned)nb), dim3(kThreads), 0, st, a);
       else
-        hipLaunchKernelGGL(bwd_kv_bf16_kernel<128>, grid, dim3(kBwdThreads), 0, st, a);
+        hipLaunchKernelGGL(bwd_kv_bf16_kernel<128>, dim3((unsigned)nb), dim3(kThreads), 0, st, a);
       const hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
     }
   }
-  const dim3 grid(a.n_prefix_q_tiles + a.n_suffix_q_tiles, a.hq, n_qz);
-  if (grid.x == 0 || n_qz == 0) return hipSuccess;
+  const long nb = (long)(a.n_prefix_q_tiles + a.n_suffix_q_tiles) * a.hq * n_qz;
+  if (nb == 0) return hipSuccess;
   ProfileScope ps("bwd_q_bf16", st);
   if (head_dim == 64)
-    hipLaunchKernelGGL(bwd_q_bf16_kernel<64>, grid, dim3(kBwdThreads), 0, st, a);
+    hipLaunchKernelGGL(bwd_q_bf16_kernel<64>, dim3((unsigned)nb), dim3(kThreads), 0, st, a);
   else
-    hipLaunchKernelGGL(bwd_q_bf16_kernel<128>, grid, dim3(kBwdThreads), 0, st, a);
+    hipLaunchKernelGGL(bwd_q_bf16_kernel<128>, dim3((unsigned)nb), dim3(kThreads), 0, st, a);
   return hipGetLastError();
 }
 

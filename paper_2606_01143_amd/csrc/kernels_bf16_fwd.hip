@@ -7,17 +7,16 @@
 // (H_2 = P_21 V_1 + P_22 V_2), plus the row's natural-log LSE.
 //
 // Structure: one workgroup = 4 waves = 128 query rows of one q head; each
-// wave owns 32 rows.  Keys stream through LDS in tiles of 64, first the
-// prefix tiles (read in place from K_P/V_P), then the suffix's own tiles,
-// double-buffered: the next tile's global loads are in flight while the
-// current one is multiplied.  An online softmax carries the row max and
-// sum across tiles.  Per tile and wave (v_mfma_f32_32x32x16_bf16):
-//   S^T (64 keys x 32 rows) = K Q^T   A = K rows (natural tile), B = Q (registers)
-//   O^T (d x 32 rows)      += V^T P^T  A = V columns (transposed tile),
+// wave owns 32 rows.  Keys stream through LDS in 64-row tiles, first the
+// prefix tiles (read in place from K_P/V_P), then the suffix's own tiles.
+// Tiles are double-buffered: the next tile's direct-to-LDS loads are issued
+// before the current tile's products.  Per tile and wave
+// (v_mfma_f32_32x32x16_bf16, operand conventions in tile.hpp):
+//   S^T (64 keys x 32 rows) = K Q^T   A = K tile rows, B = Q (registers)
+//   O^T (d x 32 rows)      += V^T P^T  A = V tile read transposed,
 //                                      B = P^T straight from the S^T registers
-// Computing S^T leaves each lane holding 16 keys of one query row: the row
-// max/sum need one cross-lane exchange, and the keys already sit in the
-// B-operand slots of the PV product.
+// With S^T each lane holds 16 keys of ONE query row, so the online softmax
+// needs a single cross-lane exchange per statistic.
 #include "common.hpp"
 #include "launch.hpp"
 #include "tile.hpp"
@@ -26,160 +25,161 @@ namespace spr {
 
 namespace {
 constexpr int kFwdBQ = 128;
-constexpr int kFwdBK = 64;
-constexpr int kFwdThreads = 256;
 }  // namespace
 
 int fwd_bf16_block_q() { return kFwdBQ; }
 
+// Query-outer grids are 1D: block b -> (kv head b % Hkv, q head of that kv
+// group, row tile, suffix).  Workgroups are dispatched round-robin over the
+// eight XCDs, so every block of one kv head lands on the same XCD (for
+// Hkv dividing 8) and the K/V it streams stays in that XCD's L2.
+struct RowBlock {
+  int tile, z, hq;
+};
+__device__ __forceinline__ RowBlock decode_row_block(const AttnArgs& a, int ntx) {
+  const int G = a.hq / a.hkv;
+  int b = blockIdx.x;
+  const int hk = b % a.hkv;
+  b /= a.hkv;
+  const int gi = b % G;
+  b /= G;
+  RowBlock rb;
+  rb.tile = ntx - 1 - b % ntx;  // rows with the most keys first
+  rb.z = b / ntx;
+  rb.hq = hk * G + gi;
+  return rb;
+}
+
 template <int D>
-__global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(AttnArgs a) {
-  using TG = TileGeom<D>;
-  constexpr int BQ = kFwdBQ, BK = kFwdBK;
+__global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(AttnArgs a) {
   constexpr int NS = D / 16;   // k-steps over d for S^T
   constexpr int NDB = D / 32;  // 32-wide d blocks of O^T
-  __shared__ __attribute__((aligned(16))) bf16 Kn[2 * TG::NAT];
-  __shared__ __attribute__((aligned(16))) bf16 Vt[2 * TG::TRN];
+  constexpr int TE = Tile<D>::ELEMS, BK = kTileRows;
+  __shared__ __attribute__((aligned(1024))) bf16 K0[TE];
+  __shared__ __attribute__((aligned(1024))) bf16 K1[TE];
+  __shared__ __attribute__((aligned(1024))) bf16 V0[TE];
+  __shared__ __attribute__((aligned(1024))) bf16 V1[TE];
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int r = lane & 31, h = lane >> 5;
 
   // ---- which 128 query rows: prefix rows, or rows of suffix seq_base + z
-  const int tile = gridDim.x - 1 - blockIdx.x;  // rows with the most keys first
-  const int seq = a.seq_base + blockIdx.z;
+  const RowBlock blk = decode_row_block(a, a.n_prefix_q_tiles + a.n_suffix_q_tiles);
+  const int seq = a.seq_base + blk.z;
   bool prefix_rows;
   int lp0, seg_len, row_base;
-  if (tile < a.n_prefix_q_tiles) {
+  if (blk.tile < a.n_prefix_q_tiles) {
     prefix_rows = true;
-    lp0 = tile * BQ;
+    lp0 = blk.tile * kFwdBQ;
     seg_len = a.P;
     row_base = 0;
   } else {
     prefix_rows = false;
-    lp0 = (tile - a.n_prefix_q_tiles) * BQ;
+    lp0 = (blk.tile - a.n_prefix_q_tiles) * kFwdBQ;
     row_base = a.cu[seq];
     seg_len = a.cu[seq + 1] - row_base;
   }
   if (lp0 >= seg_len) return;
-  const int hq = blockIdx.y, hk = hq / (a.hq / a.hkv);
+  const int hq = blk.hq, hk = hq / (a.hq / a.hkv);
   const int wave_lp0 = lp0 + 32 * w;  // first row of this wave
-  const int my_lp = wave_lp0 + r;     // this lane's query row (segment-local)
-  const bool row_valid = my_lp < seg_len;
+  const int row_lp = wave_lp0 + r;    // this lane's query row (segment-local)
+  const bool row_valid = row_lp < seg_len;
+  const int my_lp = row_valid ? row_lp : seg_len - 1;  // rows past the end recompute the last one
 
   // Q as the B operand of S^T = K Q^T: slot (h, j) of k-step s is d = 16 s + 8 h + j
   bf16x8 qf[NS];
   {
     const bf16* qb = (const bf16*)(prefix_rows ? a.q_p : a.q_s);
-    const size_t off = ((size_t)(row_base + (row_valid ? my_lp : 0)) * a.hq + hq) * D + 8 * h;
+    const size_t off = ((size_t)(row_base + my_lp) * a.hq + hq) * D + 8 * h;
 #pragma unroll
-    for (int s = 0; s < NS; ++s) qf[s] = row_valid ? *(const bf16x8*)(qb + off + 16 * s) : zero_bf8();
+    for (int s = 0; s < NS; ++s) qf[s] = *(const bf16x8*)(qb + off + 16 * s);
   }
   f32x16 o[NDB];
 #pragma unroll
   for (int db = 0; db < NDB; ++db) o[db] = zero16();
   float m = -INFINITY, l = 0.f;  // running max (log2 domain) and sum of row my_lp
 
-  // LDS offsets of this lane's fragments: K rows at k_off + immediates; the
-  // V column of d block db is v_col + db * 32 * kTileRows, its 16-key step u
-  // at chunk (2 u + h) ^ trn_swz(32 db + r)
-  const int k_off = nat_off<D>(r, 0, h);
-  const int v_col = r * kTileRows;
-
   // key tiles: prefix keys first (causal for prefix rows), then own suffix keys
-  const int last_lp = min(lp0 + BQ, seg_len) - 1;
+  const int last_lp = min(lp0 + kFwdBQ, seg_len) - 1;
   const int nkeys0 = prefix_rows ? min(a.P, last_lp + 1) : a.P;
   const int nkeys1 = prefix_rows ? 0 : last_lp + 1;
   const int nt0 = (nkeys0 + BK - 1) / BK, nt1 = (nkeys1 + BK - 1) / BK;
   const int ntiles = nt0 + nt1;
-  auto tile_info = [&](int t, int& seg, int& k0, int& nk) {
-    seg = t < nt0 ? 0 : 1;
-    k0 = (seg == 0 ? t : t - nt0) * BK;
-    nk = min(BK, (seg == 0 ? nkeys0 : nkeys1) - k0);
-  };
-  Stager<D> sk, sv;
-  auto stage_load = [&](int t) {
-    int seg, k0, nk;
-    tile_info(t, seg, k0, nk);
-    const bf16* kb = (const bf16*)(seg == 0 ? a.k_p : a.k_s);
-    const bf16* vb = (const bf16*)(seg == 0 ? a.v_p : a.v_s);
-    const int kbase = seg == 0 ? 0 : row_base;
-    sk.load(kb, kbase + k0, nk, a.hkv, hk, tid);
-    sv.load(vb, kbase + k0, nk, a.hkv, hk, tid);
-  };
-  if (ntiles > 0) {
-    stage_load(0);
-    sk.store_nat(Kn, tid);
-    sv.store_trn(Vt, tid);
-  }
-  __syncthreads();
 
-  for (int t = 0; t < ntiles; ++t) {
-    const int buf = t & 1;
-    if (t + 1 < ntiles) stage_load(t + 1);  // global loads in flight during the MFMAs
-    int seg, k0, nk;
-    tile_info(t, seg, k0, nk);
+  auto issue = [&](int t, bf16* Kd, bf16* Vd) {
+    const int seg = t < nt0 ? 0 : 1;
+    const int k0 = (seg == 0 ? t : t - nt0) * BK;
+    const int nk = min(BK, (seg == 0 ? nkeys0 : nkeys1) - k0);
+    const int kbase = seg == 0 ? 0 : row_base;
+    load_tile<D>(Kd, (const bf16*)(seg == 0 ? a.k_p : a.k_s), kbase + k0, nk, a.hkv, hk, w, lane);
+    load_tile<D>(Vd, (const bf16*)(seg == 0 ? a.v_p : a.v_s), kbase + k0, nk, a.hkv, hk, w, lane);
+  };
+
+  auto compute = [&](int t, const bf16* Kc, const bf16* Vc) {
+    const int seg = t < nt0 ? 0 : 1;
+    const int k0 = (seg == 0 ? t : t - nt0) * BK;
+    const int nk = min(BK, (seg == 0 ? nkeys0 : nkeys1) - k0);
     const bool causal = (seg == 0) == prefix_rows;  // keys of the row's own segment
-    if (!(causal && k0 > wave_lp0 + 31)) {          // else no row of this wave sees the tile
-      const bf16* Kb = Kn + buf * TG::NAT + k_off;
-      const bf16* Vb = Vt + buf * TG::TRN;
-      // S^T = K Q^T ; st[kb][i] = S^T[key k0 + 32 kb + c_row(i, h)][row my_lp]
-      f32x16 st[BK / 32];
+    if (causal && k0 > wave_lp0 + 31) return;       // no row of this wave sees the tile
+    // S^T = K Q^T ; st[kb][i] = S^T[key k0 + 32 kb + c_row(i, h)][row my_lp]
+    f32x16 st[2] = {zero16(), zero16()};
 #pragma unroll
-      for (int kb = 0; kb < BK / 32; ++kb) st[kb] = zero16();
+    for (int s = 0; s < NS; ++s)
 #pragma unroll
-      for (int s = 0; s < NS; ++s)  // independent chains interleaved
-#pragma unroll
-        for (int kb = 0; kb < BK / 32; ++kb)
-          st[kb] = mfma32(lds8(Kb, nat_off<D>(32 * kb, 16 * s, 0)), qf[s], st[kb]);
+      for (int kb = 0; kb < 2; ++kb) st[kb] = mfma32(row_frag<D>(Kc, 32 * kb + r, 16 * s + 8 * h), qf[s], st[kb]);
 #define SC(e) st[(e) >> 4][(e) & 15]
-      if (nk < BK || (causal && k0 + BK - 1 > wave_lp0)) {  // partial or diagonal tile
-        const int lim = causal ? min(nk, my_lp - k0 + 1) : nk;  // keys kk < lim are visible
+    if (nk < BK || (causal && k0 + BK - 1 > wave_lp0)) {  // partial or diagonal tile
+      const int lim = causal ? min(nk, my_lp - k0 + 1) : nk;  // keys kk < lim are visible
 #pragma unroll
-        for (int e = 0; e < BK / 2; ++e) SC(e) = 32 * (e >> 4) + c_row(e & 15, h) < lim ? SC(e) : -INFINITY;
-      }
-      float mt = -INFINITY;
+      for (int e = 0; e < 32; ++e) SC(e) = 32 * (e >> 4) + c_row(e & 15, h) < lim ? SC(e) : -INFINITY;
+    }
+    float mt = -INFINITY;
 #pragma unroll
-      for (int e = 0; e < BK / 2; ++e) mt = fmaxf(mt, SC(e));
-      mt = fmaxf(mt, __shfl_xor(mt, 32)) * a.scale_log2;
-      const float mn = fmaxf(m, mt);
-      const float mu = mn == -INFINITY ? 0.f : mn;
-      if (__builtin_expect(__any(mn > m), 0)) {  // rescale only when some row's max grew
-        const float corr = fast_exp2(m - mu);
-        l *= corr;
+    for (int e = 0; e < 32; ++e) mt = fmaxf(mt, SC(e));
+    mt = fmaxf(mt, __shfl_xor(mt, 32)) * a.scale_log2;
+    const float mn = fmaxf(m, mt);
+    const float mu = mn == -INFINITY ? 0.f : mn;
+    if (__builtin_expect(__any(mn > m), 0)) {  // rescale only when some row's max grew
+      const float corr = fast_exp2(m - mu);
+      l *= corr;
 #pragma unroll
-        for (int db = 0; db < NDB; ++db) o[db] *= corr;
-      }
-      m = mn;
-      float rs = 0.f;
+      for (int db = 0; db < NDB; ++db) o[db] *= corr;
+    }
+    m = mn;
+    float rs = 0.f;
 #pragma unroll
-      for (int e = 0; e < BK / 2; ++e) {
-        SC(e) = fast_exp2(fmaf(SC(e), a.scale_log2, -mu));
-        rs += SC(e);
-      }
-      rs += __shfl_xor(rs, 32);
-      l += rs;
+    for (int e = 0; e < 32; ++e) {
+      SC(e) = fast_exp2(fmaf(SC(e), a.scale_log2, -mu));
+      rs += SC(e);
+    }
 #undef SC
-      // O^T += V^T P^T over 16-key steps u: keys 16 u + 8 h + 0..7
+    rs += __shfl_xor(rs, 32);
+    l += rs;
+    // O^T += V^T P^T over 16-key steps u (C-order keys 16 u + k(h, j))
 #pragma unroll
-      for (int u = 0; u < BK / 16; ++u) {
-        const bf16x8 pb = c_to_kfrag(st[u >> 1], u & 1);
+    for (int u = 0; u < BK / 16; ++u) {
+      const bf16x8 pb = c_kfrag(st[u >> 1], u & 1);
 #pragma unroll
-        for (int db = 0; db < NDB; ++db)
-          o[db] = mfma32(lds8(Vb, v_col + db * 32 * kTileRows +
-                                      8 * ((2 * u + h) ^ trn_swz(32 * db + r))),
-                         pb, o[db]);
-      }
+      for (int db = 0; db < NDB; ++db) o[db] = mfma32(tr_frag<D>(Vc, 16 * u, 32 * db, lane), pb, o[db]);
     }
+  };
+
+  if (ntiles > 0) issue(0, K0, V0);
+  tile_barrier();
+  for (int t = 0; t < ntiles; t += 2) {
+    if (t + 1 < ntiles) issue(t + 1, K1, V1);
     compiler_fence();
-    if (t + 1 < ntiles) {
-      sk.store_nat(Kn + (buf ^ 1) * TG::NAT, tid);
-      sv.store_trn(Vt + (buf ^ 1) * TG::TRN, tid);
-    }
-    __syncthreads();
+    compute(t, K0, V0);
+    tile_barrier();
+    if (t + 1 >= ntiles) break;
+    if (t + 2 < ntiles) issue(t + 2, K0, V0);
+    compiler_fence();
+    compute(t + 1, K1, V1);
+    tile_barrier();
   }
 
   if (!row_valid) return;
-  // o[db][i] = O^T[d = 32 db + 8 (i/4) + 4 h + i%4][row my_lp]
+  // o[db][i] = O^T[d = 32 db + c_row(i, h)][row my_lp]
   const float inv = 1.f / l;
   bf16* ob = (bf16*)(prefix_rows ? a.o_p : a.o_s);
   const size_t off = ((size_t)(row_base + my_lp) * a.hq + hq) * D + 4 * h;
@@ -198,13 +198,13 @@ __global__ __launch_bounds__(kFwdThreads) void fwd_bf16_kernel(AttnArgs a) {
 }
 
 hipError_t launch_fwd_bf16(const AttnArgs& a, int head_dim, int n_z, hipStream_t st) {
-  const dim3 grid(a.n_prefix_q_tiles + a.n_suffix_q_tiles, a.hq, n_z);
-  if (grid.x == 0 || n_z == 0) return hipSuccess;
+  const long nb = (long)(a.n_prefix_q_tiles + a.n_suffix_q_tiles) * a.hq * n_z;
+  if (nb == 0) return hipSuccess;
   ProfileScope ps("fwd_bf16", st);
   if (head_dim == 64)
-    hipLaunchKernelGGL(fwd_bf16_kernel<64>, grid, dim3(kFwdThreads), 0, st, a);
+    hipLaunchKernelGGL(fwd_bf16_kernel<64>, dim3((unsigned)nb), dim3(kThreads), 0, st, a);
   else
-    hipLaunchKernelGGL(fwd_bf16_kernel<128>, grid, dim3(kFwdThreads), 0, st, a);
+    hipLaunchKernelGGL(fwd_bf16_kernel<128>, dim3((unsigned)nb), dim3(kThreads), 0, st, a);
   return hipGetLastError();
 }
 

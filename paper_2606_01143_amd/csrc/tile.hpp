@@ -1,35 +1,31 @@
-// LDS tile layouts and gfx950 matrix-core fragments shared by the bf16
-// kernels.
+// LDS tiles and gfx950 matrix-core fragments shared by the bf16 kernels.
 //
 // v_mfma_f32_32x32x16_bf16 operand layout (lane l, r = l % 32, h = l / 32):
-//   A (32 x 16): element j of lane l is A[r][8 h + j]
-//   B (16 x 32): element j of lane l is B[8 h + j][r]
-//   C (32 x 32): element i of lane l is C[8 (i / 4) + 4 h + i % 4][r]
-// The contraction only needs A and B to agree on which k each (h, j) slot
-// holds.
+//   A (32 x 16): slot j of lane l holds A[r][k(h, j)]
+//   B (16 x 32): slot j of lane l holds B[k(h, j)][r]
+//   C (32 x 32): element i of lane l holds C[8 (i / 4) + 4 h + i % 4][r]
+// A and B only have to agree on which k each slot (h, j) stands for.  Two
+// k orders are used:
+//   natural    k(h, j) = 8 h + j, for products that contract over the head
+//              dimension d: the operand is 16 contiguous bytes of one tile
+//              row (one ds_read_b128) or of a register-resident row;
+//   C-order    k(h, j) = 4 h + j (j < 4), 8 + 4 h + j - 4 (j >= 4), for
+//              products that contract over rows of a previous C result
+//              (P V, dS K, P^T dO, dS^T Q): then the slots of a 16-row
+//              k-step v are exactly C elements 8 v .. 8 v + 7, so the
+//              probabilities never leave the registers; the other operand
+//              is read transposed from its row-major tile with two
+//              ds_read_b64_tr_b16 (rows 4 h .. 4 h + 3 and 8 + 4 h ..).
 //
-// Tiles are 64 rows x d columns and live in LDS in two forms:
-//
-// natural [64][d + 8], rows PERMUTED: LDS row m holds tile row perm16(m),
-//   which swaps bits 2 and 3 of the row index (an involution inside every
-//   16-row block).  Used as the A operand of products that contract over d
-//   (S = Q K^T, S^T = K Q^T, ...).  With the permutation, element i of a C
-//   result in lane (r, h) belongs to tile row 16 (i / 8) + 8 h + i % 8, so
-//   C elements 8 u .. 8 u + 7 of a 32-row block are eight CONSECUTIVE rows
-//   16 u + 8 h + 0..7: exactly the B/A slots (h, j) = row 16 u + 8 h + j of
-//   a 16-row k-step when those rows are contracted next (P^T dO, dS^T Q,
-//   V^T P^T, K^T dS^T).  The 8-element pad keeps the 16-byte row reads of
-//   eight lanes on distinct banks.
-// transposed [d][64] in 16-byte chunks of 8 rows: chunk c of column d sits
-//   at chunk position c ^ trn_swz(d), trn_swz(d) = (d % 8) ^ (d / 8 % 8).
-//   A k-step fragment (8 consecutive rows of one column) is one 16-byte
-//   read; eight lanes reading eight consecutive columns hit eight distinct
-//   positions, and the staging writes (columns 8 apart) spread likewise.
-//
-// Each staging thread holds 4 consecutive rows x 8 columns (four 16-byte
-// global loads; 16 lanes cover a row of d = 128), writes them to the natural
-// tile at the permuted rows and to the transposed tile as eight 4-row
-// half-chunks.
+// Tiles: 64 rows x D bf16, row-major, filled straight from global memory by
+// global_load_lds_dwordx4 (no VGPR staging).  One load instruction writes
+// 1 KB contiguously (lane l -> bytes 16 l), so the layout is chosen on the
+// global side: 16-byte chunk c of row m is stored at chunk position
+// c ^ swz(m).  swz makes both access kinds conflict-free on the 64 banks:
+//   ds_read_b128 of an A/B row operand: 16 lanes read 16 rows at one chunk;
+//   ds_read_b64_tr_b16: 16 lanes read 4 consecutive rows x 32 bytes.
+// Rows of a partial tile repeat the last valid row: the values stay finite
+// and the kernels mask what they must.
 #pragma once
 
 #include "common.hpp"
@@ -37,8 +33,32 @@
 namespace spr {
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4_t;
 
 constexpr int kTileRows = 64;
+constexpr int kThreads = 256;  // 4 waves per workgroup in every bf16 kernel
+
+template <int D>
+struct Tile {
+  static constexpr int CH = D / 8;                 // 16-byte chunks per row
+  static constexpr int ELEMS = kTileRows * D;      // bf16 elements per tile
+  static constexpr int RPI = 64 / CH;              // rows per 1 KB load instruction
+  static constexpr int IPW = kTileRows / RPI / 4;  // load instructions per wave
+};
+
+template <int D>
+__device__ __forceinline__ int swz(int row);
+template <>
+__device__ __forceinline__ int swz<128>(int row) { return ((row & 3) << 2) | ((row >> 2) & 3); }
+template <>
+__device__ __forceinline__ int swz<64>(int row) { return (((row >> 1) & 1) << 2) | ((row >> 2) & 3); }
+
+// element offset of (row, col) in a swizzled tile
+template <int D>
+__device__ __forceinline__ int toff(int row, int col) {
+  return row * D + ((((col >> 3) ^ swz<D>(row))) << 3) + (col & 7);
+}
 
 __device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -48,129 +68,74 @@ __device__ __forceinline__ f32x16 zero16() {
   return f32x16{0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 }
 
-__device__ __forceinline__ bf16x8 zero_bf8() {
-  const bf16 z = (bf16)0.f;
-  return bf16x8{z, z, z, z, z, z, z, z};
-}
-
-// v_exp_f32: 2^x without the denormal-range fix-up of exp2f; softmax weights
-// below 2^-126 are flushed to zero, far below bf16 resolution.
+// v_exp_f32: 2^x without the denormal fix-up of exp2f; softmax weights below
+// 2^-126 flush to zero, far below bf16 resolution.
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// tile row held by LDS row m of a natural tile (and vice versa)
-__device__ __forceinline__ int perm16(int m) { return (m & ~12) | ((m & 4) << 1) | ((m & 8) >> 1); }
-
-// tile row of C element i in lane half h, within a 32-row block whose A
-// operand came from a natural (permuted) tile
-__device__ __forceinline__ int c_row(int i, int h) { return 16 * (i >> 3) + 8 * h + (i & 7); }
-
-__device__ __forceinline__ int trn_swz(int d) { return (d & 7) ^ ((d >> 3) & 7); }
-
-template <int D>
-struct TileGeom {
-  static constexpr int NST = D + 8;                      // natural row stride (elements)
-  static constexpr int NAT = kTileRows * NST;            // natural tile elements
-  static constexpr int TRN = D * kTileRows;              // transposed tile elements
-  static constexpr int CPR = D / 8;                      // 16-byte chunks per row
-  static constexpr int STAGERS = kTileRows * CPR / 4;    // threads that stage a tile
-};
-
-// C elements 8u .. 8u+7 of a 32x32 result, rounded to bf16: rows 16 u + 8 h
-// + 0..7 of the block as the (h, j) slots of the next product's k-step.
-__device__ __forceinline__ bf16x8 c_to_kfrag(const f32x16& c, int u) {
-  return bf16x8{(bf16)c[8 * u + 0], (bf16)c[8 * u + 1], (bf16)c[8 * u + 2], (bf16)c[8 * u + 3],
-                (bf16)c[8 * u + 4], (bf16)c[8 * u + 5], (bf16)c[8 * u + 6], (bf16)c[8 * u + 7]};
-}
-
-// Element offset of the A-operand read of LDS row `row`, columns
-// col0 + 8 h .. + 7 of a natural tile.
-template <int D>
-__device__ __forceinline__ int nat_off(int row, int col0, int h) {
-  return row * TileGeom<D>::NST + col0 + 8 * h;
-}
-
-// Element offset of rows 16 u + 8 h .. + 7 of column d of a transposed tile.
-__device__ __forceinline__ int trn_off(int d, int u, int h) {
-  return d * kTileRows + 8 * ((2 * u + h) ^ trn_swz(d));
-}
-
-__device__ __forceinline__ bf16x8 lds8(const bf16* base, int off) {
-  return *(const bf16x8*)(base + off);
-}
-
-// Keeps the compiler from moving memory operations across this point: the
-// next tile's LDS stores must stay after the current tile's products so the
-// wait on their global loads does not precede the matrix work.
+// Keeps the compiler from moving memory operations across this point (the
+// next tile's loads must be issued before the current tile's products).
 __device__ __forceinline__ void compiler_fence() { asm volatile("" ::: "memory"); }
 
-typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
-typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+// Waits for this wave's direct-to-LDS loads, then for every wave.
+__device__ __forceinline__ void tile_barrier() {
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+}
 
-// Staging of one 64-row tile: rows row0 .. row0 + 63 of a token-major
-// [rows, H, D] tensor, head hh; rows >= nvalid are zero.  A thread's four
-// rows are four named registers of 32-bit words (two bf16 per word): the
-// transposed store builds its 4-row columns with byte selects (v_perm_b32)
-// instead of element extraction, which keeps everything in VGPRs.
+// Rows row0 .. row0 + 63 of a token-major [rows, H, D] tensor, head hh, into
+// a swizzled LDS tile; rows at or past row0 + nvalid (nvalid >= 1) repeat row
+// row0 + nvalid - 1.  Called by all four waves (w = wave index).
 template <int D>
-struct Stager {
-  u32x4 v0, v1, v2, v3;
-
-  __device__ __forceinline__ void load(const bf16* base, int row0, int nvalid, int H, int hh,
-                                       int tid) {
-    constexpr int CPR = TileGeom<D>::CPR;
-    if (tid < TileGeom<D>::STAGERS) {
-      const int c16 = tid % CPR, rg = tid / CPR;
-      const bf16* p = base + ((size_t)(row0 + 4 * rg) * H + hh) * D + 8 * c16;
-      const size_t rs = (size_t)H * D;
-      const u32x4 z = {0u, 0u, 0u, 0u};
-      if (nvalid >= kTileRows) {  // full tile: no per-row checks
-        v0 = *(const u32x4*)(p);
-        v1 = *(const u32x4*)(p + rs);
-        v2 = *(const u32x4*)(p + 2 * rs);
-        v3 = *(const u32x4*)(p + 3 * rs);
-      } else {
-        const int rr = 4 * rg;
-        v0 = rr + 0 < nvalid ? *(const u32x4*)(p) : z;
-        v1 = rr + 1 < nvalid ? *(const u32x4*)(p + rs) : z;
-        v2 = rr + 2 < nvalid ? *(const u32x4*)(p + 2 * rs) : z;
-        v3 = rr + 3 < nvalid ? *(const u32x4*)(p + 3 * rs) : z;
-      }
-    }
-  }
-
-  __device__ __forceinline__ void store_nat(bf16* nat, int tid) const {
-    constexpr int CPR = TileGeom<D>::CPR, NST = TileGeom<D>::NST;
-    if (tid < TileGeom<D>::STAGERS) {
-      const int c16 = tid % CPR, rg = tid / CPR;
-      // rows 4 rg + i live at LDS rows perm16(4 rg + i) = perm16(4 rg) + i
-      bf16* p = nat + perm16(4 * rg) * NST + 8 * c16;
-      *(u32x4*)(p) = v0;
-      *(u32x4*)(p + NST) = v1;
-      *(u32x4*)(p + 2 * NST) = v2;
-      *(u32x4*)(p + 3 * NST) = v3;
-    }
-  }
-
-  __device__ __forceinline__ void store_trn(bf16* trn, int tid) const {
-    constexpr int CPR = TileGeom<D>::CPR;
-    if (tid < TileGeom<D>::STAGERS) {
-      const int c16 = tid % CPR, rg = tid / CPR;
-      // rows 4 rg .. 4 rg + 3 are half (rg & 1) of the 8-row chunk rg / 2;
-      // word w of a row holds columns 2 w (low half) and 2 w + 1 (high half)
+__device__ __forceinline__ void load_tile(bf16* tile, const bf16* base, int row0, int nvalid,
+                                          int H, int hh, int w, int lane) {
+  constexpr int CH = Tile<D>::CH, RPI = Tile<D>::RPI;
+  const int last = row0 + nvalid - 1;
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        const unsigned lo01 = __builtin_amdgcn_perm(v1[w], v0[w], 0x05040100u);
-        const unsigned lo23 = __builtin_amdgcn_perm(v3[w], v2[w], 0x05040100u);
-        const unsigned hi01 = __builtin_amdgcn_perm(v1[w], v0[w], 0x07060302u);
-        const unsigned hi23 = __builtin_amdgcn_perm(v3[w], v2[w], 0x07060302u);
-        const int d0 = 8 * c16 + 2 * w, d1 = d0 + 1;
-        *(u32x2*)(trn + d0 * kTileRows + 8 * ((rg >> 1) ^ trn_swz(d0)) + 4 * (rg & 1)) =
-            u32x2{lo01, lo23};
-        *(u32x2*)(trn + d1 * kTileRows + 8 * ((rg >> 1) ^ trn_swz(d1)) + 4 * (rg & 1)) =
-            u32x2{hi01, hi23};
-      }
-    }
+  for (int i = 0; i < Tile<D>::IPW; ++i) {
+    const int lrow0 = (w * Tile<D>::IPW + i) * RPI;
+    const int lrow = lrow0 + lane / CH;
+    const int c = (lane % CH) ^ swz<D>(lrow);
+    const int grow = min(row0 + lrow, last);
+    __builtin_amdgcn_global_load_lds(base + ((size_t)grow * H + hh) * D + 8 * c,
+                                     (lds_void_t*)(tile + lrow0 * D), 16, 0, 0);
   }
-};
+}
+
+// 64 fp32 row values v[(row0 + i) * stride] (i < 64; rows past nvalid repeat
+// the last valid one) into LDS, by one wave.
+__device__ __forceinline__ void load_row_vec(float* dst, const float* src, int row0, int nvalid,
+                                             int stride, int lane) {
+  const int row = min(row0 + lane, row0 + nvalid - 1);
+  __builtin_amdgcn_global_load_lds(src + (size_t)row * stride, (lds_void_t*)dst, 4, 0, 0);
+}
+
+// natural-k operand: 8 contiguous elements (cols col .. col + 7) of tile row `row`
+template <int D>
+__device__ __forceinline__ bf16x8 row_frag(const bf16* tile, int row, int col) {
+  return *(const bf16x8*)(tile + toff<D>(row, col));
+}
+
+// C-order operand read transposed from a row-major tile: slot (h, j) of lane
+// (r, h) holds tile[base + k(h, j)][col0 + r].
+template <int D>
+__device__ __forceinline__ bf16x8 tr_frag(const bf16* tile, int base, int col0, int lane) {
+  const int h = lane >> 5, i16 = lane & 15;
+  const int col = col0 + (lane & 16) + 4 * (i16 & 3);
+  const int row = base + 4 * h + (i16 >> 2);
+  const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(tile + toff<D>(row, col)));
+  const bf16x4 hi =
+      __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(tile + toff<D>(row + 8, col)));
+  return bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+}
+
+// C-order operand from registers: elements 8 v .. 8 v + 7 of a C result,
+// i.e. its rows 16 v + k(h, j), rounded to bf16.
+__device__ __forceinline__ bf16x8 c_kfrag(const f32x16& c, int v) {
+  return bf16x8{(bf16)c[8 * v + 0], (bf16)c[8 * v + 1], (bf16)c[8 * v + 2], (bf16)c[8 * v + 3],
+                (bf16)c[8 * v + 4], (bf16)c[8 * v + 5], (bf16)c[8 * v + 6], (bf16)c[8 * v + 7]};
+}
+
+// row of C element i in lane half h (within a 32-row block)
+__device__ __forceinline__ int c_row(int i, int h) { return 8 * (i >> 2) + 4 * h + (i & 3); }
 
 }  // namespace spr

@@ -26,9 +26,6 @@ COMMON_FLAGS = [
     "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-I", os.path.join(ROOT, "include"), "-Wno-unused-result",
-    # keep MFMA accumulators in VGPRs: the kernels rescale/convert them with
-    # vector ALU ops, and AGPR placement costs a copy per tile
-    "-mllvm", "-amdgpu-mfma-vgpr-form",
 ]
 
 

@@ -55,8 +55,10 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_kv_bf16_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(256))) float E0[BQ];  // rowsum(dO * O)
   __shared__ __attribute__((aligned(256))) float E1[BQ];
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
   const int r = lane & 31, h = lane >> 5;
+  FragOffsets<D> fo;
+  fo.init(lane);
   // 1D grid: block b -> kv head b % Hkv (one XCD per kv head), key tile b / Hkv
   const int hk = blockIdx.x % a.hkv, x = blockIdx.x / a.hkv;
   const int G = a.hq / a.hkv;
@@ -155,49 +157,81 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_kv_bf16_kernel(AttnArgs a) {
     if (w == 1) load_row_vec(Ed, (rt.prefix ? a.dd_p : a.dd_s) + rt.hh, rt.row0, rt.nr, a.hq, lane);
   };
 
+  // S and dP of row block rb (32 rows) against this wave's 32 keys:
+  // s[i] = S[row 32 rb + c_row0(i) + 4 h][key my_key]; dp likewise
+  auto sdp = [&](const bf16* Qc, const bf16* Oc, int rb, f32x16& s, f32x16& dp) {
+    s = zero16();
+    dp = zero16();
+#pragma unroll
+    for (int k = 0; k < NS; ++k) {
+      s = mfma32(row_frag<D>(Qc, fo, 32 * rb, k), kf[k], s);
+      dp = mfma32(row_frag<D>(Oc, fo, 32 * rb, k), vf[k], dp);
+    }
+  };
+  // P = exp(S - LSE) (masked rows: q < q_lo or q >= q_hi give 0) and
+  // dS = P (dP - rowsum(dO O)), in place
+  auto softmax_bwd = [&](const float* Lc, const float* Ec, int rb, f32x16& s, f32x16& dp,
+                         bool mask, int q_lo, int q_hi) {
+#pragma unroll
+    for (int g4 = 0; g4 < 4; ++g4) {
+      const float4 l4 = *(const float4*)(Lc + 32 * rb + 8 * g4 + 4 * h);
+      s[4 * g4 + 0] = fast_exp2(fmaf(s[4 * g4 + 0], a.scale_log2, -l4.x * kLog2e));
+      s[4 * g4 + 1] = fast_exp2(fmaf(s[4 * g4 + 1], a.scale_log2, -l4.y * kLog2e));
+      s[4 * g4 + 2] = fast_exp2(fmaf(s[4 * g4 + 2], a.scale_log2, -l4.z * kLog2e));
+      s[4 * g4 + 3] = fast_exp2(fmaf(s[4 * g4 + 3], a.scale_log2, -l4.w * kLog2e));
+    }
+    if (mask) {  // row 32 rb + c_row0(i) + 4 h: compare the constant c_row0(i)
+      const int lo = q_lo - 32 * rb - 4 * h, hi = q_hi - 32 * rb - 4 * h;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) s[i] = (c_row0(i) >= lo && c_row0(i) < hi) ? s[i] : 0.f;
+    }
+#pragma unroll
+    for (int g4 = 0; g4 < 4; ++g4) {
+      const float4 e4 = *(const float4*)(Ec + 32 * rb + 8 * g4 + 4 * h);
+      dp[4 * g4 + 0] = s[4 * g4 + 0] * (dp[4 * g4 + 0] - e4.x);
+      dp[4 * g4 + 1] = s[4 * g4 + 1] * (dp[4 * g4 + 1] - e4.y);
+      dp[4 * g4 + 2] = s[4 * g4 + 2] * (dp[4 * g4 + 2] - e4.z);
+      dp[4 * g4 + 3] = s[4 * g4 + 3] * (dp[4 * g4 + 3] - e4.w);
+    }
+  };
+  // dV^T += dO^T P ; dK^T += Q^T dS over the 16-row k-steps v of block rb
+  auto dvdk = [&](const bf16* Qc, const bf16* Oc, int rb, const f32x16& s, const f32x16& dp) {
+#pragma unroll
+    for (int v = 0; v < 2; ++v) {
+      const bf16x8 pb = c_kfrag(s, v);
+      const bf16x8 sb = c_kfrag(dp, v);
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        dv[db] = mfma32(tr_frag<D>(Oc, fo, 32 * rb + 16 * v, db), pb, dv[db]);
+        dk[db] = mfma32(tr_frag<D>(Qc, fo, 32 * rb + 16 * v, db), sb, dk[db]);
+      }
+    }
+  };
+
   auto compute = [&](int t, const bf16* Qc, const bf16* Oc, const float* Lc, const float* Ec) {
     const RowTile rt = tile_info(t);
     if (rt.causal && rt.lp_first + BQ - 1 < wave_k0) return;  // no row sees this wave's keys
+    const bool full = rt.nr == BQ && !(rt.causal && rt.lp_first < wave_k0 + 31);
+    if (full) {
+      // every (row, key) pair visible: the second block's S/dP products
+      // overlap the first block's softmax backward
+      f32x16 s0, dp0, s1, dp1;
+      sdp(Qc, Oc, 0, s0, dp0);
+      sdp(Qc, Oc, 1, s1, dp1);
+      softmax_bwd(Lc, Ec, 0, s0, dp0, false, 0, 0);
+      dvdk(Qc, Oc, 0, s0, dp0);
+      softmax_bwd(Lc, Ec, 1, s1, dp1, false, 0, 0);
+      dvdk(Qc, Oc, 1, s1, dp1);
+    } else {
+      // ragged or diagonal tile: rows q visible iff q_lo <= q < nr
+      const int q_lo = rt.causal ? my_key - rt.lp_first : 0;
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb) {
-      if (rt.causal && rt.lp_first + 32 * rb + 31 < wave_k0) continue;
-      // s[i] = S[row 32 rb + c_row(i, h)][key my_key]; dp likewise
-      f32x16 s = zero16(), dp = zero16();
-#pragma unroll
-      for (int k = 0; k < NS; ++k) {
-        s = mfma32(row_frag<D>(Qc, 32 * rb + r, 16 * k + 8 * h), kf[k], s);
-        dp = mfma32(row_frag<D>(Oc, 32 * rb + r, 16 * k + 8 * h), vf[k], dp);
-      }
-      const bool need_mask = rt.nr < 32 * rb + 32 || (rt.causal && rt.lp_first + 32 * rb < wave_k0 + 31);
-#pragma unroll
-      for (int g4 = 0; g4 < 4; ++g4) {
-        const int q0 = 32 * rb + 8 * g4 + 4 * h;
-        const float4 l4 = *(const float4*)(Lc + q0);
-        const float4 e4 = *(const float4*)(Ec + q0);
-        const float lq[4] = {l4.x, l4.y, l4.z, l4.w};
-        const float eq[4] = {e4.x, e4.y, e4.z, e4.w};
-#pragma unroll
-        for (int b = 0; b < 4; ++b) {
-          const int i = 4 * g4 + b, q = q0 + b;
-          float p = fast_exp2(fmaf(s[i], a.scale_log2, -lq[b] * kLog2e));
-          if (need_mask) {
-            const bool vis = q < rt.nr && (!rt.causal || my_key <= rt.lp_first + q);
-            p = vis ? p : 0.f;
-          }
-          s[i] = p;
-          dp[i] = p * (dp[i] - eq[b]);
-        }
-      }
-      // dV^T += dO^T P ; dK^T += Q^T dS over 16-row k-steps v (C-order rows)
-#pragma unroll
-      for (int v = 0; v < 2; ++v) {
-        const bf16x8 pb = c_kfrag(s, v);
-        const bf16x8 sb = c_kfrag(dp, v);
-#pragma unroll
-        for (int db = 0; db < NDB; ++db) {
-          dv[db] = mfma32(tr_frag<D>(Oc, 32 * rb + 16 * v, 32 * db, lane), pb, dv[db]);
-          dk[db] = mfma32(tr_frag<D>(Qc, 32 * rb + 16 * v, 32 * db, lane), sb, dk[db]);
-        }
+      for (int rb = 0; rb < 2; ++rb) {
+        if (rt.causal && rt.lp_first + 32 * rb + 31 < wave_k0) continue;
+        f32x16 s, dp;
+        sdp(Qc, Oc, rb, s, dp);
+        softmax_bwd(Lc, Ec, rb, s, dp, true, q_lo, rt.nr);
+        dvdk(Qc, Oc, rb, s, dp);
       }
     }
   };
@@ -216,7 +250,7 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_kv_bf16_kernel(AttnArgs a) {
     tile_barrier();
   }
 
-  // ---- epilogue: dk[db][i] is dK^T[d = 32 db + c_row(i, h)][key wave_k0 + r]
+  // ---- epilogue: dk[db][i] is dK^T[d = 32 db + c_row0(i) + 4 h][key wave_k0 + r]
   if (wave_k0 + r >= kseg) return;
   const int key = wave_k0 + r;
   if (kpre) {
@@ -305,8 +339,10 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_q_bf16_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(1024))) bf16 V0[TE];
   __shared__ __attribute__((aligned(1024))) bf16 V1[TE];
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
   const int r = lane & 31, h = lane >> 5;
+  FragOffsets<D> fo;
+  fo.init(lane);
 
   const QBlock blk = decode_q_block(a, a.n_prefix_q_tiles + a.n_suffix_q_tiles);
   const int seq = a.seq_base + blk.z;
@@ -371,31 +407,37 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_q_bf16_kernel(AttnArgs a) {
     const int nk = min(BK, (seg == 0 ? nkeys0 : nkeys1) - k0);
     const bool causal = (seg == 0) == prefix_rows;
     if (causal && k0 > wave_lp0 + 31) return;  // no row of this wave sees the tile
-    // st[kb][i] = S^T[key k0 + 32 kb + c_row(i, h)][row my_lp]; pt = dP^T
+    // st[kb][i] = S^T[key k0 + 32 kb + c_row0(i) + 4 h][row my_lp]; pt = dP^T
     f32x16 st[2] = {zero16(), zero16()}, pt[2] = {zero16(), zero16()};
 #pragma unroll
     for (int s = 0; s < NS; ++s)
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
-        st[kb] = mfma32(row_frag<D>(Kc, 32 * kb + r, 16 * s + 8 * h), qf[s], st[kb]);
-        pt[kb] = mfma32(row_frag<D>(Vc, 32 * kb + r, 16 * s + 8 * h), df[s], pt[kb]);
+        st[kb] = mfma32(row_frag<D>(Kc, fo, 32 * kb, s), qf[s], st[kb]);
+        pt[kb] = mfma32(row_frag<D>(Vc, fo, 32 * kb, s), df[s], pt[kb]);
       }
     const bool need_mask = nk < BK || (causal && k0 + BK - 1 > wave_lp0);
-    const int lim = causal ? min(nk, my_lp - k0 + 1) : nk;  // keys kk < lim are visible
+    const int lim = (causal ? min(nk, my_lp - k0 + 1) : nk) - 4 * h;  // keys c_row0 + 4 h < lim + 4 h are visible
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        float p = fast_exp2(fmaf(st[kb][i], a.scale_log2, -lse2));
-        if (need_mask) p = 32 * kb + c_row(i, h) < lim ? p : 0.f;
-        pt[kb][i] = p * (pt[kb][i] - drow);  // dS^T
-      }
+      for (int i = 0; i < 16; ++i) st[kb][i] = fast_exp2(fmaf(st[kb][i], a.scale_log2, -lse2));
+    if (need_mask) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) st[kb][i] = 32 * kb + c_row0(i) < lim ? st[kb][i] : 0.f;
+    }
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) pt[kb][i] = st[kb][i] * (pt[kb][i] - drow);  // dS^T
     // dQ^T += K^T dS^T over 16-key steps u (C-order keys)
 #pragma unroll
     for (int u = 0; u < BK / 16; ++u) {
       const bf16x8 sb = c_kfrag(pt[u >> 1], u & 1);
 #pragma unroll
-      for (int db = 0; db < NDB; ++db) dq[db] = mfma32(tr_frag<D>(Kc, 16 * u, 32 * db, lane), sb, dq[db]);
+      for (int db = 0; db < NDB; ++db) dq[db] = mfma32(tr_frag<D>(Kc, fo, 16 * u, db), sb, dq[db]);
     }
   };
 
@@ -414,7 +456,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_q_bf16_kernel(AttnArgs a) {
   }
 
   if (!row_valid) return;
-  // dq[db][i] = dQ^T[d = 32 db + c_row(i, h)][row my_lp] (unscaled)
+  // dq[db][i] = dQ^T[d = 32 db + c_row0(i) + 4 h][row my_lp] (unscaled)
   const size_t off = ((size_t)(row_base + my_lp) * a.hq + hq) * D + 4 * h;
   if (prefix_rows && a.dq_p_accumulate) {
     // dense baseline: the prefix rows' dQ sums over the trajectories

@@ -60,8 +60,10 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(1024))) bf16 V0[TE];
   __shared__ __attribute__((aligned(1024))) bf16 V1[TE];
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
   const int r = lane & 31, h = lane >> 5;
+  FragOffsets<D> fo;
+  fo.init(lane);
 
   // ---- which 128 query rows: prefix rows, or rows of suffix seq_base + z
   const RowBlock blk = decode_row_block(a, a.n_prefix_q_tiles + a.n_suffix_q_tiles);
@@ -121,17 +123,18 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(AttnArgs a) {
     const int nk = min(BK, (seg == 0 ? nkeys0 : nkeys1) - k0);
     const bool causal = (seg == 0) == prefix_rows;  // keys of the row's own segment
     if (causal && k0 > wave_lp0 + 31) return;       // no row of this wave sees the tile
-    // S^T = K Q^T ; st[kb][i] = S^T[key k0 + 32 kb + c_row(i, h)][row my_lp]
+    // S^T = K Q^T ; st[kb][i] = S^T[key k0 + 32 kb + c_row0(i) + 4 h][row my_lp]
     f32x16 st[2] = {zero16(), zero16()};
 #pragma unroll
     for (int s = 0; s < NS; ++s)
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) st[kb] = mfma32(row_frag<D>(Kc, 32 * kb + r, 16 * s + 8 * h), qf[s], st[kb]);
+      for (int kb = 0; kb < 2; ++kb) st[kb] = mfma32(row_frag<D>(Kc, fo, 32 * kb, s), qf[s], st[kb]);
 #define SC(e) st[(e) >> 4][(e) & 15]
     if (nk < BK || (causal && k0 + BK - 1 > wave_lp0)) {  // partial or diagonal tile
-      const int lim = causal ? min(nk, my_lp - k0 + 1) : nk;  // keys kk < lim are visible
+      // keys kk = 32 (e / 16) + c_row0(e % 16) + 4 h are visible iff kk < lim
+      const int lim = (causal ? min(nk, my_lp - k0 + 1) : nk) - 4 * h;
 #pragma unroll
-      for (int e = 0; e < 32; ++e) SC(e) = 32 * (e >> 4) + c_row(e & 15, h) < lim ? SC(e) : -INFINITY;
+      for (int e = 0; e < 32; ++e) SC(e) = 32 * (e >> 4) + c_row0(e & 15) < lim ? SC(e) : -INFINITY;
     }
     float mt = -INFINITY;
 #pragma unroll
@@ -160,7 +163,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(AttnArgs a) {
     for (int u = 0; u < BK / 16; ++u) {
       const bf16x8 pb = c_kfrag(st[u >> 1], u & 1);
 #pragma unroll
-      for (int db = 0; db < NDB; ++db) o[db] = mfma32(tr_frag<D>(Vc, 16 * u, 32 * db, lane), pb, o[db]);
+      for (int db = 0; db < NDB; ++db) o[db] = mfma32(tr_frag<D>(Vc, fo, 16 * u, db), pb, o[db]);
     }
   };
 
@@ -179,7 +182,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(AttnArgs a) {
   }
 
   if (!row_valid) return;
-  // o[db][i] = O^T[d = 32 db + c_row(i, h)][row my_lp]
+  // o[db][i] = O^T[d = 32 db + c_row0(i) + 4 h][row my_lp]
   const float inv = 1.f / l;
   bf16* ob = (bf16*)(prefix_rows ? a.o_p : a.o_s);
   const size_t off = ((size_t)(row_base + my_lp) * a.hq + hq) * D + 4 * h;

@@ -60,6 +60,9 @@ __device__ __forceinline__ int toff(int row, int col) {
   return row * D + ((((col >> 3) ^ swz<D>(row))) << 3) + (col & 7);
 }
 
+// wave index inside the workgroup, in a scalar register (wave-uniform)
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
+
 __device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
@@ -109,22 +112,42 @@ __device__ __forceinline__ void load_row_vec(float* dst, const float* src, int r
   __builtin_amdgcn_global_load_lds(src + (size_t)row * stride, (lds_void_t*)dst, 4, 0, 0);
 }
 
-// natural-k operand: 8 contiguous elements (cols col .. col + 7) of tile row `row`
+// Per-lane LDS offsets of the operand reads.  swz depends only on the low
+// four bits of the row, so moving a read by a multiple of 16 rows adds
+// 16 m D to its offset: the kernels precompute the lane-dependent part once
+// and add row offsets as compile-time constants, which the hardware takes as
+// the instruction's immediate offset.
 template <int D>
-__device__ __forceinline__ bf16x8 row_frag(const bf16* tile, int row, int col) {
-  return *(const bf16x8*)(tile + toff<D>(row, col));
+struct FragOffsets {
+  int row[D / 16];    // natural-k read of row r, cols 16 k + 8 h .. + 7
+  int trlo[D / 32];   // transposed read, rows 4 h .. 4 h + 3, col 32 db + r
+  int trhi[D / 32];   // rows 8 + 4 h .. 8 + 4 h + 3
+  __device__ __forceinline__ void init(int lane) {
+    const int r = lane & 31, h = lane >> 5, i16 = lane & 15;
+#pragma unroll
+    for (int k = 0; k < D / 16; ++k) row[k] = toff<D>(r, 16 * k + 8 * h);
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) {
+      const int col = 32 * db + (lane & 16) + 4 * (i16 & 3);
+      trlo[db] = toff<D>(4 * h + (i16 >> 2), col);
+      trhi[db] = toff<D>(8 + 4 * h + (i16 >> 2), col);
+    }
+  }
+};
+
+// natural-k operand: tile row row0 + r (row0 a multiple of 16), columns
+// 16 k + 8 h .. + 7
+template <int D>
+__device__ __forceinline__ bf16x8 row_frag(const bf16* tile, const FragOffsets<D>& fo, int row0, int k) {
+  return *(const bf16x8*)(tile + row0 * D + fo.row[k]);
 }
 
 // C-order operand read transposed from a row-major tile: slot (h, j) of lane
-// (r, h) holds tile[base + k(h, j)][col0 + r].
+// (r, h) holds tile[base + k(h, j)][32 db + r] (base a multiple of 16).
 template <int D>
-__device__ __forceinline__ bf16x8 tr_frag(const bf16* tile, int base, int col0, int lane) {
-  const int h = lane >> 5, i16 = lane & 15;
-  const int col = col0 + (lane & 16) + 4 * (i16 & 3);
-  const int row = base + 4 * h + (i16 >> 2);
-  const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(tile + toff<D>(row, col)));
-  const bf16x4 hi =
-      __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(tile + toff<D>(row + 8, col)));
+__device__ __forceinline__ bf16x8 tr_frag(const bf16* tile, const FragOffsets<D>& fo, int base, int db) {
+  const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(tile + base * D + fo.trlo[db]));
+  const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(tile + base * D + fo.trhi[db]));
   return bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
 }
 
@@ -135,7 +158,7 @@ __device__ __forceinline__ bf16x8 c_kfrag(const f32x16& c, int v) {
                 (bf16)c[8 * v + 4], (bf16)c[8 * v + 5], (bf16)c[8 * v + 6], (bf16)c[8 * v + 7]};
 }
 
-// row of C element i in lane half h (within a 32-row block)
-__device__ __forceinline__ int c_row(int i, int h) { return 8 * (i >> 2) + 4 * h + (i & 3); }
+// row of C element i in lane half h (within a 32-row block) is c_row0(i) + 4 h
+__device__ __forceinline__ constexpr int c_row0(int i) { return 8 * (i >> 2) + (i & 3); }
 
 }  // namespace spr

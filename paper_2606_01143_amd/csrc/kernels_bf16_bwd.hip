@@ -26,7 +26,9 @@
 //     dQ^T += K^T dS^T             A = K tile read transposed, B = dS^T registers
 //   and writes dQ once, already scaled and rounded.
 // Both stream their tiles through double-buffered LDS, filled by
-// direct-to-LDS loads issued one tile ahead of the products.
+// direct-to-LDS loads issued one tile ahead of the products.  The loads
+// are invisible to the compiler's wait tracking: every tile is read only
+// after tile_barrier (vmcnt(0) + workgroup barrier).
 #include "common.hpp"
 #include "launch.hpp"
 #include "tile.hpp"
@@ -46,14 +48,11 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_kv_bf16_kernel(AttnArgs a) {
   constexpr int NS = D / 16;
   constexpr int NDB = D / 32;
   constexpr int TE = Tile<D>::ELEMS, BQ = kTileRows;
-  __shared__ __attribute__((aligned(1024))) bf16 Q0[TE];
-  __shared__ __attribute__((aligned(1024))) bf16 Q1[TE];
-  __shared__ __attribute__((aligned(1024))) bf16 O0[TE];  // dO
-  __shared__ __attribute__((aligned(1024))) bf16 O1[TE];
-  __shared__ __attribute__((aligned(256))) float L0[BQ];  // LSE of the tile rows
-  __shared__ __attribute__((aligned(256))) float L1[BQ];
-  __shared__ __attribute__((aligned(256))) float E0[BQ];  // rowsum(dO * O)
-  __shared__ __attribute__((aligned(256))) float E1[BQ];
+  // double-buffered tiles of the streamed rows: Q, dO, LSE, rowsum(dO * O)
+  __shared__ __attribute__((aligned(1024))) bf16 Qs[2][TE];
+  __shared__ __attribute__((aligned(1024))) bf16 Os[2][TE];
+  __shared__ __attribute__((aligned(256))) float Ls[2][BQ];
+  __shared__ __attribute__((aligned(256))) float Es[2][BQ];
 
   const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
   const int r = lane & 31, h = lane >> 5;
@@ -157,96 +156,93 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_kv_bf16_kernel(AttnArgs a) {
     if (w == 1) load_row_vec(Ed, (rt.prefix ? a.dd_p : a.dd_s) + rt.hh, rt.row0, rt.nr, a.hq, lane);
   };
 
-  // S and dP of row block rb (32 rows) against this wave's 32 keys:
-  // s[i] = S[row 32 rb + c_row0(i) + 4 h][key my_key]; dp likewise
-  auto sdp = [&](const bf16* Qc, const bf16* Oc, int rb, f32x16& s, f32x16& dp) {
-    s = zero16();
-    dp = zero16();
+  // One 32-row block rb of a streamed tile against this wave's 32 keys.
+  // Rows q = 32 rb + c_row0(i) + 4 h with q_lo <= q < q_hi are visible.
+  auto block = [&](const bf16* Qc, const bf16* Oc, const float* Lc, const float* Ec, int rb,
+                   int q_lo, int q_hi) {
+    // S = Q K^T, dP = dO V^T: s[i] = S[row q(i)][key my_key], dp likewise;
+    // all operand reads are issued before the products
+    bf16x8 qa[NS], oa[NS];
 #pragma unroll
     for (int k = 0; k < NS; ++k) {
-      s = mfma32(row_frag<D>(Qc, fo, 32 * rb, k), kf[k], s);
-      dp = mfma32(row_frag<D>(Oc, fo, 32 * rb, k), vf[k], dp);
+      qa[k] = row_frag<D>(Qc, fo, 32 * rb, k);
+      oa[k] = row_frag<D>(Oc, fo, 32 * rb, k);
     }
-  };
-  // P = exp(S - LSE) (masked rows: q < q_lo or q >= q_hi give 0) and
-  // dS = P (dP - rowsum(dO O)), in place
-  auto softmax_bwd = [&](const float* Lc, const float* Ec, int rb, f32x16& s, f32x16& dp,
-                         bool mask, int q_lo, int q_hi) {
+    f32x16 s = zero16(), dp = zero16();
+#pragma unroll
+    for (int k = 0; k < NS; ++k) {
+      s = mfma32(qa[k], kf[k], s);
+      dp = mfma32(oa[k], vf[k], dp);
+    }
+    // schedule: four reads ahead of the products, then one read per product
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+    for (int k = 0; k < 2 * NS - 4; ++k) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+    // P = exp(S - LSE) on visible rows, dS = P (dP - rowsum(dO O))
+    const int lo = q_lo - 32 * rb - 4 * h, hi = q_hi - 32 * rb - 4 * h;
 #pragma unroll
     for (int g4 = 0; g4 < 4; ++g4) {
       const float4 l4 = *(const float4*)(Lc + 32 * rb + 8 * g4 + 4 * h);
-      s[4 * g4 + 0] = fast_exp2(fmaf(s[4 * g4 + 0], a.scale_log2, -l4.x * kLog2e));
-      s[4 * g4 + 1] = fast_exp2(fmaf(s[4 * g4 + 1], a.scale_log2, -l4.y * kLog2e));
-      s[4 * g4 + 2] = fast_exp2(fmaf(s[4 * g4 + 2], a.scale_log2, -l4.z * kLog2e));
-      s[4 * g4 + 3] = fast_exp2(fmaf(s[4 * g4 + 3], a.scale_log2, -l4.w * kLog2e));
-    }
-    if (mask) {  // row 32 rb + c_row0(i) + 4 h: compare the constant c_row0(i)
-      const int lo = q_lo - 32 * rb - 4 * h, hi = q_hi - 32 * rb - 4 * h;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) s[i] = (c_row0(i) >= lo && c_row0(i) < hi) ? s[i] : 0.f;
-    }
-#pragma unroll
-    for (int g4 = 0; g4 < 4; ++g4) {
       const float4 e4 = *(const float4*)(Ec + 32 * rb + 8 * g4 + 4 * h);
-      dp[4 * g4 + 0] = s[4 * g4 + 0] * (dp[4 * g4 + 0] - e4.x);
-      dp[4 * g4 + 1] = s[4 * g4 + 1] * (dp[4 * g4 + 1] - e4.y);
-      dp[4 * g4 + 2] = s[4 * g4 + 2] * (dp[4 * g4 + 2] - e4.z);
-      dp[4 * g4 + 3] = s[4 * g4 + 3] * (dp[4 * g4 + 3] - e4.w);
+      const float lq[4] = {l4.x, l4.y, l4.z, l4.w};
+      const float eq[4] = {e4.x, e4.y, e4.z, e4.w};
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const int i = 4 * g4 + b;
+        const float p = fast_exp2(fmaf(s[i], a.scale_log2, -lq[b] * kLog2e));
+        s[i] = (c_row0(i) >= lo && c_row0(i) < hi) ? p : 0.f;
+        dp[i] = s[i] * (dp[i] - eq[b]);
+      }
     }
-  };
-  // dV^T += dO^T P ; dK^T += Q^T dS over the 16-row k-steps v of block rb
-  auto dvdk = [&](const bf16* Qc, const bf16* Oc, int rb, const f32x16& s, const f32x16& dp) {
+    // dV^T += dO^T P ; dK^T += Q^T dS over the 16-row k-steps v
 #pragma unroll
     for (int v = 0; v < 2; ++v) {
       const bf16x8 pb = c_kfrag(s, v);
       const bf16x8 sb = c_kfrag(dp, v);
+      bf16x8 ot[NDB], qt[NDB];
 #pragma unroll
       for (int db = 0; db < NDB; ++db) {
-        dv[db] = mfma32(tr_frag<D>(Oc, fo, 32 * rb + 16 * v, db), pb, dv[db]);
-        dk[db] = mfma32(tr_frag<D>(Qc, fo, 32 * rb + 16 * v, db), sb, dk[db]);
+        ot[db] = tr_frag<D>(Oc, fo, 32 * rb + 16 * v, db);
+        qt[db] = tr_frag<D>(Qc, fo, 32 * rb + 16 * v, db);
       }
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        dv[db] = mfma32(ot[db], pb, dv[db]);
+        dk[db] = mfma32(qt[db], sb, dk[db]);
+      }
+      // two operands (four transposed reads) ahead of the products
+      __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+      for (int k = 0; k < 2 * NDB - 2; ++k) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
     }
   };
 
   auto compute = [&](int t, const bf16* Qc, const bf16* Oc, const float* Lc, const float* Ec) {
     const RowTile rt = tile_info(t);
-    if (rt.causal && rt.lp_first + BQ - 1 < wave_k0) return;  // no row sees this wave's keys
-    const bool full = rt.nr == BQ && !(rt.causal && rt.lp_first < wave_k0 + 31);
-    if (full) {
-      // every (row, key) pair visible: the second block's S/dP products
-      // overlap the first block's softmax backward
-      f32x16 s0, dp0, s1, dp1;
-      sdp(Qc, Oc, 0, s0, dp0);
-      sdp(Qc, Oc, 1, s1, dp1);
-      softmax_bwd(Lc, Ec, 0, s0, dp0, false, 0, 0);
-      dvdk(Qc, Oc, 0, s0, dp0);
-      softmax_bwd(Lc, Ec, 1, s1, dp1, false, 0, 0);
-      dvdk(Qc, Oc, 1, s1, dp1);
-    } else {
-      // ragged or diagonal tile: rows q visible iff q_lo <= q < nr
-      const int q_lo = rt.causal ? my_key - rt.lp_first : 0;
+    // causal tiles: row lp_first + q sees my_key iff q >= my_key - lp_first
+    const int q_lo = rt.causal ? my_key - rt.lp_first : 0;
 #pragma unroll
-      for (int rb = 0; rb < 2; ++rb) {
-        if (rt.causal && rt.lp_first + 32 * rb + 31 < wave_k0) continue;
-        f32x16 s, dp;
-        sdp(Qc, Oc, rb, s, dp);
-        softmax_bwd(Lc, Ec, rb, s, dp, true, q_lo, rt.nr);
-        dvdk(Qc, Oc, rb, s, dp);
-      }
+    for (int rb = 0; rb < 2; ++rb) {
+      if (rt.causal && rt.lp_first + 32 * rb + 31 < wave_k0) continue;  // no row sees these keys
+      block(Qc, Oc, Lc, Ec, rb, q_lo, rt.nr);
     }
   };
 
-  if (ntiles > 0) issue(0, Q0, O0, L0, E0);
+  if (ntiles > 0) issue(0, Qs[0], Os[0], Ls[0], Es[0]);
   tile_barrier();
-  for (int t = 0; t < ntiles; t += 2) {
-    if (t + 1 < ntiles) issue(t + 1, Q1, O1, L1, E1);
+  for (int t = 0; t < ntiles; ++t) {
+    const int cur = t & 1;
+    if (t + 1 < ntiles) issue(t + 1, Qs[cur ^ 1], Os[cur ^ 1], Ls[cur ^ 1], Es[cur ^ 1]);
     compiler_fence();
-    compute(t, Q0, O0, L0, E0);
-    tile_barrier();
-    if (t + 1 >= ntiles) break;
-    if (t + 2 < ntiles) issue(t + 2, Q0, O0, L0, E0);
-    compiler_fence();
-    compute(t + 1, Q1, O1, L1, E1);
+    compute(t, Qs[cur], Os[cur], Ls[cur], Es[cur]);
     tile_barrier();
   }
 
@@ -334,10 +330,9 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_q_bf16_kernel(AttnArgs a) {
   constexpr int NS = D / 16;
   constexpr int NDB = D / 32;
   constexpr int TE = Tile<D>::ELEMS, BK = kTileRows;
-  __shared__ __attribute__((aligned(1024))) bf16 K0[TE];
-  __shared__ __attribute__((aligned(1024))) bf16 K1[TE];
-  __shared__ __attribute__((aligned(1024))) bf16 V0[TE];
-  __shared__ __attribute__((aligned(1024))) bf16 V1[TE];
+  // double-buffered key tiles
+  __shared__ __attribute__((aligned(1024))) bf16 Ks[2][TE];
+  __shared__ __attribute__((aligned(1024))) bf16 Vs[2][TE];
 
   const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
   const int r = lane & 31, h = lane >> 5;
@@ -441,17 +436,13 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_q_bf16_kernel(AttnArgs a) {
     }
   };
 
-  if (ntiles > 0) issue(0, K0, V0);
+  if (ntiles > 0) issue(0, Ks[0], Vs[0]);
   tile_barrier();
-  for (int t = 0; t < ntiles; t += 2) {
-    if (t + 1 < ntiles) issue(t + 1, K1, V1);
+  for (int t = 0; t < ntiles; ++t) {
+    const int cur = t & 1;
+    if (t + 1 < ntiles) issue(t + 1, Ks[cur ^ 1], Vs[cur ^ 1]);
     compiler_fence();
-    compute(t, K0, V0);
-    tile_barrier();
-    if (t + 1 >= ntiles) break;
-    if (t + 2 < ntiles) issue(t + 2, K0, V0);
-    compiler_fence();
-    compute(t + 1, K1, V1);
+    compute(t, Ks[cur], Vs[cur]);
     tile_barrier();
   }
 

@@ -55,10 +55,9 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(AttnArgs a) {
   constexpr int NS = D / 16;   // k-steps over d for S^T
   constexpr int NDB = D / 32;  // 32-wide d blocks of O^T
   constexpr int TE = Tile<D>::ELEMS, BK = kTileRows;
-  __shared__ __attribute__((aligned(1024))) bf16 K0[TE];
-  __shared__ __attribute__((aligned(1024))) bf16 K1[TE];
-  __shared__ __attribute__((aligned(1024))) bf16 V0[TE];
-  __shared__ __attribute__((aligned(1024))) bf16 V1[TE];
+  // double-buffered key tiles
+  __shared__ __attribute__((aligned(1024))) bf16 Ks[2][TE];
+  __shared__ __attribute__((aligned(1024))) bf16 Vs[2][TE];
 
   const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
   const int r = lane & 31, h = lane >> 5;
@@ -167,17 +166,13 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(AttnArgs a) {
     }
   };
 
-  if (ntiles > 0) issue(0, K0, V0);
+  if (ntiles > 0) issue(0, Ks[0], Vs[0]);
   tile_barrier();
-  for (int t = 0; t < ntiles; t += 2) {
-    if (t + 1 < ntiles) issue(t + 1, K1, V1);
+  for (int t = 0; t < ntiles; ++t) {
+    const int cur = t & 1;
+    if (t + 1 < ntiles) issue(t + 1, Ks[cur ^ 1], Vs[cur ^ 1]);
     compiler_fence();
-    compute(t, K0, V0);
-    tile_barrier();
-    if (t + 1 >= ntiles) break;
-    if (t + 2 < ntiles) issue(t + 2, K0, V0);
-    compiler_fence();
-    compute(t + 1, K1, V1);
+    compute(t, Ks[cur], Vs[cur]);
     tile_barrier();
   }
 

@@ -44,22 +44,21 @@ int bwd_bf16_block_k() { return kKvBK; }
 
 // ---------------------------------------------------------------- bwd_kv
 template <int D>
-__global__ __launch_bounds__(kThreads, 1) void bwd_kv_bf16_kernel(AttnArgs a) {
+__device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, bf16 (*Qs)[Tile<D>::ELEMS],
+                                            bf16 (*Os)[Tile<D>::ELEMS], float (*Ls)[kTileRows],
+                                            float (*Es)[kTileRows]) {
   constexpr int NS = D / 16;
   constexpr int NDB = D / 32;
-  constexpr int TE = Tile<D>::ELEMS, BQ = kTileRows;
-  // double-buffered tiles of the streamed rows: Q, dO, LSE, rowsum(dO * O)
-  __shared__ __attribute__((aligned(1024))) bf16 Qs[2][TE];
-  __shared__ __attribute__((aligned(1024))) bf16 Os[2][TE];
-  __shared__ __attribute__((aligned(256))) float Ls[2][BQ];
-  __shared__ __attribute__((aligned(256))) float Es[2][BQ];
+  constexpr int BQ = kTileRows;
+  // Qs/Os: double-buffered tiles of the streamed rows' Q and dO; Ls/Es: their
+  // LSE and rowsum(dO * O)
 
   const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
   const int r = lane & 31, h = lane >> 5;
   FragOffsets<D> fo;
   fo.init(lane);
-  // 1D grid: block b -> kv head b % Hkv (one XCD per kv head), key tile b / Hkv
-  const int hk = blockIdx.x % a.hkv, x = blockIdx.x / a.hkv;
+  // block b -> kv head b % Hkv (one XCD per kv head), key tile b / Hkv
+  const int hk = bid % a.hkv, x = bid / a.hkv;
   const int G = a.hq / a.hkv;
 
   // ---- which 128 keys: a prefix tile, or a tile of suffix s
@@ -311,9 +310,9 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_kv_bf16_kernel(AttnArgs a) {
 struct QBlock {
   int tile, z, hq;
 };
-__device__ __forceinline__ QBlock decode_q_block(const AttnArgs& a, int ntx) {
+__device__ __forceinline__ QBlock decode_q_block(const AttnArgs& a, int bid, int ntx) {
   const int G = a.hq / a.hkv;
-  int b = blockIdx.x;
+  int b = bid;
   const int hk = b % a.hkv;
   b /= a.hkv;
   const int gi = b % G;
@@ -326,20 +325,19 @@ __device__ __forceinline__ QBlock decode_q_block(const AttnArgs& a, int ntx) {
 }
 
 template <int D>
-__global__ __launch_bounds__(kThreads, 2) void bwd_q_bf16_kernel(AttnArgs a) {
+__device__ __forceinline__ void bwd_q_body(const AttnArgs& a, const int bid, bf16 (*Ks)[Tile<D>::ELEMS],
+                                           bf16 (*Vs)[Tile<D>::ELEMS]) {
   constexpr int NS = D / 16;
   constexpr int NDB = D / 32;
-  constexpr int TE = Tile<D>::ELEMS, BK = kTileRows;
-  // double-buffered key tiles
-  __shared__ __attribute__((aligned(1024))) bf16 Ks[2][TE];
-  __shared__ __attribute__((aligned(1024))) bf16 Vs[2][TE];
+  constexpr int BK = kTileRows;
+  // Ks/Vs: double-buffered key tiles
 
   const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
   const int r = lane & 31, h = lane >> 5;
   FragOffsets<D> fo;
   fo.init(lane);
 
-  const QBlock blk = decode_q_block(a, a.n_prefix_q_tiles + a.n_suffix_q_tiles);
+  const QBlock blk = decode_q_block(a, bid, a.n_prefix_q_tiles + a.n_suffix_q_tiles);
   const int seq = a.seq_base + blk.z;
   bool prefix_rows;
   int lp0, seg_len, row_base;
@@ -477,28 +475,47 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_q_bf16_kernel(AttnArgs a) {
     }
 }
 
+// One launch runs both kernels' workgroups: the first n_first blocks take
+// one role, the rest the other, so that the key-outer and query-outer work
+// of a microbatch share the GPU (a suffix microbatch alone fills neither).
+// The heavier role goes first; both segments start on a multiple of 8 blocks
+// so the XCD mapping of each role holds.
+template <int D>
+__global__ __launch_bounds__(kThreads, 1) void bwd_bf16_kernel(AttnArgs a, int n_first, int n_kv,
+                                                               int n_q, int kv_first) {
+  constexpr int TE = Tile<D>::ELEMS;
+  __shared__ __attribute__((aligned(1024))) bf16 tiles[4][TE];
+  __shared__ __attribute__((aligned(256))) float rowv[4][kTileRows];
+  const int b = blockIdx.x;
+  const bool first = b < n_first;
+  const int bid = first ? b : b - n_first;
+  // the first segment is padded to a multiple of 8 blocks: padding exits
+  if (first == (kv_first != 0)) {
+    if (bid < n_kv) bwd_kv_body<D>(a, bid, tiles, tiles + 2, rowv, rowv + 2);
+  } else {
+    if (bid < n_q) bwd_q_body<D>(a, bid, tiles, tiles + 2);
+  }
+}
+
 hipError_t launch_bwd_bf16(const AttnArgs& a, int head_dim, int n_qz, bool deterministic,
                            hipStream_t st) {
-  (void)deterministic;  // both kernels are deterministic: no atomics anywhere
-  {
-    const long nb = (long)(a.n_prefix_k_tiles + a.n_seq * a.n_suffix_k_tiles) * a.hkv;
-    if (nb > 0) {
-      ProfileScope ps("bwd_kv_bf16", st);
-      if (head_dim == 64)
-        hipLaunchKernelGGL(bwd_kv_bf16_kernel<64>, dim3((unsigned)nb), dim3(kThreads), 0, st, a);
-      else
-        hipLaunchKernelGGL(bwd_kv_bf16_kernel<128>, dim3((unsigned)nb), dim3(kThreads), 0, st, a);
-      const hipError_t e = hipGetLastError();
-      if (e != hipSuccess) return e;
-    }
-  }
-  const long nb = (long)(a.n_prefix_q_tiles + a.n_suffix_q_tiles) * a.hq * n_qz;
-  if (nb == 0) return hipSuccess;
-  ProfileScope ps("bwd_q_bf16", st);
+  (void)deterministic;  // both roles are deterministic: no atomics anywhere
+  const long n_kv = (long)(a.n_prefix_k_tiles + a.n_seq * a.n_suffix_k_tiles) * a.hkv;
+  const long n_q = (long)(a.n_prefix_q_tiles + a.n_suffix_q_tiles) * a.hq * n_qz;
+  if (n_kv + n_q == 0) return hipSuccess;
+  // Phase C / dense prefix: the causal key tiles near the start of the prefix
+  // carry the most rows; Phase B suffix: every query tile sweeps the prefix
+  const int kv_first = a.prefix_rows ? 1 : 0;
+  const long first = kv_first ? n_kv : n_q;
+  const long n_first = (first + 7) / 8 * 8;
+  const long nb = n_first + (kv_first ? n_q : n_kv);
+  ProfileScope ps("bwd_bf16", st);
   if (head_dim == 64)
-    hipLaunchKernelGGL(bwd_q_bf16_kernel<64>, dim3((unsigned)nb), dim3(kThreads), 0, st, a);
+    hipLaunchKernelGGL(bwd_bf16_kernel<64>, dim3((unsigned)nb), dim3(kThreads), 0, st, a, (int)n_first,
+                       (int)n_kv, (int)n_q, kv_first);
   else
-    hipLaunchKernelGGL(bwd_q_bf16_kernel<128>, dim3((unsigned)nb), dim3(kThreads), 0, st, a);
+    hipLaunchKernelGGL(bwd_bf16_kernel<128>, dim3((unsigned)nb), dim3(kThreads), 0, st, a, (int)n_first,
+                       (int)n_kv, (int)n_q, kv_first);
   return hipGetLastError();
 }
 

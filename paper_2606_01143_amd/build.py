@@ -26,6 +26,9 @@ COMMON_FLAGS = [
     "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-I", os.path.join(ROOT, "include"), "-Wno-unused-result",
+    # MFMA results in VGPRs: the kernels feed S/dP straight into vector ALU
+    # code, and AGPR results would cost a copy per element
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
 ]
 
 

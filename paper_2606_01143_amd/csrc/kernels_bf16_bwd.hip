@@ -210,8 +210,8 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, bf
       }
 #pragma unroll
       for (int db = 0; db < NDB; ++db) {
-        dv[db] = mfma32(ot[db], pb, dv[db]);
-        dk[db] = mfma32(qt[db], sb, dk[db]);
+        mfma32_acc(dv[db], ot[db], pb);
+        mfma32_acc(dk[db], qt[db], sb);
       }
       // two operands (four transposed reads) ahead of the products
       __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
@@ -245,6 +245,7 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, bf
     tile_barrier();
   }
 
+  acc_fence();
   // ---- epilogue: dk[db][i] is dK^T[d = 32 db + c_row0(i) + 4 h][key wave_k0 + r]
   if (wave_k0 + r >= kseg) return;
   const int key = wave_k0 + r;

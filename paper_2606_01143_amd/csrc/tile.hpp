@@ -67,6 +67,18 @@ __device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+// Accumulating product whose accumulator lives in AGPRs for the whole
+// sweep (it is only read back in the epilogue, after acc_fence()): keeps the
+// VGPRs free for the operands and the softmax.  The two wait states in front
+// cover a vector-ALU write of b (or a) just before.
+__device__ __forceinline__ void mfma32_acc(f32x16& acc, const bf16x8& a, const bf16x8& b) {
+  asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+}
+
+// Wait states between the last mfma32_acc and any read of its accumulators
+// (the longest matrix-core write-to-read distance is 18 wait states).
+__device__ __forceinline__ void acc_fence() { asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory"); }
+
 __device__ __forceinline__ f32x16 zero16() {
   return f32x16{0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 }

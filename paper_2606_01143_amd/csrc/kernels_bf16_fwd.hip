@@ -17,6 +17,8 @@
 //                                      B = P^T straight from the S^T registers
 // With S^T each lane holds 16 keys of ONE query row, so the online softmax
 // needs a single cross-lane exchange per statistic.
+#include <algorithm>
+
 #include "common.hpp"
 #include "launch.hpp"
 #include "tile.hpp"
@@ -34,7 +36,7 @@ int fwd_bf16_block_q() { return kFwdBQ; }
 // eight XCDs, so every block of one kv head lands on the same XCD (for
 // Hkv dividing 8) and the K/V it streams stays in that XCD's L2.
 struct RowBlock {
-  int tile, z, hq;
+  int tile, z, hq, split;
 };
 __device__ __forceinline__ RowBlock decode_row_block(const AttnArgs& a, int ntx) {
   const int G = a.hq / a.hkv;
@@ -44,6 +46,8 @@ __device__ __forceinline__ RowBlock decode_row_block(const AttnArgs& a, int ntx)
   const int gi = b % G;
   b /= G;
   RowBlock rb;
+  rb.split = b % a.n_split;
+  b /= a.n_split;
   rb.tile = ntx - 1 - b % ntx;  // rows with the most keys first
   rb.z = b / ntx;
   rb.hq = hk * G + gi;
@@ -105,7 +109,9 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(AttnArgs a) {
   const int nkeys0 = prefix_rows ? min(a.P, last_lp + 1) : a.P;
   const int nkeys1 = prefix_rows ? 0 : last_lp + 1;
   const int nt0 = (nkeys0 + BK - 1) / BK, nt1 = (nkeys1 + BK - 1) / BK;
-  const int ntiles = nt0 + nt1;
+  // this block's contiguous share of the key tiles
+  const int t_begin = (int)((long)(nt0 + nt1) * blk.split / a.n_split);
+  const int t_end = (int)((long)(nt0 + nt1) * (blk.split + 1) / a.n_split);
 
   auto issue = [&](int t, bf16* Kd, bf16* Vd) {
     const int seg = t < nt0 ? 0 : 1;
@@ -166,17 +172,32 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(AttnArgs a) {
     }
   };
 
-  if (ntiles > 0) issue(0, Ks[0], Vs[0]);
+  if (t_begin < t_end) issue(t_begin, Ks[0], Vs[0]);
   tile_barrier();
-  for (int t = 0; t < ntiles; ++t) {
-    const int cur = t & 1;
-    if (t + 1 < ntiles) issue(t + 1, Ks[cur ^ 1], Vs[cur ^ 1]);
+  for (int t = t_begin; t < t_end; ++t) {
+    const int cur = (t - t_begin) & 1;
+    if (t + 1 < t_end) issue(t + 1, Ks[cur ^ 1], Vs[cur ^ 1]);
     compiler_fence();
     compute(t, Ks[cur], Vs[cur]);
     tile_barrier();
   }
 
   if (!row_valid) return;
+  if (a.n_split > 1) {
+    // partial result of this key range: O / l and log2(sum) + max (a range
+    // with no visible key gives l = 0: weight 0 in the combine)
+    const size_t prow = ((size_t)blk.split * a.total_len + row_base + my_lp) * a.hq + hq;
+    const float inv = l > 0.f ? 1.f / l : 0.f;
+    float* po = a.part_o + prow * D + 4 * h;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4)
+        *(float4*)(po + 32 * db + 8 * g4) = make_float4(o[db][4 * g4] * inv, o[db][4 * g4 + 1] * inv,
+                                                        o[db][4 * g4 + 2] * inv, o[db][4 * g4 + 3] * inv);
+    if (h == 0) a.part_lse[prow] = l > 0.f ? m + log2f(l) : -INFINITY;
+    return;
+  }
   // o[db][i] = O^T[d = 32 db + c_row0(i) + 4 h][row my_lp]
   const float inv = 1.f / l;
   bf16* ob = (bf16*)(prefix_rows ? a.o_p : a.o_s);
@@ -195,15 +216,64 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(AttnArgs a) {
   }
 }
 
+// Merge of the n_split partial outputs of every (suffix row, q head):
+// lse = log2 sum_j 2^lse_j, O = sum_j 2^(lse_j - lse) O_j.  One group of
+// D / 4 threads per (row, head), 16-byte accesses.
+template <int D>
+__global__ __launch_bounds__(256) void fwd_combine_kernel(AttnArgs a) {
+  constexpr int TPR = D / 4;  // threads per (row, head)
+  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+  const long rh = idx / TPR;  // row * hq + head
+  const int c = (int)(idx % TPR);
+  const long nrh = (long)a.total_len * a.hq;
+  if (rh >= nrh) return;
+  float mx = -INFINITY;
+  for (int j = 0; j < a.n_split; ++j) mx = fmaxf(mx, a.part_lse[(size_t)j * nrh + rh]);
+  float sum = 0.f;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int j = 0; j < a.n_split; ++j) {
+    const float lj = a.part_lse[(size_t)j * nrh + rh];
+    const float wj = lj == -INFINITY ? 0.f : exp2f(lj - mx);
+    const float4 oj = *(const float4*)(a.part_o + ((size_t)j * nrh + rh) * D + 4 * c);
+    sum += wj;
+    acc.x += wj * oj.x;
+    acc.y += wj * oj.y;
+    acc.z += wj * oj.z;
+    acc.w += wj * oj.w;
+  }
+  const float inv = 1.f / sum;
+  const bf16x4 v = {(bf16)(acc.x * inv), (bf16)(acc.y * inv), (bf16)(acc.z * inv), (bf16)(acc.w * inv)};
+  *(bf16x4*)((bf16*)a.o_s + (size_t)rh * D + 4 * c) = v;
+  if (c == 0) a.lse_s[rh] = (mx + log2f(sum)) * kLn2;
+}
+
 hipError_t launch_fwd_bf16(const AttnArgs& a, int head_dim, int n_z, hipStream_t st) {
-  const long nb = (long)(a.n_prefix_q_tiles + a.n_suffix_q_tiles) * a.hq * n_z;
+  const long nb = (long)(a.n_prefix_q_tiles + a.n_suffix_q_tiles) * a.hq * n_z * a.n_split;
   if (nb == 0) return hipSuccess;
   ProfileScope ps("fwd_bf16", st);
   if (head_dim == 64)
     hipLaunchKernelGGL(fwd_bf16_kernel<64>, dim3((unsigned)nb), dim3(kThreads), 0, st, a);
   else
     hipLaunchKernelGGL(fwd_bf16_kernel<128>, dim3((unsigned)nb), dim3(kThreads), 0, st, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.n_split <= 1) return e;
+  const long threads = (long)a.total_len * a.hq * (head_dim / 4);
+  const unsigned cb = (unsigned)((threads + 255) / 256);
+  ProfileScope pc("fwd_combine", st);
+  if (head_dim == 64)
+    hipLaunchKernelGGL(fwd_combine_kernel<64>, dim3(cb), dim3(256), 0, st, a);
+  else
+    hipLaunchKernelGGL(fwd_combine_kernel<128>, dim3(cb), dim3(256), 0, st, a);
   return hipGetLastError();
+}
+
+int fwd_bf16_split(int n_row_blocks, int prefix_len) {
+  // enough workgroups for two per CU on 256 CUs, each split keeping at
+  // least four 64-key tiles of the prefix
+  if (n_row_blocks <= 0) return 1;
+  int ns = (512 + n_row_blocks - 1) / n_row_blocks;
+  ns = std::min(ns, std::max(1, prefix_len / (4 * kTileRows)));
+  return std::max(1, std::min(ns, 16));
 }
 
 }  // namespace spr

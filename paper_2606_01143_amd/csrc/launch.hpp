@@ -51,6 +51,9 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, int head_dim, int n_qz, bool deter
                            hipStream_t st);
 // Row-tile sizes the launchers expect in AttnArgs (q tiles / k tiles).
 int fwd_bf16_block_q();
+// key splits of the bf16 suffix forward for n_row_blocks (row tile, q head,
+// suffix) blocks and a prefix of prefix_len keys
+int fwd_bf16_split(int n_row_blocks, int prefix_len);
 int bwd_bf16_block_k();
 int f32_block_q();
 int f32_block_k();

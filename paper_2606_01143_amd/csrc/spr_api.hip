@@ -125,7 +125,15 @@ AttnArgs base_args(const spr_dims* d) {
   a.hkv = d->num_kv_heads;
   a.scale = eff_scale(d);
   a.scale_log2 = a.scale * kLog2e;
+  a.n_split = 1;
   return a;
+}
+
+// key splits of the suffix forward (bf16 path only), see fwd_bf16_split
+int suffix_fwd_splits(const spr_dims* d, int32_t n_mb, int32_t max_len) {
+  if (d->dtype != SPR_BF16) return 1;
+  const int nrb = tiles(max_len, fwd_bf16_block_q()) * d->num_q_heads * n_mb;
+  return fwd_bf16_split(nrb, d->prefix_len);
 }
 
 int block_q(int dtype) { return dtype == SPR_BF16 ? fwd_bf16_block_q() : f32_block_q(); }
@@ -145,11 +153,11 @@ hipError_t launch_bwd(const spr_dims* d, const AttnArgs& a, int n_qz, hipStream_
 // ------------------------------------------------------------- workspace
 struct WsLayout {
   size_t dd_p = 0, dq_acc_p = 0, dd_s = 0, dq_acc_s = 0, dk_acc_p = 0, dv_acc_p = 0;
+  size_t part_o = 0, part_lse = 0;
   size_t total = 0;
 };
 
-WsLayout ws_layout(int op, const spr_dims* d, int32_t max_len, int32_t total_len) {
-  (void)max_len;
+WsLayout ws_layout(int op, const spr_dims* d, int32_t n_mb, int32_t max_len, int32_t total_len) {
   WsLayout w;
   const size_t hq = d->num_q_heads, hkv = d->num_kv_heads, hd = d->head_dim;
   const size_t P = d->prefix_len, T = total_len > 0 ? total_len : 0;
@@ -164,8 +172,15 @@ WsLayout ws_layout(int op, const spr_dims* d, int32_t max_len, int32_t total_len
   const bool f32 = d->dtype == SPR_F32;
   switch (op) {
     case SPR_OP_PREFIX_FWD:
-    case SPR_OP_SUFFIX_FWD:
       break;
+    case SPR_OP_SUFFIX_FWD: {
+      const size_t ns = suffix_fwd_splits(d, n_mb, max_len);
+      if (ns > 1) {
+        w.part_o = take(ns * T * hq * hd * 4);
+        w.part_lse = take(ns * T * hq * 4);
+      }
+      break;
+    }
     case SPR_OP_SUFFIX_BWD:
       w.dd_s = take(hq * T * 4);
       if (f32) w.dq_acc_s = take(T * hq * hd * 4);
@@ -291,7 +306,7 @@ spr_status spr_workspace_size(int32_t op, const spr_dims* dims, int32_t n_mb, in
     st = check_suffix_sizes(n_mb, max_len, total_len);
     if (st != SPR_OK) return st;
   }
-  *bytes = ws_layout(op, dims, max_len, total_len).total;
+  *bytes = ws_layout(op, dims, n_mb, max_len, total_len).total;
   return ok();
 }
 
@@ -334,7 +349,7 @@ spr_status spr_suffix_attn_fwd(const spr_dims* dims, const void* k_p, const void
                            {o_s, T * hq * hd * eb, "o_s", true},
                            {lse_s, hq * T * 4, "lse_s", true, 4}};
   if ((st = check_bufs(bufs)) != SPR_OK) return st;
-  const WsLayout w = ws_layout(SPR_OP_SUFFIX_FWD, dims, max_len, total_len);
+  const WsLayout w = ws_layout(SPR_OP_SUFFIX_FWD, dims, n_mb, max_len, total_len);
   if ((st = check_ws(w, ws, ws_bytes)) != SPR_OK) return st;
   AttnArgs a = base_args(dims);
   a.k_p = k_p; a.v_p = v_p;
@@ -344,6 +359,11 @@ spr_status spr_suffix_attn_fwd(const spr_dims* dims, const void* k_p, const void
   a.seq_base = 0;
   a.n_seq = n_mb;
   a.n_suffix_q_tiles = tiles(max_len, block_q(dims->dtype));
+  a.n_split = suffix_fwd_splits(dims, n_mb, max_len);
+  if (a.n_split > 1) {
+    a.part_o = at<float>(ws, w.part_o);
+    a.part_lse = at<float>(ws, w.part_lse);
+  }
   if ((st = hip_check(launch_fwd(dims, a, n_mb, stream), "suffix forward")) != SPR_OK) return st;
   return ok();
 }
@@ -375,7 +395,7 @@ spr_status spr_suffix_attn_bwd_accum(const spr_dims* dims, const void* k_p, cons
                            {gk_cache, P * hkv * hd * 4, "gk_cache", true},
                            {gv_cache, P * hkv * hd * 4, "gv_cache", true}};
   if ((st = check_bufs(bufs)) != SPR_OK) return st;
-  const WsLayout w = ws_layout(SPR_OP_SUFFIX_BWD, dims, max_len, total_len);
+  const WsLayout w = ws_layout(SPR_OP_SUFFIX_BWD, dims, n_mb, max_len, total_len);
   if ((st = check_ws(w, ws, ws_bytes)) != SPR_OK) return st;
   std::vector<Buf> all = bufs;
   all.push_back({ws, w.total, "ws", false});
@@ -434,7 +454,7 @@ spr_status spr_prefix_bwd(const spr_dims* dims, const void* q_p, const void* k_p
                            {dk_p, P * hkv * hd * eb, "dk_p", true},
                            {dv_p, P * hkv * hd * eb, "dv_p", true}};
   if ((st = check_bufs(bufs)) != SPR_OK) return st;
-  const WsLayout w = ws_layout(SPR_OP_PREFIX_BWD, dims, 0, 0);
+  const WsLayout w = ws_layout(SPR_OP_PREFIX_BWD, dims, 0, 0, 0);
   if (do_p != nullptr && (st = check_ws(w, ws, ws_bytes)) != SPR_OK) return st;
   std::vector<Buf> all = bufs;
   if (do_p != nullptr) all.push_back({ws, w.total, "ws", false});
@@ -511,7 +531,7 @@ spr_status spr_dense_recompute_baseline(
                            {dk_p, P * hkv * hd * eb, "dk_p", true},
                            {dv_p, P * hkv * hd * eb, "dv_p", true}};
   if ((st = check_bufs(bufs)) != SPR_OK) return st;
-  const WsLayout w = ws_layout(SPR_OP_DENSE_BASELINE, dims, max_len, total_len);
+  const WsLayout w = ws_layout(SPR_OP_DENSE_BASELINE, dims, n, max_len, total_len);
   if ((st = check_ws(w, ws, ws_bytes)) != SPR_OK) return st;
   float* dd_p = at<float>(ws, w.dd_p);
   float* dq_acc_p = at<float>(ws, w.dq_acc_p);

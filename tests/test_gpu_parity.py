@@ -67,6 +67,9 @@ SHAPES = [
     ("bf16_p0", GroupShape(4, 2, 128, 0, (90, 40), "bf16")),
     ("bf16_n1", GroupShape(4, 1, 128, 257, (100,), "bf16")),
     ("bf16_p1_s1", GroupShape(2, 1, 128, 1, (1, 2), "bf16")),
+    # prefixes long enough for the suffix forward to split its key range
+    ("bf16_split_ragged", GroupShape(4, 2, 128, 1100, (70, 129, 33), "bf16")),
+    ("bf16_split_d64", GroupShape(4, 2, 64, 700, (65, 3), "bf16")),
 ]
 
 

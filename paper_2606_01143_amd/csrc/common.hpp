@@ -37,6 +37,7 @@ struct AttnArgs {
   float* lse_p;        // [P, Hq]
   const void* do_p;    // upstream adjoint of the prefix rows (bwd)
   float* dd_p;         // rowsum(dO * O) [P, Hq] (bwd)
+  float* lse2_p;       // LSE * log2(e) [P, Hq] (bf16 bwd)
   float* dq_acc_p;     // fp32 dQ accumulator [P, Hq, d] (bwd)
   // suffix segment: packed rows, suffix s = rows cu[s] .. cu[s+1]-1
   const void* q_s;
@@ -46,6 +47,7 @@ struct AttnArgs {
   float* lse_s;        // [total_len, Hq]
   const void* do_s;
   float* dd_s;         // [total_len, Hq]
+  float* lse2_s;       // [total_len, Hq]
   float* dq_acc_s;     // [total_len, Hq, d]
   // bf16 backward: dQ is written once, scaled, in the storage dtype; the
   // dense baseline accumulates the prefix rows' dQ over the trajectories in

@@ -26,12 +26,16 @@ int aux_blocks(size_t n_vec) {
 // One wave per (row, head): each lane takes d/64 consecutive elements.
 // With cu != nullptr the rows are those of suffix `seq` only:
 // cu[seq] .. cu[seq+1]-1, and `rows` is an upper bound on their count.
+// Also converts the row's LSE to the log2 domain the backward kernels use:
+// lse2 = lse * log2(e).
 template <typename T, int D>
 __global__ __launch_bounds__(kAuxThreads) void row_dot_kernel(const T* __restrict__ dO,
                                                             const T* __restrict__ O, int rows,
                                                             const int32_t* __restrict__ cu,
                                                             int seq, int hq,
-                                                            float* __restrict__ dd) {
+                                                            float* __restrict__ dd,
+                                                            const float* __restrict__ lse,
+                                                            float* __restrict__ lse2) {
   constexpr int PER = D / 64;
   const int wave = (blockIdx.x * kAuxThreads + threadIdx.x) >> 6;
   const int lane = threadIdx.x & 63;
@@ -50,7 +54,10 @@ __global__ __launch_bounds__(kAuxThreads) void row_dot_kernel(const T* __restric
   }
 #pragma unroll
   for (int m = 32; m >= 1; m >>= 1) acc += __shfl_xor(acc, m);
-  if (lane == 0) dd[(size_t)row * hq + h] = acc;
+  if (lane == 0) {
+    dd[(size_t)row * hq + h] = acc;
+    lse2[(size_t)row * hq + h] = lse[(size_t)row * hq + h] * kLog2e;
+  }
 }
 
 __global__ __launch_bounds__(kAuxThreads) void fill_zero_kernel(float4* p, size_t n4) {
@@ -92,7 +99,8 @@ __global__ __launch_bounds__(kAuxThreads) void convert_kernel(const float4* __re
 }
 
 hipError_t launch_row_dot(int dtype, const void* dO, const void* O, int rows, const int32_t* cu,
-                          int seq, int hq, int head_dim, float* dd, hipStream_t st) {
+                          int seq, int hq, int head_dim, float* dd, const float* lse, float* lse2,
+                          hipStream_t st) {
   if (rows <= 0) return hipSuccess;
   const size_t waves = (size_t)rows * hq;
   const int blocks = (int)((waves * 64 + kAuxThreads - 1) / kAuxThreads);
@@ -100,17 +108,17 @@ hipError_t launch_row_dot(int dtype, const void* dO, const void* O, int rows, co
   if (dtype == 0) {
     if (head_dim == 64)
       hipLaunchKernelGGL((row_dot_kernel<float, 64>), blocks, kAuxThreads, 0, st,
-                         (const float*)dO, (const float*)O, rows, cu, seq, hq, dd);
+                         (const float*)dO, (const float*)O, rows, cu, seq, hq, dd, lse, lse2);
     else
       hipLaunchKernelGGL((row_dot_kernel<float, 128>), blocks, kAuxThreads, 0, st,
-                         (const float*)dO, (const float*)O, rows, cu, seq, hq, dd);
+                         (const float*)dO, (const float*)O, rows, cu, seq, hq, dd, lse, lse2);
   } else {
     if (head_dim == 64)
       hipLaunchKernelGGL((row_dot_kernel<bf16, 64>), blocks, kAuxThreads, 0, st,
-                         (const bf16*)dO, (const bf16*)O, rows, cu, seq, hq, dd);
+                         (const bf16*)dO, (const bf16*)O, rows, cu, seq, hq, dd, lse, lse2);
     else
       hipLaunchKernelGGL((row_dot_kernel<bf16, 128>), blocks, kAuxThreads, 0, st,
-                         (const bf16*)dO, (const bf16*)O, rows, cu, seq, hq, dd);
+                         (const bf16*)dO, (const bf16*)O, rows, cu, seq, hq, dd, lse, lse2);
   }
   return hipGetLastError();
 }

@@ -151,14 +151,14 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, bf
     const RowTile rt = tile_info(t);
     load_tile<D>(Qd, (const bf16*)(rt.prefix ? a.q_p : a.q_s), rt.row0, rt.nr, a.hq, rt.hh, w, lane);
     load_tile<D>(Od, (const bf16*)(rt.prefix ? a.do_p : a.do_s), rt.row0, rt.nr, a.hq, rt.hh, w, lane);
-    if (w == 0) load_row_vec(Ld, (rt.prefix ? a.lse_p : a.lse_s) + rt.hh, rt.row0, rt.nr, a.hq, lane);
+    if (w == 0) load_row_vec(Ld, (rt.prefix ? a.lse2_p : a.lse2_s) + rt.hh, rt.row0, rt.nr, a.hq, lane);
     if (w == 1) load_row_vec(Ed, (rt.prefix ? a.dd_p : a.dd_s) + rt.hh, rt.row0, rt.nr, a.hq, lane);
   };
 
   // One 32-row block rb of a streamed tile against this wave's 32 keys.
   // Rows q = 32 rb + c_row0(i) + 4 h with q_lo <= q < q_hi are visible.
   auto block = [&](const bf16* Qc, const bf16* Oc, const float* Lc, const float* Ec, int rb,
-                   int q_lo, int q_hi) {
+                   int q_lo, int q_hi, bool masked) {
     // S = Q K^T, dP = dO V^T: s[i] = S[row q(i)][key my_key], dp likewise;
     // all operand reads are issued before the products
     bf16x8 qa[NS], oa[NS];
@@ -181,21 +181,28 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, bf
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     }
     __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
-    // P = exp(S - LSE) on visible rows, dS = P (dP - rowsum(dO O))
-    const int lo = q_lo - 32 * rb - 4 * h, hi = q_hi - 32 * rb - 4 * h;
+    // P = exp(S - LSE) (Lc holds LSE in the log2 domain), zero on rows
+    // outside [q_lo, q_hi); dS = P (dP - rowsum(dO O))
 #pragma unroll
     for (int g4 = 0; g4 < 4; ++g4) {
       const float4 l4 = *(const float4*)(Lc + 32 * rb + 8 * g4 + 4 * h);
-      const float4 e4 = *(const float4*)(Ec + 32 * rb + 8 * g4 + 4 * h);
-      const float lq[4] = {l4.x, l4.y, l4.z, l4.w};
-      const float eq[4] = {e4.x, e4.y, e4.z, e4.w};
+      s[4 * g4 + 0] = fast_exp2(fmaf(s[4 * g4 + 0], a.scale_log2, -l4.x));
+      s[4 * g4 + 1] = fast_exp2(fmaf(s[4 * g4 + 1], a.scale_log2, -l4.y));
+      s[4 * g4 + 2] = fast_exp2(fmaf(s[4 * g4 + 2], a.scale_log2, -l4.z));
+      s[4 * g4 + 3] = fast_exp2(fmaf(s[4 * g4 + 3], a.scale_log2, -l4.w));
+    }
+    if (masked) {  // wave-uniform: diagonal or ragged block
+      const int lo = q_lo - 32 * rb - 4 * h, hi = q_hi - 32 * rb - 4 * h;
 #pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        const int i = 4 * g4 + b;
-        const float p = fast_exp2(fmaf(s[i], a.scale_log2, -lq[b] * kLog2e));
-        s[i] = (c_row0(i) >= lo && c_row0(i) < hi) ? p : 0.f;
-        dp[i] = s[i] * (dp[i] - eq[b]);
-      }
+      for (int i = 0; i < 16; ++i) s[i] = (c_row0(i) >= lo && c_row0(i) < hi) ? s[i] : 0.f;
+    }
+#pragma unroll
+    for (int g4 = 0; g4 < 4; ++g4) {
+      const float4 e4 = *(const float4*)(Ec + 32 * rb + 8 * g4 + 4 * h);
+      dp[4 * g4 + 0] = s[4 * g4 + 0] * (dp[4 * g4 + 0] - e4.x);
+      dp[4 * g4 + 1] = s[4 * g4 + 1] * (dp[4 * g4 + 1] - e4.y);
+      dp[4 * g4 + 2] = s[4 * g4 + 2] * (dp[4 * g4 + 2] - e4.z);
+      dp[4 * g4 + 3] = s[4 * g4 + 3] * (dp[4 * g4 + 3] - e4.w);
     }
     // dV^T += dO^T P ; dK^T += Q^T dS over the 16-row k-steps v
 #pragma unroll
@@ -231,7 +238,8 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, bf
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb) {
       if (rt.causal && rt.lp_first + 32 * rb + 31 < wave_k0) continue;  // no row sees these keys
-      block(Qc, Oc, Lc, Ec, rb, q_lo, rt.nr);
+      const bool masked = rt.nr < 32 * rb + 32 || (rt.causal && rt.lp_first + 32 * rb < wave_k0 + 31);
+      block(Qc, Oc, Lc, Ec, rb, q_lo, rt.nr, masked);
     }
   };
 
@@ -373,7 +381,7 @@ __device__ __forceinline__ void bwd_q_body(const AttnArgs& a, const int bid, bf1
       qf[s] = *(const bf16x8*)(qb + off + 16 * s);
       df[s] = *(const bf16x8*)(dob + off + 16 * s);
     }
-    lse2 = (prefix_rows ? a.lse_p : a.lse_s)[row * a.hq + hq] * kLog2e;
+    lse2 = (prefix_rows ? a.lse2_p : a.lse2_s)[row * a.hq + hq];
     drow = (prefix_rows ? a.dd_p : a.dd_s)[row * a.hq + hq];
   }
   f32x16 dq[NDB];

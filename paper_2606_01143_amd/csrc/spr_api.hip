@@ -153,6 +153,7 @@ hipError_t launch_bwd(const spr_dims* d, const AttnArgs& a, int n_qz, hipStream_
 // ------------------------------------------------------------- workspace
 struct WsLayout {
   size_t dd_p = 0, dq_acc_p = 0, dd_s = 0, dq_acc_s = 0, dk_acc_p = 0, dv_acc_p = 0;
+  size_t lse2_p = 0, lse2_s = 0;
   size_t part_o = 0, part_lse = 0;
   size_t total = 0;
 };
@@ -183,16 +184,20 @@ WsLayout ws_layout(int op, const spr_dims* d, int32_t n_mb, int32_t max_len, int
     }
     case SPR_OP_SUFFIX_BWD:
       w.dd_s = take(hq * T * 4);
+      w.lse2_s = take(hq * T * 4);
       if (f32) w.dq_acc_s = take(T * hq * hd * 4);
       break;
     case SPR_OP_PREFIX_BWD:
       w.dd_p = take(hq * P * 4);
+      w.lse2_p = take(hq * P * 4);
       if (f32) w.dq_acc_p = take(P * hq * hd * 4);
       break;
     case SPR_OP_DENSE_BASELINE:
       w.dd_p = take(hq * P * 4);
+      w.lse2_p = take(hq * P * 4);
       w.dq_acc_p = take(P * hq * hd * 4);
       w.dd_s = take(hq * T * 4);
+      w.lse2_s = take(hq * T * 4);
       if (f32) w.dq_acc_s = take(T * hq * hd * 4);
       w.dk_acc_p = take(P * hkv * hd * 4);
       w.dv_acc_p = take(P * hkv * hd * 4);
@@ -403,9 +408,10 @@ spr_status spr_suffix_attn_bwd_accum(const spr_dims* dims, const void* k_p, cons
 
   const bool f32 = dims->dtype == SPR_F32;
   float* dd_s = at<float>(ws, w.dd_s);
+  float* lse2_s = at<float>(ws, w.lse2_s);
   float* dq_acc = f32 ? at<float>(ws, w.dq_acc_s) : nullptr;
   if ((st = hip_check(launch_row_dot(dims->dtype, do_s, o_s, total_len, nullptr, 0, (int)hq,
-                                     (int)hd, dd_s, stream), "row statistic")) != SPR_OK)
+                                     (int)hd, dd_s, lse_s, lse2_s, stream), "row statistic")) != SPR_OK)
     return st;
   if (f32 && (st = hip_check(launch_fill_zero(dq_acc, T * hq * hd, stream), "dq clear")) != SPR_OK)
     return st;
@@ -414,7 +420,7 @@ spr_status spr_suffix_attn_bwd_accum(const spr_dims* dims, const void* k_p, cons
   a.k_p = k_p; a.v_p = v_p;
   a.q_s = q_s; a.k_s = k_s; a.v_s = v_s; a.do_s = do_s;
   a.lse_s = const_cast<float*>(lse_s);
-  a.dd_s = dd_s; a.dq_acc_s = dq_acc;
+  a.dd_s = dd_s; a.lse2_s = lse2_s; a.dq_acc_s = dq_acc;
   a.cu = cu_seqlens;
   a.total_len = total_len;
   a.seq_base = 0;
@@ -475,9 +481,10 @@ spr_status spr_prefix_bwd(const spr_dims* dims, const void* q_p, const void* k_p
   }
   const bool f32 = dims->dtype == SPR_F32;
   float* dd_p = at<float>(ws, w.dd_p);
+  float* lse2_p = at<float>(ws, w.lse2_p);
   float* dq_acc = f32 ? at<float>(ws, w.dq_acc_p) : nullptr;
   if ((st = hip_check(launch_row_dot(dims->dtype, do_p, o_p, (int)P, nullptr, 0, (int)hq, (int)hd,
-                                     dd_p, stream), "row statistic")) != SPR_OK)
+                                     dd_p, lse_p, lse2_p, stream), "row statistic")) != SPR_OK)
     return st;
   if (f32 && (st = hip_check(launch_fill_zero(dq_acc, P * hq * hd, stream), "dq clear")) != SPR_OK)
     return st;
@@ -485,7 +492,7 @@ spr_status spr_prefix_bwd(const spr_dims* dims, const void* q_p, const void* k_p
   a.dq_p = dq_p;
   a.q_p = q_p; a.k_p = k_p; a.v_p = v_p; a.do_p = do_p;
   a.lse_p = const_cast<float*>(lse_p);
-  a.dd_p = dd_p; a.dq_acc_p = dq_acc;
+  a.dd_p = dd_p; a.lse2_p = lse2_p; a.dq_acc_p = dq_acc;
   a.n_prefix_k_tiles = tiles(dims->prefix_len, block_k(dims->dtype));
   a.prefix_rows = 1;
   a.suffix_rows = 0;
@@ -537,6 +544,8 @@ spr_status spr_dense_recompute_baseline(
   float* dq_acc_p = at<float>(ws, w.dq_acc_p);
   const bool f32 = dims->dtype == SPR_F32;
   float* dd_s = at<float>(ws, w.dd_s);
+  float* lse2_p = at<float>(ws, w.lse2_p);
+  float* lse2_s = at<float>(ws, w.lse2_s);
   float* dq_acc_s = f32 ? at<float>(ws, w.dq_acc_s) : nullptr;
   float* dk_acc = at<float>(ws, w.dk_acc_p);
   float* dv_acc = at<float>(ws, w.dv_acc_p);
@@ -563,11 +572,11 @@ spr_status spr_dense_recompute_baseline(
     const void* dop_i = have_dop ? (const char*)do_p_seq + (size_t)i * P * hq * hd * eb : nullptr;
     if (have_dop && P > 0)
       SPR_TRY(launch_row_dot(dims->dtype, dop_i, o_p, (int)P, nullptr, 0, (int)hq, (int)hd, dd_p,
-                             stream), "row statistic");
+                             lse_p, lse2_p, stream), "row statistic");
     SPR_TRY(launch_row_dot(dims->dtype, do_s, o_s, max_len, cu_seqlens, i, (int)hq, (int)hd, dd_s,
-                           stream), "row statistic");
-    a.do_p = dop_i; a.dd_p = dd_p; a.dq_acc_p = dq_acc_p;
-    a.do_s = do_s; a.dd_s = dd_s; a.dq_acc_s = dq_acc_s;
+                           lse_s, lse2_s, stream), "row statistic");
+    a.do_p = dop_i; a.dd_p = dd_p; a.lse2_p = lse2_p; a.dq_acc_p = dq_acc_p;
+    a.do_s = do_s; a.dd_s = dd_s; a.lse2_s = lse2_s; a.dq_acc_s = dq_acc_s;
     a.dq_s = dq_s;
     a.dq_p_accumulate = 1;
     a.n_prefix_k_tiles = tiles(dims->prefix_len, block_k(dims->dtype));

@@ -36,22 +36,32 @@
 namespace spr {
 
 namespace {
-constexpr int kKvBK = 128;  // keys per bwd_kv workgroup (32 per wave)
+constexpr int kKvBK = 64;   // keys per key-outer workgroup (two 32-key wave pairs)
 constexpr int kQBQ = 128;   // rows per bwd_q workgroup (32 per wave)
 }  // namespace
 
 int bwd_bf16_block_k() { return kKvBK; }
 
 // ---------------------------------------------------------------- bwd_kv
+// Key-outer role: one workgroup owns 64 keys of one kv head.  Its four waves
+// form two pairs, one per 32-key block.  In a pair, the P-wave holds K and
+// accumulates dV, the dS-wave holds V and accumulates dK:
+//   P-wave:  S = Q K^T, P = exp(S - LSE) (also written to LDS in bf16),
+//            dV^T += dO^T P
+//   dS-wave: dP = dO V^T, dS = P (dP - rowsum(dO O)) with P read from LDS,
+//            dK^T += Q^T dS
+// Every product is computed once, and each wave carries half the state of a
+// wave that did all four, so two waves fit per SIMD.
 template <int D>
 __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, bf16 (*Qs)[Tile<D>::ELEMS],
                                             bf16 (*Os)[Tile<D>::ELEMS], float (*Ls)[kTileRows],
-                                            float (*Es)[kTileRows]) {
+                                            float (*Es)[kTileRows], bf16* Px) {
   constexpr int NS = D / 16;
   constexpr int NDB = D / 32;
   constexpr int BQ = kTileRows;
   // Qs/Os: double-buffered tiles of the streamed rows' Q and dO; Ls/Es: their
-  // LSE and rowsum(dO * O)
+  // log2-domain LSE and rowsum(dO * O); Px: P of the current tile,
+  // [key block][row block][lane][16] bf16
 
   const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
   const int r = lane & 31, h = lane >> 5;
@@ -61,7 +71,7 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, bf
   const int hk = bid % a.hkv, x = bid / a.hkv;
   const int G = a.hq / a.hkv;
 
-  // ---- which 128 keys: a prefix tile, or a tile of suffix s
+  // ---- which 64 keys: a prefix tile, or a tile of suffix s
   bool kpre;
   int k0, kseg, kbase;
   if (x < a.n_prefix_k_tiles) {
@@ -78,27 +88,23 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, bf
     kpre = false;
   }
   if (k0 >= kseg) return;
-  const int wave_k0 = k0 + 32 * w;
+  const int kb = w >> 1;               // key block of this wave's pair
+  const bool pw = (w & 1) == 0;        // P-wave (dV) or dS-wave (dK)
+  const int wave_k0 = k0 + 32 * kb;
   const int my_key = min(wave_k0 + r, kseg - 1);  // keys past the end recompute the last one
+  bf16* Pblk = Px + kb * (2 * 64 * 16);  // this pair's P exchange, [rb][lane][16]
 
-  // K, V as the B operand of S = Q K^T and dP = dO V^T (natural k)
-  bf16x8 kf[NS], vf[NS];
+  // K (P-wave) or V (dS-wave) as the B operand of S = Q K^T / dP = dO V^T
+  bf16x8 kvf[NS];
   {
-    const bf16* kg = (const bf16*)(kpre ? a.k_p : a.k_s);
-    const bf16* vg = (const bf16*)(kpre ? a.v_p : a.v_s);
+    const bf16* g = (const bf16*)(pw ? (kpre ? a.k_p : a.k_s) : (kpre ? a.v_p : a.v_s));
     const size_t off = ((size_t)(kbase + my_key) * a.hkv + hk) * D + 8 * h;
 #pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      kf[s] = *(const bf16x8*)(kg + off + 16 * s);
-      vf[s] = *(const bf16x8*)(vg + off + 16 * s);
-    }
+    for (int s = 0; s < NS; ++s) kvf[s] = *(const bf16x8*)(g + off + 16 * s);
   }
-  f32x16 dk[NDB], dv[NDB];
+  f32x16 acc[NDB];  // dV^T (P-wave) or dK^T (dS-wave), kept in AGPRs
 #pragma unroll
-  for (int db = 0; db < NDB; ++db) {
-    dk[db] = zero16();
-    dv[db] = zero16();
-  }
+  for (int db = 0; db < NDB; ++db) acc[db] = zero16();
 
   // ---- the row tiles this key tile sees, per q head of the group:
   // prefix key tile: prefix rows from k0 on (causal) and/or every suffix row
@@ -155,75 +161,42 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, bf
     if (w == 1) load_row_vec(Ed, (rt.prefix ? a.dd_p : a.dd_s) + rt.hh, rt.row0, rt.nr, a.hq, lane);
   };
 
-  // One 32-row block rb of a streamed tile against this wave's 32 keys.
-  // Rows q = 32 rb + c_row0(i) + 4 h with q_lo <= q < q_hi are visible.
-  auto block = [&](const bf16* Qc, const bf16* Oc, const float* Lc, const float* Ec, int rb,
-                   int q_lo, int q_hi, bool masked) {
-    // S = Q K^T, dP = dO V^T: s[i] = S[row q(i)][key my_key], dp likewise;
-    // all operand reads are issued before the products
-    bf16x8 qa[NS], oa[NS];
+  // Row block rb (rows 32 rb + c_row0(i) + 4 h of the tile) against this
+  // pair's 32 keys: hidden when a causal tile's rows all precede the keys;
+  // masked (rows outside [q_lo, nr) get P = 0) on the diagonal or a ragged end.
+  auto hidden = [&](const RowTile& rt, int rb) { return rt.causal && rt.lp_first + 32 * rb + 31 < wave_k0; };
+  auto masked = [&](const RowTile& rt, int rb) {
+    return rt.nr < 32 * rb + 32 || (rt.causal && rt.lp_first + 32 * rb < wave_k0 + 31);
+  };
+  // the S or dP product of block rb: A = Q or dO tile rows, B = kvf
+  auto product = [&](const bf16* T, int rb) {
+    bf16x8 ta[NS];
 #pragma unroll
-    for (int k = 0; k < NS; ++k) {
-      qa[k] = row_frag<D>(Qc, fo, 32 * rb, k);
-      oa[k] = row_frag<D>(Oc, fo, 32 * rb, k);
-    }
-    f32x16 s = zero16(), dp = zero16();
+    for (int k = 0; k < NS; ++k) ta[k] = row_frag<D>(T, fo, 32 * rb, k);
+    f32x16 c = zero16();
 #pragma unroll
-    for (int k = 0; k < NS; ++k) {
-      s = mfma32(qa[k], kf[k], s);
-      dp = mfma32(oa[k], vf[k], dp);
-    }
-    // schedule: four reads ahead of the products, then one read per product
+    for (int k = 0; k < NS; ++k) c = mfma32(ta[k], kvf[k], c);
     __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
-    for (int k = 0; k < 2 * NS - 4; ++k) {
+    for (int k = 0; k < NS - 4; ++k) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
     }
     __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
-    // P = exp(S - LSE) (Lc holds LSE in the log2 domain), zero on rows
-    // outside [q_lo, q_hi); dS = P (dP - rowsum(dO O))
-#pragma unroll
-    for (int g4 = 0; g4 < 4; ++g4) {
-      const float4 l4 = *(const float4*)(Lc + 32 * rb + 8 * g4 + 4 * h);
-      s[4 * g4 + 0] = fast_exp2(fmaf(s[4 * g4 + 0], a.scale_log2, -l4.x));
-      s[4 * g4 + 1] = fast_exp2(fmaf(s[4 * g4 + 1], a.scale_log2, -l4.y));
-      s[4 * g4 + 2] = fast_exp2(fmaf(s[4 * g4 + 2], a.scale_log2, -l4.z));
-      s[4 * g4 + 3] = fast_exp2(fmaf(s[4 * g4 + 3], a.scale_log2, -l4.w));
-    }
-    if (masked) {  // wave-uniform: diagonal or ragged block
-      const int lo = q_lo - 32 * rb - 4 * h, hi = q_hi - 32 * rb - 4 * h;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) s[i] = (c_row0(i) >= lo && c_row0(i) < hi) ? s[i] : 0.f;
-    }
-#pragma unroll
-    for (int g4 = 0; g4 < 4; ++g4) {
-      const float4 e4 = *(const float4*)(Ec + 32 * rb + 8 * g4 + 4 * h);
-      dp[4 * g4 + 0] = s[4 * g4 + 0] * (dp[4 * g4 + 0] - e4.x);
-      dp[4 * g4 + 1] = s[4 * g4 + 1] * (dp[4 * g4 + 1] - e4.y);
-      dp[4 * g4 + 2] = s[4 * g4 + 2] * (dp[4 * g4 + 2] - e4.z);
-      dp[4 * g4 + 3] = s[4 * g4 + 3] * (dp[4 * g4 + 3] - e4.w);
-    }
-    // dV^T += dO^T P ; dK^T += Q^T dS over the 16-row k-steps v
+    return c;
+  };
+  // acc += (dO or Q)^T (P or dS) for block rb, operands pb[v] (C-order rows)
+  auto accumulate = [&](const bf16* T, int rb, const bf16x8 (&pb)[2]) {
 #pragma unroll
     for (int v = 0; v < 2; ++v) {
-      const bf16x8 pb = c_kfrag(s, v);
-      const bf16x8 sb = c_kfrag(dp, v);
-      bf16x8 ot[NDB], qt[NDB];
+      bf16x8 at[NDB];
 #pragma unroll
-      for (int db = 0; db < NDB; ++db) {
-        ot[db] = tr_frag<D>(Oc, fo, 32 * rb + 16 * v, db);
-        qt[db] = tr_frag<D>(Qc, fo, 32 * rb + 16 * v, db);
-      }
+      for (int db = 0; db < NDB; ++db) at[db] = tr_frag<D>(T, fo, 32 * rb + 16 * v, db);
 #pragma unroll
-      for (int db = 0; db < NDB; ++db) {
-        mfma32_acc(dv[db], ot[db], pb);
-        mfma32_acc(dk[db], qt[db], sb);
-      }
-      // two operands (four transposed reads) ahead of the products
+      for (int db = 0; db < NDB; ++db) mfma32_acc(acc[db], at[db], pb[v]);
       __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
-      for (int k = 0; k < 2 * NDB - 2; ++k) {
+      for (int k = 0; k < NDB - 2; ++k) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
       }
@@ -233,13 +206,67 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, bf
 
   auto compute = [&](int t, const bf16* Qc, const bf16* Oc, const float* Lc, const float* Ec) {
     const RowTile rt = tile_info(t);
-    // causal tiles: row lp_first + q sees my_key iff q >= my_key - lp_first
-    const int q_lo = rt.causal ? my_key - rt.lp_first : 0;
+    const int q_lo = rt.causal ? my_key - rt.lp_first : 0;  // row lp_first + q sees my_key iff q >= q_lo
+    // phase 1: P-wave S -> P (kept as bf16 operands, copied to LDS);
+    //          dS-wave dP.  One product call site for both roles.
+    bf16x8 pb[2][2];
+    f32x16 dpv[2];
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb) {
-      if (rt.causal && rt.lp_first + 32 * rb + 31 < wave_k0) continue;  // no row sees these keys
-      const bool masked = rt.nr < 32 * rb + 32 || (rt.causal && rt.lp_first + 32 * rb < wave_k0 + 31);
-      block(Qc, Oc, Lc, Ec, rb, q_lo, rt.nr, masked);
+      if (hidden(rt, rb)) continue;
+      f32x16 c = product(pw ? Qc : Oc, rb);
+      if (pw) {
+#pragma unroll
+        for (int g4 = 0; g4 < 4; ++g4) {
+          const float4 l4 = *(const float4*)(Lc + 32 * rb + 8 * g4 + 4 * h);
+          c[4 * g4 + 0] = fast_exp2(fmaf(c[4 * g4 + 0], a.scale_log2, -l4.x));
+          c[4 * g4 + 1] = fast_exp2(fmaf(c[4 * g4 + 1], a.scale_log2, -l4.y));
+          c[4 * g4 + 2] = fast_exp2(fmaf(c[4 * g4 + 2], a.scale_log2, -l4.z));
+          c[4 * g4 + 3] = fast_exp2(fmaf(c[4 * g4 + 3], a.scale_log2, -l4.w));
+        }
+        if (masked(rt, rb)) {
+          const int lo = q_lo - 32 * rb - 4 * h, hi = rt.nr - 32 * rb - 4 * h;
+#pragma unroll
+          for (int i = 0; i < 16; ++i) c[i] = (c_row0(i) >= lo && c_row0(i) < hi) ? c[i] : 0.f;
+        }
+        pb[rb][0] = c_kfrag(c, 0);
+        pb[rb][1] = c_kfrag(c, 1);
+        bf16x8* px = (bf16x8*)(Pblk + (rb * 64 + lane) * 16);
+        px[0] = pb[rb][0];
+        px[1] = pb[rb][1];
+      } else {
+        dpv[rb] = c;
+      }
+    }
+    __syncthreads();  // P of both row blocks visible to the dS-waves
+    // phase 2: P-wave dV^T += dO^T P; dS-wave dS -> dK^T += Q^T dS.  One
+    // accumulate call site, so the AGPR accumulators are never copied.
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb) {
+      if (hidden(rt, rb)) continue;
+      bf16x8 ops[2];
+      if (pw) {
+        ops[0] = pb[rb][0];
+        ops[1] = pb[rb][1];
+      } else {
+        const bf16x8* px = (const bf16x8*)(Pblk + (rb * 64 + lane) * 16);
+        const bf16x8 p0 = px[0], p1 = px[1];
+        f32x16 ds;
+#pragma unroll
+        for (int g4 = 0; g4 < 4; ++g4) {
+          const float4 e4 = *(const float4*)(Ec + 32 * rb + 8 * g4 + 4 * h);
+          const float eq[4] = {e4.x, e4.y, e4.z, e4.w};
+#pragma unroll
+          for (int b = 0; b < 4; ++b) {
+            const int i = 4 * g4 + b;
+            const float p = (float)(i < 8 ? p0[i] : p1[i - 8]);
+            ds[i] = p * (dpv[rb][i] - eq[b]);
+          }
+        }
+        ops[0] = c_kfrag(ds, 0);
+        ops[1] = c_kfrag(ds, 1);
+      }
+      accumulate(pw ? Oc : Qc, rb, ops);
     }
   };
 
@@ -254,63 +281,49 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, bf
   }
 
   acc_fence();
-  // ---- epilogue: dk[db][i] is dK^T[d = 32 db + c_row0(i) + 4 h][key wave_k0 + r]
+  // ---- epilogue: acc[db][i] is dV^T or dK^T at d = 32 db + c_row0(i) + 4 h,
+  // key wave_k0 + r
   if (wave_k0 + r >= kseg) return;
   const int key = wave_k0 + r;
+  const float sc = pw ? 1.f : a.scale;
   if (kpre) {
     const size_t off = ((size_t)key * a.hkv + hk) * D + 4 * h;
+    float* cache = pw ? a.gv : a.gk;
     if (a.pk_mode == kPkAccumulate) {
 #pragma unroll
       for (int db = 0; db < NDB; ++db)
 #pragma unroll
         for (int g4 = 0; g4 < 4; ++g4) {
-          float4* pk = (float4*)(a.gk + off + 32 * db + 8 * g4);
-          float4* pv = (float4*)(a.gv + off + 32 * db + 8 * g4);
-          float4 ck = *pk, cv = *pv;
-          ck.x += dk[db][4 * g4] * a.scale;
-          ck.y += dk[db][4 * g4 + 1] * a.scale;
-          ck.z += dk[db][4 * g4 + 2] * a.scale;
-          ck.w += dk[db][4 * g4 + 3] * a.scale;
-          cv.x += dv[db][4 * g4];
-          cv.y += dv[db][4 * g4 + 1];
-          cv.z += dv[db][4 * g4 + 2];
-          cv.w += dv[db][4 * g4 + 3];
-          *pk = ck;
-          *pv = cv;
+          float4* pc = (float4*)(cache + off + 32 * db + 8 * g4);
+          float4 c = *pc;
+          c.x += acc[db][4 * g4] * sc;
+          c.y += acc[db][4 * g4 + 1] * sc;
+          c.z += acc[db][4 * g4 + 2] * sc;
+          c.w += acc[db][4 * g4 + 3] * sc;
+          *pc = c;
         }
     } else {
-      bf16* okp = (bf16*)a.dk_p;
-      bf16* ovp = (bf16*)a.dv_p;
+      bf16* out = (bf16*)(pw ? a.dv_p : a.dk_p);
 #pragma unroll
       for (int db = 0; db < NDB; ++db)
 #pragma unroll
         for (int g4 = 0; g4 < 4; ++g4) {
-          const float4 ck = *(const float4*)(a.gk + off + 32 * db + 8 * g4);
-          const float4 cv = *(const float4*)(a.gv + off + 32 * db + 8 * g4);
-          const bf16x4 vk = {(bf16)(dk[db][4 * g4] * a.scale + ck.x),
-                             (bf16)(dk[db][4 * g4 + 1] * a.scale + ck.y),
-                             (bf16)(dk[db][4 * g4 + 2] * a.scale + ck.z),
-                             (bf16)(dk[db][4 * g4 + 3] * a.scale + ck.w)};
-          const bf16x4 vv = {(bf16)(dv[db][4 * g4] + cv.x), (bf16)(dv[db][4 * g4 + 1] + cv.y),
-                             (bf16)(dv[db][4 * g4 + 2] + cv.z), (bf16)(dv[db][4 * g4 + 3] + cv.w)};
-          *(bf16x4*)(okp + off + 32 * db + 8 * g4) = vk;
-          *(bf16x4*)(ovp + off + 32 * db + 8 * g4) = vv;
+          const float4 c = *(const float4*)(cache + off + 32 * db + 8 * g4);
+          const bf16x4 v = {(bf16)(acc[db][4 * g4] * sc + c.x), (bf16)(acc[db][4 * g4 + 1] * sc + c.y),
+                            (bf16)(acc[db][4 * g4 + 2] * sc + c.z), (bf16)(acc[db][4 * g4 + 3] * sc + c.w)};
+          *(bf16x4*)(out + off + 32 * db + 8 * g4) = v;
         }
     }
   } else {
     const size_t off = ((size_t)(kbase + key) * a.hkv + hk) * D + 4 * h;
-    bf16* oks = (bf16*)a.dk_s;
-    bf16* ovs = (bf16*)a.dv_s;
+    bf16* out = (bf16*)(pw ? a.dv_s : a.dk_s);
 #pragma unroll
     for (int db = 0; db < NDB; ++db)
 #pragma unroll
       for (int g4 = 0; g4 < 4; ++g4) {
-        const bf16x4 vk = {(bf16)(dk[db][4 * g4] * a.scale), (bf16)(dk[db][4 * g4 + 1] * a.scale),
-                           (bf16)(dk[db][4 * g4 + 2] * a.scale), (bf16)(dk[db][4 * g4 + 3] * a.scale)};
-        const bf16x4 vv = {(bf16)dv[db][4 * g4], (bf16)dv[db][4 * g4 + 1], (bf16)dv[db][4 * g4 + 2],
-                           (bf16)dv[db][4 * g4 + 3]};
-        *(bf16x4*)(oks + off + 32 * db + 8 * g4) = vk;
-        *(bf16x4*)(ovs + off + 32 * db + 8 * g4) = vv;
+        const bf16x4 v = {(bf16)(acc[db][4 * g4] * sc), (bf16)(acc[db][4 * g4 + 1] * sc),
+                          (bf16)(acc[db][4 * g4 + 2] * sc), (bf16)(acc[db][4 * g4 + 3] * sc)};
+        *(bf16x4*)(out + off + 32 * db + 8 * g4) = v;
       }
   }
 }
@@ -490,17 +503,18 @@ __device__ __forceinline__ void bwd_q_body(const AttnArgs& a, const int bid, bf1
 // The heavier role goes first; both segments start on a multiple of 8 blocks
 // so the XCD mapping of each role holds.
 template <int D>
-__global__ __launch_bounds__(kThreads, 1) void bwd_bf16_kernel(AttnArgs a, int n_first, int n_kv,
+__global__ __launch_bounds__(kThreads, 2) void bwd_bf16_kernel(AttnArgs a, int n_first, int n_kv,
                                                                int n_q, int kv_first) {
   constexpr int TE = Tile<D>::ELEMS;
   __shared__ __attribute__((aligned(1024))) bf16 tiles[4][TE];
   __shared__ __attribute__((aligned(256))) float rowv[4][kTileRows];
+  __shared__ __attribute__((aligned(1024))) bf16 pex[2 * 2 * 64 * 16];
   const int b = blockIdx.x;
   const bool first = b < n_first;
   const int bid = first ? b : b - n_first;
   // the first segment is padded to a multiple of 8 blocks: padding exits
   if (first == (kv_first != 0)) {
-    if (bid < n_kv) bwd_kv_body<D>(a, bid, tiles, tiles + 2, rowv, rowv + 2);
+    if (bid < n_kv) bwd_kv_body<D>(a, bid, tiles, tiles + 2, rowv, rowv + 2, pex);
   } else {
     if (bid < n_q) bwd_q_body<D>(a, bid, tiles, tiles + 2);
   }

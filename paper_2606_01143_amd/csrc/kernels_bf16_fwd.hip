@@ -134,6 +134,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(AttnArgs a) {
     for (int s = 0; s < NS; ++s)
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) st[kb] = mfma32(row_frag<D>(Kc, fo, 32 * kb, s), qf[s], st[kb]);
+    sched_reads_ahead<2 * NS, 1, 4>();
 #define SC(e) st[(e) >> 4][(e) & 15]
     if (nk < BK || (causal && k0 + BK - 1 > wave_lp0)) {  // partial or diagonal tile
       // keys kk = 32 (e / 16) + c_row0(e % 16) + 4 h are visible iff kk < lim
@@ -170,6 +171,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(AttnArgs a) {
 #pragma unroll
       for (int db = 0; db < NDB; ++db) o[db] = mfma32(tr_frag<D>(Vc, fo, 16 * u, db), pb, o[db]);
     }
+    sched_reads_ahead<BK / 16 * NDB, 2, 2>();
   };
 
   if (t_begin < t_end) issue(t_begin, Ks[0], Vs[0]);

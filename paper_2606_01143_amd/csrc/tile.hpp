@@ -87,6 +87,21 @@ __device__ __forceinline__ f32x16 zero16() {
 // 2^-126 flush to zero, far below bf16 resolution.
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Scheduling templates for a run of n products fed by LDS reads (r reads
+// per product): the first `ahead` reads are issued before any product, then
+// each product is followed by the reads of a later one, so the read latency
+// hides behind the matrix work instead of stalling every product.
+template <int N, int R, int AHEAD>
+__device__ __forceinline__ void sched_reads_ahead() {
+  __builtin_amdgcn_sched_group_barrier(0x100, AHEAD * R, 0);
+#pragma unroll
+  for (int k = 0; k < N - AHEAD; ++k) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, R, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, AHEAD, 0);
+}
+
 // Keeps the compiler from moving memory operations across this point (the
 // next tile's loads must be issued before the current tile's products).
 __device__ __forceinline__ void compiler_fence() { asm volatile("" ::: "memory"); }

@@ -67,13 +67,16 @@ struct AttnArgs {
   // query-outer launches (forward, fp32 dQ): grid.x = prefix row tiles then
   // suffix row tiles of suffix seq_base + blockIdx.z
   int32_t n_prefix_q_tiles;
-  // bf16 forward over suffix rows may split each row tile's keys into
-  // n_split contiguous ranges; split j writes its normalized partial output
-  // part_o[j][row][h][:] (fp32) and partial log2-domain LSE
-  // part_lse[j][row][h], merged afterwards by the combine kernel
+  // bf16 forward and backward over suffix rows only may split each row
+  // tile's keys into n_split contiguous ranges.  Forward: split j writes its
+  // normalized partial output part_o[j][row][h][:] (fp32) and partial
+  // log2-domain LSE part_lse[j][row][h]; backward: split j writes its
+  // unscaled partial dQ part_dq[j][row][h][:] (fp32).  A combine kernel
+  // merges the splits in index order afterwards.
   int32_t n_split;
   float* part_o;
   float* part_lse;
+  float* part_dq;
   int32_t n_suffix_q_tiles;
   // key-outer launches (backward): grid.x = prefix key tiles, then
   // n_seq * n_suffix_k_tiles suffix key tiles

@@ -29,6 +29,8 @@
 // direct-to-LDS loads issued one tile ahead of the products.  The loads
 // are invisible to the compiler's wait tracking: every tile is read only
 // after tile_barrier (vmcnt(0) + workgroup barrier).
+#include <algorithm>
+
 #include "common.hpp"
 #include "launch.hpp"
 #include "tile.hpp"
@@ -52,16 +54,35 @@ int bwd_bf16_block_k() { return kKvBK; }
 //            dK^T += Q^T dS
 // Every product is computed once, and each wave carries half the state of a
 // wave that did all four, so two waves fit per SIMD.
+//
+// The rows stream through LDS in 32-row tiles.  The dS-wave runs one tile
+// behind its P-wave: between two workgroup barriers the P-wave takes tile t
+// (product, exp, P to LDS, accumulate) while the dS-wave takes tile t - 1
+// (product, P from LDS, dS, accumulate).  Both waves then do the same kind
+// and amount of work per barrier interval, and one barrier per tile both
+// publishes P and retires a buffer.  Tiles t - 1 and t are read while tile
+// t + 1 loads, so the Q/dO tiles are triple-buffered, and P is
+// double-buffered.
+namespace {
+constexpr int kKvBQ = 32;  // rows per key-outer tile
+constexpr int kKvBufs = 3;
+}  // namespace
+
 template <int D>
-__device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, bf16 (*Qs)[Tile<D>::ELEMS],
-                                            bf16 (*Os)[Tile<D>::ELEMS], float (*Ls)[kTileRows],
-                                            float (*Es)[kTileRows], bf16* Px) {
+struct KvLds {
+  static constexpr int TE = kKvBQ * D;  // bf16 elements of one 32-row tile
+  bf16 q[kKvBufs][TE];
+  bf16 o[kKvBufs][TE];
+  float l[kKvBufs][64];  // log2-domain LSE of the tile's rows (32 used)
+  float e[kKvBufs][64];  // rowsum(dO * O) of the tile's rows (32 used)
+  bf16 p[2][2][64 * 16];  // P exchange [tile parity][key block][lane][16]
+};
+
+template <int D>
+__device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, KvLds<D>& L) {
   constexpr int NS = D / 16;
   constexpr int NDB = D / 32;
-  constexpr int BQ = kTileRows;
-  // Qs/Os: double-buffered tiles of the streamed rows' Q and dO; Ls/Es: their
-  // log2-domain LSE and rowsum(dO * O); Px: P of the current tile,
-  // [key block][row block][lane][16] bf16
+  constexpr int BQ = kKvBQ;
 
   const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
   const int r = lane & 31, h = lane >> 5;
@@ -71,16 +92,21 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, bf
   const int hk = bid % a.hkv, x = bid / a.hkv;
   const int G = a.hq / a.hkv;
 
-  // ---- which 64 keys: a prefix tile, or a tile of suffix s
+  // ---- which 64 keys: a prefix tile, or a tile of suffix s.  Launches
+  // without prefix rows take the suffix key tiles first: the causal tiles at
+  // the start of a suffix carry about as many rows as a prefix tile, and the
+  // shorter ones should not start last.
+  const int n_sfx = a.n_seq * a.n_suffix_k_tiles;
+  const bool sfx_first = !a.prefix_rows;
   bool kpre;
   int k0, kseg, kbase;
-  if (x < a.n_prefix_k_tiles) {
+  if (sfx_first ? x >= n_sfx : x < a.n_prefix_k_tiles) {
     kpre = true;
-    k0 = x * kKvBK;
+    k0 = (sfx_first ? x - n_sfx : x) * kKvBK;
     kseg = a.P;
     kbase = 0;
   } else {
-    const int y = x - a.n_prefix_k_tiles;
+    const int y = sfx_first ? x : x - a.n_prefix_k_tiles;
     const int s = a.seq_base + y / a.n_suffix_k_tiles;
     k0 = (y % a.n_suffix_k_tiles) * kKvBK;
     kbase = a.cu[s];
@@ -92,7 +118,6 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, bf
   const bool pw = (w & 1) == 0;        // P-wave (dV) or dS-wave (dK)
   const int wave_k0 = k0 + 32 * kb;
   const int my_key = min(wave_k0 + r, kseg - 1);  // keys past the end recompute the last one
-  bf16* Pblk = Px + kb * (2 * 64 * 16);  // this pair's P exchange, [rb][lane][16]
 
   // K (P-wave) or V (dS-wave) as the B operand of S = Q K^T / dP = dO V^T
   bf16x8 kvf[NS];
@@ -102,11 +127,11 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, bf
 #pragma unroll
     for (int s = 0; s < NS; ++s) kvf[s] = *(const bf16x8*)(g + off + 16 * s);
   }
-  f32x16 acc[NDB];  // dV^T (P-wave) or dK^T (dS-wave), kept in AGPRs
+  f32x16 acc[NDB];  // dV^T (P-wave) or dK^T (dS-wave)
 #pragma unroll
   for (int db = 0; db < NDB; ++db) acc[db] = zero16();
 
-  // ---- the row tiles this key tile sees, per q head of the group:
+  // ---- the 32-row tiles this key tile sees, per q head of the group:
   // prefix key tile: prefix rows from k0 on (causal) and/or every suffix row
   // of suffixes seq_base .. seq_base + n_seq - 1 (all visible);
   // suffix key tile: the suffix's own rows from k0 on (causal).
@@ -127,10 +152,24 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, bf
     int hh, row0, nr, lp_first;
     bool prefix, causal;
   };
-  auto tile_info = [&](int t) {
+  // Tiles run head by head, j = 0 .. per_head - 1 within a head.  The loop
+  // keeps (head, j) cursors instead of dividing a flat index: every wave of
+  // the CU leaves a barrier at once, and their divisions would queue on the
+  // shared scalar unit.
+  struct Cursor {
+    int g, j, buf;  // q head of the group, tile within it, LDS buffer
+  };
+  auto advance = [&](Cursor& c) {
+    if (++c.j == per_head) {
+      c.j = 0;
+      ++c.g;
+    }
+    c.buf = c.buf == kKvBufs - 1 ? 0 : c.buf + 1;
+  };
+  auto tile_info = [&](const Cursor& c) {
     RowTile rt;
-    rt.hh = hk * G + t / per_head;
-    const int j = t % per_head;
+    rt.hh = hk * G + c.g;
+    const int j = c.j;
     if (j < n_pr) {
       rt.prefix = true;
       rt.causal = true;
@@ -153,26 +192,32 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, bf
     return rt;
   };
 
-  auto issue = [&](int t, bf16* Qd, bf16* Od, float* Ld, float* Ed) {
-    const RowTile rt = tile_info(t);
-    load_tile<D>(Qd, (const bf16*)(rt.prefix ? a.q_p : a.q_s), rt.row0, rt.nr, a.hq, rt.hh, w, lane);
-    load_tile<D>(Od, (const bf16*)(rt.prefix ? a.do_p : a.do_s), rt.row0, rt.nr, a.hq, rt.hh, w, lane);
-    if (w == 0) load_row_vec(Ld, (rt.prefix ? a.lse2_p : a.lse2_s) + rt.hh, rt.row0, rt.nr, a.hq, lane);
-    if (w == 1) load_row_vec(Ed, (rt.prefix ? a.dd_p : a.dd_s) + rt.hh, rt.row0, rt.nr, a.hq, lane);
+  // tile t's loads, split over the four waves
+  const bf16 *q_p = in_sgpr((const bf16*)a.q_p), *q_s = in_sgpr((const bf16*)a.q_s);
+  const bf16 *do_p = in_sgpr((const bf16*)a.do_p), *do_s = in_sgpr((const bf16*)a.do_s);
+  const float *l_p = in_sgpr((const float*)a.lse2_p), *l_s = in_sgpr((const float*)a.lse2_s);
+  const float *e_p = in_sgpr((const float*)a.dd_p), *e_s = in_sgpr((const float*)a.dd_s);
+  auto issue = [&](const Cursor& cur) {
+    const RowTile rt = tile_info(cur);
+    const int b = cur.buf;
+    load_tile<D, 4, BQ>(L.q[b], pick(rt.prefix, q_p, q_s), rt.row0, rt.nr, a.hq, rt.hh, w, lane);
+    load_tile<D, 4, BQ>(L.o[b], pick(rt.prefix, do_p, do_s), rt.row0, rt.nr, a.hq, rt.hh, w, lane);
+    if (w == 0) load_row_vec(L.l[b], pick(rt.prefix, l_p, l_s) + rt.hh, rt.row0, rt.nr, a.hq, lane);
+    if (w == 1) load_row_vec(L.e[b], pick(rt.prefix, e_p, e_s) + rt.hh, rt.row0, rt.nr, a.hq, lane);
   };
 
-  // Row block rb (rows 32 rb + c_row0(i) + 4 h of the tile) against this
-  // pair's 32 keys: hidden when a causal tile's rows all precede the keys;
-  // masked (rows outside [q_lo, nr) get P = 0) on the diagonal or a ragged end.
-  auto hidden = [&](const RowTile& rt, int rb) { return rt.causal && rt.lp_first + 32 * rb + 31 < wave_k0; };
-  auto masked = [&](const RowTile& rt, int rb) {
-    return rt.nr < 32 * rb + 32 || (rt.causal && rt.lp_first + 32 * rb < wave_k0 + 31);
+  // A tile whose rows all precede this pair's keys (causal) contributes
+  // nothing: both waves of the pair skip it.  Masked (rows outside
+  // [q_lo, nr) get P = 0): the diagonal tile or a ragged end.
+  auto hidden = [&](const RowTile& rt) { return rt.causal && rt.lp_first + BQ - 1 < wave_k0; };
+  auto masked = [&](const RowTile& rt) {
+    return rt.nr < BQ || (rt.causal && rt.lp_first < wave_k0 + 31);
   };
-  // the S or dP product of block rb: A = Q or dO tile rows, B = kvf
-  auto product = [&](const bf16* T, int rb) {
+  // S or dP of the tile: A = Q or dO tile rows, B = kvf
+  auto product = [&](const bf16* T) {
     bf16x8 ta[NS];
 #pragma unroll
-    for (int k = 0; k < NS; ++k) ta[k] = row_frag<D>(T, fo, 32 * rb, k);
+    for (int k = 0; k < NS; ++k) ta[k] = row_frag<D>(T, fo, 0, k);
     f32x16 c = zero16();
 #pragma unroll
     for (int k = 0; k < NS; ++k) c = mfma32(ta[k], kvf[k], c);
@@ -185,15 +230,15 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, bf
     __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
     return c;
   };
-  // acc += (dO or Q)^T (P or dS) for block rb, operands pb[v] (C-order rows)
-  auto accumulate = [&](const bf16* T, int rb, const bf16x8 (&pb)[2]) {
+  // acc += (dO or Q)^T (P or dS), operands pb[v] (C-order rows)
+  auto accumulate = [&](const bf16* T, const bf16x8 (&pb)[2]) {
 #pragma unroll
     for (int v = 0; v < 2; ++v) {
       bf16x8 at[NDB];
 #pragma unroll
-      for (int db = 0; db < NDB; ++db) at[db] = tr_frag<D>(T, fo, 32 * rb + 16 * v, db);
+      for (int db = 0; db < NDB; ++db) at[db] = tr_frag<D>(T, fo, 16 * v, db);
 #pragma unroll
-      for (int db = 0; db < NDB; ++db) mfma32_acc(acc[db], at[db], pb[v]);
+      for (int db = 0; db < NDB; ++db) acc[db] = mfma32(at[db], pb[v], acc[db]);
       __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
       for (int k = 0; k < NDB - 2; ++k) {
@@ -204,83 +249,81 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, bf
     }
   };
 
-  auto compute = [&](int t, const bf16* Qc, const bf16* Oc, const float* Lc, const float* Ec) {
-    const RowTile rt = tile_info(t);
-    const int q_lo = rt.causal ? my_key - rt.lp_first : 0;  // row lp_first + q sees my_key iff q >= q_lo
-    // phase 1: P-wave S -> P (kept as bf16 operands, copied to LDS);
-    //          dS-wave dP.  One product call site for both roles.
-    bf16x8 pb[2][2];
-    f32x16 dpv[2];
+  // this wave's work on tile tc: one product, the role's elementwise step,
+  // one accumulation
+  auto compute = [&](int tc, const RowTile& rt, const int b) {
+    const bf16* Qc = L.q[b];
+    const bf16* Oc = L.o[b];
+    bf16* px = L.p[tc & 1][kb] + lane * 16;
+    f32x16 c = product(pw ? Qc : Oc);
+    bf16x8 ops[2];
+    if (pw) {
+      const float* Lc = L.l[b];
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb) {
-      if (hidden(rt, rb)) continue;
-      f32x16 c = product(pw ? Qc : Oc, rb);
-      if (pw) {
-#pragma unroll
-        for (int g4 = 0; g4 < 4; ++g4) {
-          const float4 l4 = *(const float4*)(Lc + 32 * rb + 8 * g4 + 4 * h);
-          c[4 * g4 + 0] = fast_exp2(fmaf(c[4 * g4 + 0], a.scale_log2, -l4.x));
-          c[4 * g4 + 1] = fast_exp2(fmaf(c[4 * g4 + 1], a.scale_log2, -l4.y));
-          c[4 * g4 + 2] = fast_exp2(fmaf(c[4 * g4 + 2], a.scale_log2, -l4.z));
-          c[4 * g4 + 3] = fast_exp2(fmaf(c[4 * g4 + 3], a.scale_log2, -l4.w));
-        }
-        if (masked(rt, rb)) {
-          const int lo = q_lo - 32 * rb - 4 * h, hi = rt.nr - 32 * rb - 4 * h;
-#pragma unroll
-          for (int i = 0; i < 16; ++i) c[i] = (c_row0(i) >= lo && c_row0(i) < hi) ? c[i] : 0.f;
-        }
-        pb[rb][0] = c_kfrag(c, 0);
-        pb[rb][1] = c_kfrag(c, 1);
-        bf16x8* px = (bf16x8*)(Pblk + (rb * 64 + lane) * 16);
-        px[0] = pb[rb][0];
-        px[1] = pb[rb][1];
-      } else {
-        dpv[rb] = c;
+      for (int g4 = 0; g4 < 4; ++g4) {
+        const float4 l4 = *(const float4*)(Lc + 8 * g4 + 4 * h);
+        c[4 * g4 + 0] = fast_exp2(fmaf(c[4 * g4 + 0], a.scale_log2, -l4.x));
+        c[4 * g4 + 1] = fast_exp2(fmaf(c[4 * g4 + 1], a.scale_log2, -l4.y));
+        c[4 * g4 + 2] = fast_exp2(fmaf(c[4 * g4 + 2], a.scale_log2, -l4.z));
+        c[4 * g4 + 3] = fast_exp2(fmaf(c[4 * g4 + 3], a.scale_log2, -l4.w));
       }
-    }
-    __syncthreads();  // P of both row blocks visible to the dS-waves
-    // phase 2: P-wave dV^T += dO^T P; dS-wave dS -> dK^T += Q^T dS.  One
-    // accumulate call site, so the AGPR accumulators are never copied.
+      if (masked(rt)) {
+        // row lp_first + q sees my_key iff q >= q_lo
+        const int q_lo = rt.causal ? my_key - rt.lp_first : 0;
+        const int lo = q_lo - 4 * h, hi = rt.nr - 4 * h;
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb) {
-      if (hidden(rt, rb)) continue;
-      bf16x8 ops[2];
-      if (pw) {
-        ops[0] = pb[rb][0];
-        ops[1] = pb[rb][1];
-      } else {
-        const bf16x8* px = (const bf16x8*)(Pblk + (rb * 64 + lane) * 16);
-        const bf16x8 p0 = px[0], p1 = px[1];
-        f32x16 ds;
-#pragma unroll
-        for (int g4 = 0; g4 < 4; ++g4) {
-          const float4 e4 = *(const float4*)(Ec + 32 * rb + 8 * g4 + 4 * h);
-          const float eq[4] = {e4.x, e4.y, e4.z, e4.w};
-#pragma unroll
-          for (int b = 0; b < 4; ++b) {
-            const int i = 4 * g4 + b;
-            const float p = (float)(i < 8 ? p0[i] : p1[i - 8]);
-            ds[i] = p * (dpv[rb][i] - eq[b]);
-          }
-        }
-        ops[0] = c_kfrag(ds, 0);
-        ops[1] = c_kfrag(ds, 1);
+        for (int i = 0; i < 16; ++i) c[i] = (c_row0(i) >= lo && c_row0(i) < hi) ? c[i] : 0.f;
       }
-      accumulate(pw ? Oc : Qc, rb, ops);
+      ops[0] = c_kfrag(c, 0);
+      ops[1] = c_kfrag(c, 1);
+      ((bf16x8*)px)[0] = ops[0];
+      ((bf16x8*)px)[1] = ops[1];
+    } else {
+      // P of this tile was written by the P-wave one barrier ago
+      const bf16x8 p0 = ((const bf16x8*)px)[0], p1 = ((const bf16x8*)px)[1];
+      const float* Ec = L.e[b];
+      f32x16 ds;
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        const float4 e4 = *(const float4*)(Ec + 8 * g4 + 4 * h);
+        const float eq[4] = {e4.x, e4.y, e4.z, e4.w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int i = 4 * g4 + q;
+          const float p = (float)(i < 8 ? p0[i] : p1[i - 8]);
+          ds[i] = p * (c[i] - eq[q]);
+        }
+      }
+      ops[0] = c_kfrag(ds, 0);
+      ops[1] = c_kfrag(ds, 1);
     }
+    accumulate(pw ? Oc : Qc, ops);
   };
 
-  if (ntiles > 0) issue(0, Qs[0], Os[0], Ls[0], Es[0]);
+  // iteration t: the P-wave takes tile t, the dS-wave tile t - 1; tile t + 1
+  // loads meanwhile
+  Cursor cl = {0, 0, 0};  // next tile to load
+  Cursor cc = {0, 0, 0};  // next tile this wave computes
+  if (ntiles > 0) {
+    issue(cl);
+    advance(cl);
+  }
   tile_barrier();
-  for (int t = 0; t < ntiles; ++t) {
-    const int cur = t & 1;
-    if (t + 1 < ntiles) issue(t + 1, Qs[cur ^ 1], Os[cur ^ 1], Ls[cur ^ 1], Es[cur ^ 1]);
+  for (int t = 0; t <= ntiles; ++t) {
+    if (t + 1 < ntiles) {
+      issue(cl);
+      advance(cl);
+    }
     compiler_fence();
-    compute(t, Qs[cur], Os[cur], Ls[cur], Es[cur]);
+    const int tc = pw ? t : t - 1;
+    if (tc >= 0 && tc < ntiles) {
+      const RowTile rt = tile_info(cc);
+      if (!hidden(rt)) compute(tc, rt, cc.buf);
+      advance(cc);
+    }
     tile_barrier();
   }
 
-  acc_fence();
   // ---- epilogue: acc[db][i] is dV^T or dK^T at d = 32 db + c_row0(i) + 4 h,
   // key wave_k0 + r
   if (wave_k0 + r >= kseg) return;
@@ -289,18 +332,24 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, bf
   if (kpre) {
     const size_t off = ((size_t)key * a.hkv + hk) * D + 4 * h;
     float* cache = pw ? a.gv : a.gk;
+    // every cache value is loaded before the first store, so the loads are
+    // in flight together instead of one round trip each
+    float4 cv[NDB][4];
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) cv[db][g4] = *(const float4*)(cache + off + 32 * db + 8 * g4);
     if (a.pk_mode == kPkAccumulate) {
 #pragma unroll
       for (int db = 0; db < NDB; ++db)
 #pragma unroll
         for (int g4 = 0; g4 < 4; ++g4) {
-          float4* pc = (float4*)(cache + off + 32 * db + 8 * g4);
-          float4 c = *pc;
+          float4 c = cv[db][g4];
           c.x += acc[db][4 * g4] * sc;
           c.y += acc[db][4 * g4 + 1] * sc;
           c.z += acc[db][4 * g4 + 2] * sc;
           c.w += acc[db][4 * g4 + 3] * sc;
-          *pc = c;
+          *(float4*)(cache + off + 32 * db + 8 * g4) = c;
         }
     } else {
       bf16* out = (bf16*)(pw ? a.dv_p : a.dk_p);
@@ -308,7 +357,7 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, bf
       for (int db = 0; db < NDB; ++db)
 #pragma unroll
         for (int g4 = 0; g4 < 4; ++g4) {
-          const float4 c = *(const float4*)(cache + off + 32 * db + 8 * g4);
+          const float4 c = cv[db][g4];
           const bf16x4 v = {(bf16)(acc[db][4 * g4] * sc + c.x), (bf16)(acc[db][4 * g4 + 1] * sc + c.y),
                             (bf16)(acc[db][4 * g4 + 2] * sc + c.z), (bf16)(acc[db][4 * g4 + 3] * sc + c.w)};
           *(bf16x4*)(out + off + 32 * db + 8 * g4) = v;
@@ -330,7 +379,7 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, bf
 
 // ----------------------------------------------------------------- bwd_q
 struct QBlock {
-  int tile, z, hq;
+  int tile, z, hq, split;
 };
 __device__ __forceinline__ QBlock decode_q_block(const AttnArgs& a, int bid, int ntx) {
   const int G = a.hq / a.hkv;
@@ -340,6 +389,8 @@ __device__ __forceinline__ QBlock decode_q_block(const AttnArgs& a, int bid, int
   const int gi = b % G;
   b /= G;
   QBlock qb;
+  qb.split = b % a.n_split;
+  b /= a.n_split;
   qb.tile = ntx - 1 - b % ntx;  // rows with the most keys first
   qb.z = b / ntx;
   qb.hq = hk * G + gi;
@@ -405,15 +456,19 @@ __device__ __forceinline__ void bwd_q_body(const AttnArgs& a, const int bid, bf1
   const int nkeys0 = prefix_rows ? min(a.P, last_lp + 1) : a.P;
   const int nkeys1 = prefix_rows ? 0 : last_lp + 1;
   const int nt0 = (nkeys0 + BK - 1) / BK, nt1 = (nkeys1 + BK - 1) / BK;
-  const int ntiles = nt0 + nt1;
+  // this split's share [t_begin, t_end) of the nt0 + nt1 key tiles
+  const int t_begin = (int)((long)(nt0 + nt1) * blk.split / a.n_split);
+  const int t_end = (int)((long)(nt0 + nt1) * (blk.split + 1) / a.n_split);
 
+  const bf16 *k_p = in_sgpr((const bf16*)a.k_p), *k_s = in_sgpr((const bf16*)a.k_s);
+  const bf16 *v_p = in_sgpr((const bf16*)a.v_p), *v_s = in_sgpr((const bf16*)a.v_s);
   auto issue = [&](int t, bf16* Kd, bf16* Vd) {
     const int seg = t < nt0 ? 0 : 1;
     const int k0 = (seg == 0 ? t : t - nt0) * BK;
     const int nk = min(BK, (seg == 0 ? nkeys0 : nkeys1) - k0);
     const int kbase = seg == 0 ? 0 : row_base;
-    load_tile<D>(Kd, (const bf16*)(seg == 0 ? a.k_p : a.k_s), kbase + k0, nk, a.hkv, hk, w, lane);
-    load_tile<D>(Vd, (const bf16*)(seg == 0 ? a.v_p : a.v_s), kbase + k0, nk, a.hkv, hk, w, lane);
+    load_tile<D>(Kd, pick(seg == 0, k_p, k_s), kbase + k0, nk, a.hkv, hk, w, lane);
+    load_tile<D>(Vd, pick(seg == 0, v_p, v_s), kbase + k0, nk, a.hkv, hk, w, lane);
   };
 
   auto compute = [&](int t, const bf16* Kc, const bf16* Vc) {
@@ -456,11 +511,11 @@ __device__ __forceinline__ void bwd_q_body(const AttnArgs& a, const int bid, bf1
     }
   };
 
-  if (ntiles > 0) issue(0, Ks[0], Vs[0]);
+  if (t_begin < t_end) issue(t_begin, Ks[0], Vs[0]);
   tile_barrier();
-  for (int t = 0; t < ntiles; ++t) {
-    const int cur = t & 1;
-    if (t + 1 < ntiles) issue(t + 1, Ks[cur ^ 1], Vs[cur ^ 1]);
+  for (int t = t_begin; t < t_end; ++t) {
+    const int cur = (t - t_begin) & 1;
+    if (t + 1 < t_end) issue(t + 1, Ks[cur ^ 1], Vs[cur ^ 1]);
     compiler_fence();
     compute(t, Ks[cur], Vs[cur]);
     tile_barrier();
@@ -469,20 +524,36 @@ __device__ __forceinline__ void bwd_q_body(const AttnArgs& a, const int bid, bf1
   if (!row_valid) return;
   // dq[db][i] = dQ^T[d = 32 db + c_row0(i) + 4 h][row my_lp] (unscaled)
   const size_t off = ((size_t)(row_base + my_lp) * a.hq + hq) * D + 4 * h;
+  if (a.n_split > 1) {
+    // suffix rows only: this split's partial, merged by bwd_dq_combine
+    float* part = a.part_dq + (size_t)blk.split * a.total_len * a.hq * D;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4)
+        *(float4*)(part + off + 32 * db + 8 * g4) =
+            make_float4(dq[db][4 * g4], dq[db][4 * g4 + 1], dq[db][4 * g4 + 2], dq[db][4 * g4 + 3]);
+    return;
+  }
   if (prefix_rows && a.dq_p_accumulate) {
-    // dense baseline: the prefix rows' dQ sums over the trajectories
+    // dense baseline: the prefix rows' dQ sums over the trajectories (all
+    // loads before the first store)
     float* acc = a.dq_acc_p;
+    float4 cv[NDB][4];
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) cv[db][g4] = *(const float4*)(acc + off + 32 * db + 8 * g4);
 #pragma unroll
     for (int db = 0; db < NDB; ++db)
 #pragma unroll
       for (int g4 = 0; g4 < 4; ++g4) {
-        float4* p4 = (float4*)(acc + off + 32 * db + 8 * g4);
-        float4 v = *p4;
+        float4 v = cv[db][g4];
         v.x += dq[db][4 * g4];
         v.y += dq[db][4 * g4 + 1];
         v.z += dq[db][4 * g4 + 2];
         v.w += dq[db][4 * g4 + 3];
-        *p4 = v;
+        *(float4*)(acc + off + 32 * db + 8 * g4) = v;
       }
     return;
   }
@@ -506,29 +577,56 @@ template <int D>
 __global__ __launch_bounds__(kThreads, 2) void bwd_bf16_kernel(AttnArgs a, int n_first, int n_kv,
                                                                int n_q, int kv_first) {
   constexpr int TE = Tile<D>::ELEMS;
-  __shared__ __attribute__((aligned(1024))) bf16 tiles[4][TE];
-  __shared__ __attribute__((aligned(256))) float rowv[4][kTileRows];
-  __shared__ __attribute__((aligned(1024))) bf16 pex[2 * 2 * 64 * 16];
+  // one LDS block shared by the two roles: the query-outer role's four
+  // 64-key tiles, or the key-outer role's KvLds
+  constexpr int kBytes = sizeof(KvLds<D>) > 4 * TE * 2 ? sizeof(KvLds<D>) : 4 * TE * 2;
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[kBytes];
   const int b = blockIdx.x;
   const bool first = b < n_first;
   const int bid = first ? b : b - n_first;
   // the first segment is padded to a multiple of 8 blocks: padding exits
   if (first == (kv_first != 0)) {
-    if (bid < n_kv) bwd_kv_body<D>(a, bid, tiles, tiles + 2, rowv, rowv + 2, pex);
+    if (bid < n_kv) bwd_kv_body<D>(a, bid, *(KvLds<D>*)lds);
   } else {
+    bf16(*tiles)[TE] = (bf16(*)[TE])lds;
     if (bid < n_q) bwd_q_body<D>(a, bid, tiles, tiles + 2);
   }
+}
+
+// dQ of every (suffix row, q head) = scale * the sum of the n_split partials
+// in split order.  One group of D / 4 threads per (row, head), 16-byte reads.
+template <int D>
+__global__ __launch_bounds__(256) void bwd_dq_combine_kernel(AttnArgs a) {
+  constexpr int TPR = D / 4;
+  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+  const long rh = idx / TPR;  // row * hq + head
+  const int c = (int)(idx % TPR);
+  const long nrh = (long)a.total_len * a.hq;
+  if (rh >= nrh) return;
+  float4 acc = *(const float4*)(a.part_dq + rh * D + 4 * c);
+  for (int j = 1; j < a.n_split; ++j) {
+    const float4 v = *(const float4*)(a.part_dq + ((size_t)j * nrh + rh) * D + 4 * c);
+    acc.x += v.x;
+    acc.y += v.y;
+    acc.z += v.z;
+    acc.w += v.w;
+  }
+  const bf16x4 o = {(bf16)(acc.x * a.scale), (bf16)(acc.y * a.scale), (bf16)(acc.z * a.scale),
+                    (bf16)(acc.w * a.scale)};
+  *(bf16x4*)((bf16*)a.dq_s + rh * D + 4 * c) = o;
 }
 
 hipError_t launch_bwd_bf16(const AttnArgs& a, int head_dim, int n_qz, bool deterministic,
                            hipStream_t st) {
   (void)deterministic;  // both roles are deterministic: no atomics anywhere
+  if (a.n_split > 1 && (a.prefix_rows || a.part_dq == nullptr)) return hipErrorInvalidValue;
   const long n_kv = (long)(a.n_prefix_k_tiles + a.n_seq * a.n_suffix_k_tiles) * a.hkv;
-  const long n_q = (long)(a.n_prefix_q_tiles + a.n_suffix_q_tiles) * a.hq * n_qz;
+  const long n_q = (long)(a.n_prefix_q_tiles + a.n_suffix_q_tiles) * a.hq * n_qz * a.n_split;
   if (n_kv + n_q == 0) return hipSuccess;
   // Phase C / dense prefix: the causal key tiles near the start of the prefix
-  // carry the most rows; Phase B suffix: every query tile sweeps the prefix
-  const int kv_first = a.prefix_rows ? 1 : 0;
+  // carry the most rows.  Phase B suffix: every query tile sweeps the prefix,
+  // so the query-outer role goes first unless its keys are split.
+  const int kv_first = (a.prefix_rows || a.n_split > 1) ? 1 : 0;
   const long first = kv_first ? n_kv : n_q;
   const long n_first = (first + 7) / 8 * 8;
   const long nb = n_first + (kv_first ? n_q : n_kv);
@@ -539,7 +637,27 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, int head_dim, int n_qz, bool deter
   else
     hipLaunchKernelGGL(bwd_bf16_kernel<128>, dim3((unsigned)nb), dim3(kThreads), 0, st, a, (int)n_first,
                        (int)n_kv, (int)n_q, kv_first);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.n_split <= 1) return e;
+  const long threads = (long)a.total_len * a.hq * (head_dim / 4);
+  const unsigned cb = (unsigned)((threads + 255) / 256);
+  ProfileScope pc("bwd_dq_combine", st);
+  if (head_dim == 64)
+    hipLaunchKernelGGL(bwd_dq_combine_kernel<64>, dim3(cb), dim3(256), 0, st, a);
+  else
+    hipLaunchKernelGGL(bwd_dq_combine_kernel<128>, dim3(cb), dim3(256), 0, st, a);
   return hipGetLastError();
+}
+
+int bwd_bf16_block_q() { return kQBQ; }
+
+int bwd_bf16_qsplit(int n_row_blocks, int n_key_tiles) {
+  // Only when the query-outer blocks alone cannot fill two slots per CU on
+  // 256 CUs; each split keeps at least 16 key tiles, so that a split costs
+  // about half of a key-outer block and packs into the tail of the launch.
+  if (n_row_blocks <= 0 || n_row_blocks >= 512) return 1;
+  int ns = std::min(n_key_tiles / 16, (512 + n_row_blocks - 1) / n_row_blocks);
+  return std::max(1, std::min(ns, 8));
 }
 
 }  // namespace spr

@@ -113,13 +113,15 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(AttnArgs a) {
   const int t_begin = (int)((long)(nt0 + nt1) * blk.split / a.n_split);
   const int t_end = (int)((long)(nt0 + nt1) * (blk.split + 1) / a.n_split);
 
+  const bf16 *k_p = in_sgpr((const bf16*)a.k_p), *k_s = in_sgpr((const bf16*)a.k_s);
+  const bf16 *v_p = in_sgpr((const bf16*)a.v_p), *v_s = in_sgpr((const bf16*)a.v_s);
   auto issue = [&](int t, bf16* Kd, bf16* Vd) {
     const int seg = t < nt0 ? 0 : 1;
     const int k0 = (seg == 0 ? t : t - nt0) * BK;
     const int nk = min(BK, (seg == 0 ? nkeys0 : nkeys1) - k0);
     const int kbase = seg == 0 ? 0 : row_base;
-    load_tile<D>(Kd, (const bf16*)(seg == 0 ? a.k_p : a.k_s), kbase + k0, nk, a.hkv, hk, w, lane);
-    load_tile<D>(Vd, (const bf16*)(seg == 0 ? a.v_p : a.v_s), kbase + k0, nk, a.hkv, hk, w, lane);
+    load_tile<D>(Kd, pick(seg == 0, k_p, k_s), kbase + k0, nk, a.hkv, hk, w, lane);
+    load_tile<D>(Vd, pick(seg == 0, v_p, v_s), kbase + k0, nk, a.hkv, hk, w, lane);
   };
 
   auto compute = [&](int t, const bf16* Kc, const bf16* Vc) {

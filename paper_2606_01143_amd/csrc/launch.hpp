@@ -55,6 +55,11 @@ int fwd_bf16_block_q();
 // suffix) blocks and a prefix of prefix_len keys
 int fwd_bf16_split(int n_row_blocks, int prefix_len);
 int bwd_bf16_block_k();
+// key splits of the bf16 suffix backward's query-outer role for
+// n_row_blocks (row tile, q head, suffix) blocks that each sweep
+// n_key_tiles key tiles
+int bwd_bf16_qsplit(int n_row_blocks, int n_key_tiles);
+int bwd_bf16_block_q();
 int f32_block_q();
 int f32_block_k();
 

@@ -136,6 +136,15 @@ int suffix_fwd_splits(const spr_dims* d, int32_t n_mb, int32_t max_len) {
   return fwd_bf16_split(nrb, d->prefix_len);
 }
 
+// key splits of the suffix backward's query-outer role (bf16 path only),
+// see bwd_bf16_qsplit
+int suffix_bwd_splits(const spr_dims* d, int32_t n_mb, int32_t max_len) {
+  if (d->dtype != SPR_BF16) return 1;
+  const int nrb = tiles(max_len, bwd_bf16_block_q()) * d->num_q_heads * n_mb;
+  const int nkt = tiles(d->prefix_len, bwd_bf16_block_k()) + tiles(max_len, bwd_bf16_block_k());
+  return bwd_bf16_qsplit(nrb, nkt);
+}
+
 int block_q(int dtype) { return dtype == SPR_BF16 ? fwd_bf16_block_q() : f32_block_q(); }
 int block_k(int dtype) { return dtype == SPR_BF16 ? bwd_bf16_block_k() : f32_block_k(); }
 
@@ -154,7 +163,7 @@ hipError_t launch_bwd(const spr_dims* d, const AttnArgs& a, int n_qz, hipStream_
 struct WsLayout {
   size_t dd_p = 0, dq_acc_p = 0, dd_s = 0, dq_acc_s = 0, dk_acc_p = 0, dv_acc_p = 0;
   size_t lse2_p = 0, lse2_s = 0;
-  size_t part_o = 0, part_lse = 0;
+  size_t part_o = 0, part_lse = 0, part_dq = 0;
   size_t total = 0;
 };
 
@@ -182,11 +191,14 @@ WsLayout ws_layout(int op, const spr_dims* d, int32_t n_mb, int32_t max_len, int
       }
       break;
     }
-    case SPR_OP_SUFFIX_BWD:
+    case SPR_OP_SUFFIX_BWD: {
       w.dd_s = take(hq * T * 4);
       w.lse2_s = take(hq * T * 4);
       if (f32) w.dq_acc_s = take(T * hq * hd * 4);
+      const size_t ns = suffix_bwd_splits(d, n_mb, max_len);
+      if (ns > 1) w.part_dq = take(ns * T * hq * hd * 4);
       break;
+    }
     case SPR_OP_PREFIX_BWD:
       w.dd_p = take(hq * P * 4);
       w.lse2_p = take(hq * P * 4);
@@ -433,6 +445,8 @@ spr_status spr_suffix_attn_bwd_accum(const spr_dims* dims, const void* k_p, cons
   a.gk = gk_cache; a.gv = gv_cache;
   a.dk_s = dk_s; a.dv_s = dv_s;
   a.n_suffix_q_tiles = tiles(max_len, block_q(dims->dtype));
+  a.n_split = suffix_bwd_splits(dims, n_mb, max_len);
+  if (a.n_split > 1) a.part_dq = at<float>(ws, w.part_dq);
   if ((st = hip_check(launch_bwd(dims, a, n_mb, stream), "suffix backward")) != SPR_OK) return st;
   if (f32 && (st = hip_check(launch_convert(dims->dtype, dq_acc, a.scale, nullptr, dq_s,
                                             T * hq * hd, stream), "dq convert")) != SPR_OK)

@@ -44,7 +44,6 @@ struct Tile {
   static constexpr int CH = D / 8;                 // 16-byte chunks per row
   static constexpr int ELEMS = kTileRows * D;      // bf16 elements per tile
   static constexpr int RPI = 64 / CH;              // rows per 1 KB load instruction
-  static constexpr int IPW = kTileRows / RPI / 4;  // load instructions per wave
 };
 
 template <int D>
@@ -66,18 +65,6 @@ __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane
 __device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
-
-// Accumulating product whose accumulator lives in AGPRs for the whole
-// sweep (it is only read back in the epilogue, after acc_fence()): keeps the
-// VGPRs free for the operands and the softmax.  The two wait states in front
-// cover a vector-ALU write of b (or a) just before.
-__device__ __forceinline__ void mfma32_acc(f32x16& acc, const bf16x8& a, const bf16x8& b) {
-  asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
-}
-
-// Wait states between the last mfma32_acc and any read of its accumulators
-// (the longest matrix-core write-to-read distance is 18 wait states).
-__device__ __forceinline__ void acc_fence() { asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory"); }
 
 __device__ __forceinline__ f32x16 zero16() {
   return f32x16{0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
@@ -112,22 +99,65 @@ __device__ __forceinline__ void tile_barrier() {
   __syncthreads();
 }
 
-// Rows row0 .. row0 + 63 of a token-major [rows, H, D] tensor, head hh, into
-// a swizzled LDS tile; rows at or past row0 + nvalid (nvalid >= 1) repeat row
-// row0 + nvalid - 1.  Called by all four waves (w = wave index).
-template <int D>
+// A kernel-argument pointer held in scalar registers from here on.  Without
+// it the compiler turns "c ? a.x : a.y" inside a loop into a load of the
+// selected argument slot on every iteration, each a scalar-memory round
+// trip the wave waits for.
+template <typename T>
+__device__ __forceinline__ T* in_sgpr(T* p) {
+  asm volatile("" : "+s"(p));
+  return p;
+}
+// c ? x : y on two uniform pointers, as a register select (the same folding
+// would otherwise select between the addresses the two values live at)
+template <typename T>
+__device__ __forceinline__ T* pick(bool c, T* x, T* y) {
+  asm volatile("" : "+s"(x), "+s"(y));
+  return c ? x : y;
+}
+
+// Direct-to-LDS loads: lane l's 16 (or 4) bytes at gptr land at LDS byte
+// address lds + 16 l (4 l).  They are issued through inline assembly so that
+// the compiler does not track them: it would otherwise wait for every such
+// load before any later LDS read it cannot prove disjoint from the
+// destination, including reads of the other buffer of a multi-buffered
+// tile, which defeats loading one tile ahead.  Every caller waits for its
+// own loads (vmcnt) and then for the workgroup before reading the data
+// (tile_barrier).  M0 takes the LDS address one wait state before the load.
+__device__ __forceinline__ unsigned lds_addr(const void* p) {
+  return (unsigned)(uintptr_t)(const lds_void_t*)p;
+}
+__device__ __forceinline__ void dma_lds16(const void* gptr, unsigned lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(gptr), "s"(lds)
+               : "memory", "m0");
+}
+__device__ __forceinline__ void dma_lds4(const void* gptr, unsigned lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
+               :
+               : "v"(gptr), "s"(lds)
+               : "memory", "m0");
+}
+
+// Rows row0 .. row0 + ROWS - 1 of a token-major [rows, H, D] tensor, head
+// hh, into a swizzled LDS tile; rows at or past row0 + nvalid (nvalid >= 1)
+// repeat row row0 + nvalid - 1.  Called by NW waves (w = index among them,
+// < NW), each issuing an equal share of the 1 KB load instructions.
+template <int D, int NW = 4, int ROWS = kTileRows>
 __device__ __forceinline__ void load_tile(bf16* tile, const bf16* base, int row0, int nvalid,
                                           int H, int hh, int w, int lane) {
   constexpr int CH = Tile<D>::CH, RPI = Tile<D>::RPI;
+  constexpr int IPW = ROWS / RPI / NW;
+  static_assert(IPW * RPI * NW == ROWS, "loading waves must split the tile evenly");
   const int last = row0 + nvalid - 1;
 #pragma unroll
-  for (int i = 0; i < Tile<D>::IPW; ++i) {
-    const int lrow0 = (w * Tile<D>::IPW + i) * RPI;
+  for (int i = 0; i < IPW; ++i) {
+    const int lrow0 = (w * IPW + i) * RPI;
     const int lrow = lrow0 + lane / CH;
     const int c = (lane % CH) ^ swz<D>(lrow);
     const int grow = min(row0 + lrow, last);
-    __builtin_amdgcn_global_load_lds(base + ((size_t)grow * H + hh) * D + 8 * c,
-                                     (lds_void_t*)(tile + lrow0 * D), 16, 0, 0);
+    dma_lds16(base + ((size_t)grow * H + hh) * D + 8 * c, lds_addr(tile + lrow0 * D));
   }
 }
 
@@ -136,7 +166,7 @@ __device__ __forceinline__ void load_tile(bf16* tile, const bf16* base, int row0
 __device__ __forceinline__ void load_row_vec(float* dst, const float* src, int row0, int nvalid,
                                              int stride, int lane) {
   const int row = min(row0 + lane, row0 + nvalid - 1);
-  __builtin_amdgcn_global_load_lds(src + (size_t)row * stride, (lds_void_t*)dst, 4, 0, 0);
+  dma_lds4(src + (size_t)row * stride, lds_addr(dst));
 }
 
 // Per-lane LDS offsets of the operand reads.  swz depends only on the low

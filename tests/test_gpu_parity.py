@@ -70,6 +70,10 @@ SHAPES = [
     # prefixes long enough for the suffix forward to split its key range
     ("bf16_split_ragged", GroupShape(4, 2, 128, 1100, (70, 129, 33), "bf16")),
     ("bf16_split_d64", GroupShape(4, 2, 64, 700, (65, 3), "bf16")),
+    # long enough prefixes that the suffix backward's query-outer role also
+    # splits its keys (2 and 3 ranges), with ragged suffix tails
+    ("bf16_qsplit_ragged", GroupShape(4, 2, 128, 2100, (70, 129, 33), "bf16")),
+    ("bf16_qsplit_d64", GroupShape(4, 2, 64, 3100, (65, 3), "bf16")),
 ]
 
 

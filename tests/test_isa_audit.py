@@ -1,13 +1,15 @@
-"""Static audit of the backward kernel's machine code (CPU only).
+"""Static audit of the gfx950 kernels' machine code (CPU only).
 
-The key-outer role keeps its dK/dV accumulators in AGPRs through inline-asm
-matrix instructions that the compiler cannot see into.  That is only safe if
-nothing else touches those registers while the products are in flight: no
-spill, no copy, no read between the first and the last of these
-instructions.  This test compiles the kernel source for gfx950 with the
-library's flags and checks exactly that, so a code change that makes the
-compiler spill or copy the accumulators fails here instead of producing
-wrong gradients on the GPU.
+Compiles the matrix-core kernels with the library's flags and checks what
+the performance design relies on:
+- no scratch (register spills) in any attention kernel;
+- no register-file copies between VGPRs and AGPRs inside the kernels (every
+  accumulator is a plain VGPR; a copy per tile would double the VALU work);
+- no compiler-inserted wait for the direct-to-LDS loads right before an LDS
+  read (the loads are issued through inline assembly precisely so that the
+  next tile's loads stay in flight while the current tile is read).
+If a code change makes the compiler spill, copy or serialize, this fails
+here instead of showing up only as a slowdown on the GPU.
 """
 import os
 import re
@@ -18,16 +20,17 @@ import tempfile
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-SRC = os.path.join(ROOT, "paper_2606_01143_amd", "csrc", "kernels_bf16_bwd.hip")
 
 
-def _compile_to_asm():
+
+def _compile_to_asm(name):
     from paper_2606_01143_amd.build import COMMON_FLAGS, HIPCC
     if not os.path.exists(HIPCC):
         pytest.skip("hipcc not available")
-    out = os.path.join(tempfile.mkdtemp(prefix="spr_isa_"), "bwd.s")
+    src = os.path.join(ROOT, "paper_2606_01143_amd", "csrc", name)
+    out = os.path.join(tempfile.mkdtemp(prefix="spr_isa_"), "k.s")
     flags = [f for f in COMMON_FLAGS if f != "-fPIC"]
-    r = subprocess.run([HIPCC, *flags, "--cuda-device-only", "-S", SRC, "-o", out],
+    r = subprocess.run([HIPCC, *flags, "--cuda-device-only", "-S", src, "-o", out],
                        capture_output=True, text=True)
     assert r.returncode == 0, r.stderr[-2000:]
     with open(out) as f:
@@ -36,28 +39,26 @@ def _compile_to_asm():
     return text
 
 
-def _functions(text):
+def _functions(text, pattern):
     funcs = {}
-    for m in re.finditer(r"^(_ZN3spr15bwd_bf16_kernel\w+):", text, re.M):
+    for m in re.finditer(r"^(_ZN3spr\w*" + pattern + r"\w*):", text, re.M):
         end = text.find(".Lfunc_end", m.end())
-        funcs[m.group(1)] = text[m.end():end]
+        funcs[m.group(1)] = [l.strip() for l in text[m.end():end].split("\n")
+                             if l.strip() and not l.strip().startswith(";")]
     return funcs
 
 
-AGPR = re.compile(r"\ba(\d+|\[\d+:\d+\])")
-ASM_MFMA = re.compile(r"^\s*v_mfma_\w+\s+a\[")
-
-
-def test_agpr_accumulators_are_untouched_inside_the_sweep():
-    text = _compile_to_asm()
-    funcs = _functions(text)
-    assert funcs, "backward kernel not found in the assembly"
-    for name, body in funcs.items():
-        lines = [l for l in body.split("\n") if l.strip() and not l.strip().startswith(";")]
-        idx = [i for i, l in enumerate(lines) if ASM_MFMA.match(l)]
-        assert idx, f"{name}: no AGPR-accumulating products found"
-        bad = [l.strip() for l in lines[idx[0]:idx[-1] + 1]
-               if AGPR.search(l) and not ASM_MFMA.match(l)]
-        assert not bad, f"{name}: AGPR accessed inside the sweep: {bad[:5]}"
-        spills = [l.strip() for l in lines if l.strip().startswith("scratch_")]
+@pytest.mark.parametrize("src,pattern", [("kernels_bf16_bwd.hip", "bwd_bf16_kernel"),
+                                         ("kernels_bf16_fwd.hip", "fwd_bf16_kernel")])
+def test_kernels_do_not_spill_copy_or_serialize(src, pattern):
+    funcs = _functions(_compile_to_asm(src), pattern)
+    assert funcs, f"{pattern} not found in the assembly"
+    for name, lines in funcs.items():
+        assert any(l.startswith("v_mfma") for l in lines), f"{name}: no matrix instructions"
+        spills = [l for l in lines if l.startswith("scratch_")]
         assert not spills, f"{name}: scratch spills: {spills[:5]}"
+        copies = [l for l in lines if l.startswith("v_accvgpr_")]
+        assert not copies, f"{name}: VGPR/AGPR copies: {copies[:5]}"
+        waits = [i for i, l in enumerate(lines[:-1])
+                 if l.startswith("s_waitcnt") and "vmcnt(0)" in l and lines[i + 1].startswith("ds_read")]
+        assert not waits, f"{name}: vmcnt(0) right before an LDS read at lines {waits[:5]}"

@@ -12,14 +12,23 @@ value = useful TFLOP/s = 14 d FLOP per visible (query row, key) pair per q
 head that the schedule computes (4d forward + 10d backward), divided by the
 step time.  The dense baseline's extra work is never counted.
 
-Prints ONE JSON line.  ``--gpus N`` with N > 1 exits: this build runs on one
-GPU.
+Also reported: per-phase times of one step, the standalone gK/gV cache
+accumulate (G += g, HBM-bound) against 8 TB/s, and the 12d (no S recompute)
+FLOP figure.  ``roofline.traffic`` is taken from the committed FETCH_SIZE /
+WRITE_SIZE counter summary of the dominant kernel when that summary was made
+from the kernel sources in the tree (else null).
+
+Prints ONE JSON line.  ``--sweep c3|c4|c5attn|all`` instead prints one JSON
+line per configuration of the speedup surface (schedule vs dense, no CPU
+baseline).  ``--gpus N`` with N > 1 exits: this build runs on one GPU.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -35,6 +44,15 @@ HBM_PEAK_GBS = 8000.0
 # the usual flash-attention count: the backward kernel's second S/dP pass
 # for dQ is implementation overhead and is not counted)
 KERNEL_FLOP_PER_PAIR_PER_D = {"fwd_bf16": 4, "bwd_bf16": 10}
+# committed counter summary of the dominant kernel's HBM traffic, and the
+# sources whose hash it records
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "bwd_bf16_traffic_llama3_8b_p4096_n8_s512.md")
+BWD_SOURCES = ["kernels_bf16_bwd.hip", "tile.hpp", "common.hpp"]
+SWEEPS = {
+    "c3": [f"qwen3_8b_p{p}_n{n}" for p in (2048, 8192, 16384) for n in (4, 8, 16)],
+    "c4": ["qwen3_moe_p8192_n16_ragged"],
+    "c5attn": ["llama3_8b_p28672_n8_s128"],
+}
 
 
 def log(msg):
@@ -63,6 +81,62 @@ def pair_counts(shape):
     suf = [s * p + s * (s + 1) // 2 for s in shape.suffix_lens]
     dense = [(p + s) * (p + s + 1) // 2 for s in shape.suffix_lens]
     return pre, suf, dense
+
+
+def bwd_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in BWD_SOURCES:
+        with open(os.path.join(ROOT, "paper_2606_01143_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def committed_traffic():
+    """(bytes per launch, note) from the counter summary, or (None, why)."""
+    if not os.path.exists(TRAFFIC_SUMMARY):
+        return None, "no counter summary"
+    text = open(TRAFFIC_SUMMARY).read()
+    m_hash = re.search(r"kernel source hash: `([0-9a-f]+)`", text)
+    m_val = re.search(r"HBM bytes per launch \(calibrated\): `([0-9.eE+]+)`", text)
+    if not m_hash or not m_val:
+        return None, "summary unreadable"
+    if m_hash.group(1) != bwd_source_hash():
+        return None, "kernel changed since the counters were taken"
+    return float(m_val.group(1)), os.path.relpath(TRAFFIC_SUMMARY, ROOT)
+
+
+def phase_times(grp, mbs):
+    """Per-phase milliseconds of one schedule step (events between phases)."""
+    import torch
+    marks = []
+
+    def mark(name):
+        e = torch.cuda.Event(enable_timing=True)
+        e.record()
+        marks.append((name, e))
+
+    start = torch.cuda.Event(enable_timing=True)
+    start.record()
+    grp.run_schedule(mbs, mark=mark)
+    torch.cuda.synchronize()
+    out, prev = {}, start
+    for name, e in marks:
+        out[name] = out.get(name, 0.0) + prev.elapsed_time(e)
+        prev = e
+    return {k: round(v, 4) for k, v in out.items()}
+
+
+def gkv_accumulate_rate(grp, reps: int = 20):
+    """Standalone G_K += g_K, G_V += g_V: HBM GB/s (12 bytes per element per
+    cache: read G, read g, write G)."""
+    import torch
+    from paper_2606_01143_amd import binding as B
+    dgk, dgv = torch.randn_like(grp.gk), torch.randn_like(grp.gv)
+    ms = time_steps(lambda: B.gkv_accumulate(grp.dims, grp.gk, grp.gv, dgk, dgv), reps, 2)
+    nbytes = 12 * (grp.gk.numel() + grp.gv.numel())
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    return {"GB/s": round(gbs, 1), "frac_of_8TB/s": round(gbs / HBM_PEAK_GBS, 4),
+            "bytes_per_call": nbytes, "ms_per_call": round(ms, 4)}
 
 
 def time_steps(fn, steps: int, warmup: int):
@@ -126,6 +200,7 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--sweep", choices=["c3", "c4", "c5attn", "all"], default=None)
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (--gpus {args.gpus} requested); the multi-GPU "
@@ -137,6 +212,11 @@ def main():
     from paper_2606_01143_amd.group import DeviceGroup
 
     B.lib()  # fails loudly without the HIP library
+    if args.sweep:
+        names = sum(SWEEPS.values(), []) if args.sweep == "all" else SWEEPS[args.sweep]
+        for name in names:
+            sweep_one(name, args)
+        return
     log(f"generating {args.workload} (seed {args.seed})")
     inp = workload(args.workload, args.seed)
     shape = inp["shape"]
@@ -182,6 +262,8 @@ def main():
     log(f"schedule {ms_step:.3f} ms/step, {value:.1f} TFLOP/s; {dominant} "
         f"{dom_count} launches avg {dom_avg_ms:.3f} ms -> {dom_achieved:.1f} TFLOP/s")
 
+    phases = phase_times(grp, mbs)
+    gkv = gkv_accumulate_rate(grp)
     out = {
         "metric": METRIC, "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
@@ -196,6 +278,9 @@ def main():
         "pct_mfma_peak": round(100 * value / BF16_PEAK_TFLOPS, 2),
         "schedule_tflop_per_step": round(sched_flops / 1e12, 4),
         "kernel_ms_one_step": per_kernel,
+        "phases_ms": phases,
+        "value_12d_tflops": round(value * 12 / 14, 3),
+        "gkv_accumulate": gkv,
     }
 
     if not args.no_dense:
@@ -207,9 +292,11 @@ def main():
         out["flop_ratio_dense_over_schedule"] = round(dense_flops / sched_flops, 3)
         log(f"dense {ms_dense:.3f} ms/step, speedup {ms_dense / ms_step:.2f}x")
 
+    traffic, traffic_src = committed_traffic() if dominant == "bwd_bf16" else (None, "n/a")
     out["roofline"] = {"bound": "mfma", "achieved": round(dom_achieved, 2),
                        "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                       "frac": round(dom_achieved / BF16_PEAK_TFLOPS, 4), "traffic": None,
+                       "frac": round(dom_achieved / BF16_PEAK_TFLOPS, 4), "traffic": traffic,
+                       "traffic_unit": "HBM bytes per launch", "traffic_source": traffic_src,
                        "kernel": dominant,
                        "flop_per_pair": f"{KERNEL_FLOP_PER_PAIR_PER_D[dominant]}d",
                        "launches_per_step": dom_count // max(args.steps, 1),
@@ -217,6 +304,40 @@ def main():
     log("cpu baseline (oracle)")
     out["cpu_baseline"] = cpu_baseline(inp, shape, args.cpu_seconds)
     print(json.dumps(out), flush=True)
+
+
+def sweep_one(name: str, args):
+    """One configuration of the speedup surface: schedule and dense baseline
+    timed on the same GPU, one suffix per microbatch."""
+    import torch
+    from paper_2606_01143_amd.group import DeviceGroup
+    log(f"sweep {name}: generating")
+    inp = workload(name, args.seed)
+    shape = inp["shape"]
+    mbs = [(i, i + 1) for i in range(shape.n)]
+    grp = DeviceGroup(inp, device="cuda:0", dense=True)
+    del inp
+    grp.prepare(mbs)
+    pre, suf, dense_pairs = pair_counts(shape)
+    hq, d = shape.num_q_heads, shape.head_dim
+    sched_flops = 14 * d * hq * (pre + sum(suf))
+    dense_flops = 14 * d * hq * sum(dense_pairs)
+    steps = max(1, args.steps)
+    ms = time_steps(lambda: grp.run_schedule(mbs), steps, max(1, args.warmup))
+    phases = phase_times(grp, mbs)
+    ms_dense = time_steps(lambda: grp.run_dense(), max(1, steps // 2), 1)
+    value = sched_flops / (ms * 1e-3) / 1e12
+    rec = {"workload": name, "num_q_heads": hq, "num_kv_heads": shape.num_kv_heads, "head_dim": d,
+           "prefix_len": shape.prefix_len, "n_suffixes": shape.n,
+           "total_suffix_tokens": int(sum(shape.suffix_lens)),
+           "ms_per_step": round(ms, 4), "value_tflops": round(value, 3),
+           "pct_mfma_peak": round(100 * value / BF16_PEAK_TFLOPS, 2),
+           "dense_ms_per_step": round(ms_dense, 4), "speedup_vs_dense": round(ms_dense / ms, 3),
+           "flop_ratio_dense_over_schedule": round(dense_flops / sched_flops, 3),
+           "phases_ms": phases, "steps": steps, "dtype": "bf16", "data": "synthetic"}
+    print(json.dumps(rec), flush=True)
+    del grp
+    torch.cuda.empty_cache()
 
 
 if __name__ == "__main__":

@@ -75,7 +75,7 @@ struct KvLds {
   bf16 o[kKvBufs][TE];
   float l[kKvBufs][64];  // log2-domain LSE of the tile's rows (32 used)
   float e[kKvBufs][64];  // rowsum(dO * O) of the tile's rows (32 used)
-  bf16 p[2][2][64 * 16];  // P exchange [tile parity][key block][lane][16]
+  float4 p[2][2][4][64];  // P exchange [tile parity][key block][quarter][lane]
 };
 
 template <int D>
@@ -126,6 +126,8 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
     const size_t off = ((size_t)(kbase + my_key) * a.hkv + hk) * D + 8 * h;
 #pragma unroll
     for (int s = 0; s < NS; ++s) kvf[s] = *(const bf16x8*)(g + off + 16 * s);
+#pragma unroll
+    for (int s = 0; s < NS; ++s) settle(kvf[s]);
   }
   f32x16 acc[NDB];  // dV^T (P-wave) or dK^T (dS-wave)
 #pragma unroll
@@ -152,17 +154,23 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
     int hh, row0, nr, lp_first;
     bool prefix, causal;
   };
-  // Tiles run head by head, j = 0 .. per_head - 1 within a head.  The loop
-  // keeps (head, j) cursors instead of dividing a flat index: every wave of
-  // the CU leaves a barrier at once, and their divisions would queue on the
-  // shared scalar unit.
+  // Tile order: row tiles outer, the G q heads inner.  The suffix rows of a
+  // prefix key tile (all visible) go first, in ascending order; causal row
+  // ranges go from the last row tile down to the diagonal.  The key tiles of
+  // one kv head run concurrently on one XCD and share the same 32-row grid,
+  // so in this order they read each Q/dO row tile at about the same time and
+  // it is fetched from HBM once for all of them (swept from each tile's own
+  // diagonal upward they drift apart and thrash the L2).
+  // The loop keeps (row tile, head) cursors instead of dividing a flat
+  // index: every wave of the CU leaves a barrier at once, and their
+  // divisions would queue on the shared scalar unit.
   struct Cursor {
-    int g, j, buf;  // q head of the group, tile within it, LDS buffer
+    int j, g, buf;  // row tile, q head of the group, LDS buffer
   };
   auto advance = [&](Cursor& c) {
-    if (++c.j == per_head) {
-      c.j = 0;
-      ++c.g;
+    if (++c.g == G) {
+      c.g = 0;
+      ++c.j;
     }
     c.buf = c.buf == kKvBufs - 1 ? 0 : c.buf + 1;
   };
@@ -170,22 +178,22 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
     RowTile rt;
     rt.hh = hk * G + c.g;
     const int j = c.j;
-    if (j < n_pr) {
-      rt.prefix = true;
-      rt.causal = true;
-      rt.lp_first = k0 + j * BQ;
-      rt.row0 = rt.lp_first;
-      rt.nr = min(BQ, a.P - rt.lp_first);
-    } else if (kpre) {
+    if (kpre && j < n_sr) {
       rt.prefix = false;
       rt.causal = false;
       rt.lp_first = 0;
-      rt.row0 = sr0 + (j - n_pr) * BQ;
+      rt.row0 = sr0 + j * BQ;
       rt.nr = min(BQ, sr1 - rt.row0);
+    } else if (kpre) {
+      rt.prefix = true;
+      rt.causal = true;
+      rt.lp_first = k0 + (n_pr - 1 - (j - n_sr)) * BQ;
+      rt.row0 = rt.lp_first;
+      rt.nr = min(BQ, a.P - rt.lp_first);
     } else {
       rt.prefix = false;
       rt.causal = true;
-      rt.lp_first = k0 + (j - n_pr) * BQ;
+      rt.lp_first = k0 + (n_sr - 1 - j) * BQ;
       rt.row0 = kbase + rt.lp_first;
       rt.nr = min(BQ, kseg - rt.lp_first);
     }
@@ -197,13 +205,17 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
   const bf16 *do_p = in_sgpr((const bf16*)a.do_p), *do_s = in_sgpr((const bf16*)a.do_s);
   const float *l_p = in_sgpr((const float*)a.lse2_p), *l_s = in_sgpr((const float*)a.lse2_s);
   const float *e_p = in_sgpr((const float*)a.dd_p), *e_s = in_sgpr((const float*)a.dd_s);
+  TileLoader<D, 4, BQ> tl;
+  tl.init(a.hq, w, lane);
+  RowVecLoader rl;
+  rl.init(a.hq, lane);
   auto issue = [&](const Cursor& cur) {
     const RowTile rt = tile_info(cur);
     const int b = cur.buf;
-    load_tile<D, 4, BQ>(L.q[b], pick(rt.prefix, q_p, q_s), rt.row0, rt.nr, a.hq, rt.hh, w, lane);
-    load_tile<D, 4, BQ>(L.o[b], pick(rt.prefix, do_p, do_s), rt.row0, rt.nr, a.hq, rt.hh, w, lane);
-    if (w == 0) load_row_vec(L.l[b], pick(rt.prefix, l_p, l_s) + rt.hh, rt.row0, rt.nr, a.hq, lane);
-    if (w == 1) load_row_vec(L.e[b], pick(rt.prefix, e_p, e_s) + rt.hh, rt.row0, rt.nr, a.hq, lane);
+    tl.load(L.q[b], pick(rt.prefix, q_p, q_s), rt.row0, rt.nr, a.hq, rt.hh);
+    tl.load(L.o[b], pick(rt.prefix, do_p, do_s), rt.row0, rt.nr, a.hq, rt.hh);
+    if (w == 0) rl.load(L.l[b], pick(rt.prefix, l_p, l_s) + rt.hh, rt.row0, rt.nr, a.hq);
+    if (w == 1) rl.load(L.e[b], pick(rt.prefix, e_p, e_s) + rt.hh, rt.row0, rt.nr, a.hq);
   };
 
   // A tile whose rows all precede this pair's keys (causal) contributes
@@ -254,7 +266,7 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
   auto compute = [&](int tc, const RowTile& rt, const int b) {
     const bf16* Qc = L.q[b];
     const bf16* Oc = L.o[b];
-    bf16* px = L.p[tc & 1][kb] + lane * 16;
+    float4* px = &L.p[tc & 1][kb][0][lane];  // quarter q at px[64 q]
     f32x16 c = product(pw ? Qc : Oc);
     bf16x8 ops[2];
     if (pw) {
@@ -276,23 +288,21 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
       }
       ops[0] = c_kfrag(c, 0);
       ops[1] = c_kfrag(c, 1);
-      ((bf16x8*)px)[0] = ops[0];
-      ((bf16x8*)px)[1] = ops[1];
+      // P in fp32 for the dS-wave (no unpacking on its side)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) px[64 * q] = make_float4(c[4 * q], c[4 * q + 1], c[4 * q + 2], c[4 * q + 3]);
     } else {
       // P of this tile was written by the P-wave one barrier ago
-      const bf16x8 p0 = ((const bf16x8*)px)[0], p1 = ((const bf16x8*)px)[1];
       const float* Ec = L.e[b];
       f32x16 ds;
 #pragma unroll
       for (int g4 = 0; g4 < 4; ++g4) {
         const float4 e4 = *(const float4*)(Ec + 8 * g4 + 4 * h);
-        const float eq[4] = {e4.x, e4.y, e4.z, e4.w};
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int i = 4 * g4 + q;
-          const float p = (float)(i < 8 ? p0[i] : p1[i - 8]);
-          ds[i] = p * (c[i] - eq[q]);
-        }
+        const float4 p4 = px[64 * g4];
+        ds[4 * g4 + 0] = p4.x * (c[4 * g4 + 0] - e4.x);
+        ds[4 * g4 + 1] = p4.y * (c[4 * g4 + 1] - e4.y);
+        ds[4 * g4 + 2] = p4.z * (c[4 * g4 + 2] - e4.z);
+        ds[4 * g4 + 3] = p4.w * (c[4 * g4 + 3] - e4.w);
       }
       ops[0] = c_kfrag(ds, 0);
       ops[1] = c_kfrag(ds, 1);
@@ -447,6 +457,13 @@ __device__ __forceinline__ void bwd_q_body(const AttnArgs& a, const int bid, bf1
     }
     lse2 = (prefix_rows ? a.lse2_p : a.lse2_s)[row * a.hq + hq];
     drow = (prefix_rows ? a.dd_p : a.dd_s)[row * a.hq + hq];
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      settle(qf[s]);
+      settle(df[s]);
+    }
+    settle(lse2);
+    settle(drow);
   }
   f32x16 dq[NDB];
 #pragma unroll
@@ -462,13 +479,15 @@ __device__ __forceinline__ void bwd_q_body(const AttnArgs& a, const int bid, bf1
 
   const bf16 *k_p = in_sgpr((const bf16*)a.k_p), *k_s = in_sgpr((const bf16*)a.k_s);
   const bf16 *v_p = in_sgpr((const bf16*)a.v_p), *v_s = in_sgpr((const bf16*)a.v_s);
+  TileLoader<D, 4, BK> tl;
+  tl.init(a.hkv, w, lane);
   auto issue = [&](int t, bf16* Kd, bf16* Vd) {
     const int seg = t < nt0 ? 0 : 1;
     const int k0 = (seg == 0 ? t : t - nt0) * BK;
     const int nk = min(BK, (seg == 0 ? nkeys0 : nkeys1) - k0);
     const int kbase = seg == 0 ? 0 : row_base;
-    load_tile<D>(Kd, pick(seg == 0, k_p, k_s), kbase + k0, nk, a.hkv, hk, w, lane);
-    load_tile<D>(Vd, pick(seg == 0, v_p, v_s), kbase + k0, nk, a.hkv, hk, w, lane);
+    tl.load(Kd, pick(seg == 0, k_p, k_s), kbase + k0, nk, a.hkv, hk);
+    tl.load(Vd, pick(seg == 0, v_p, v_s), kbase + k0, nk, a.hkv, hk);
   };
 
   auto compute = [&](int t, const bf16* Kc, const bf16* Vc) {

@@ -98,6 +98,8 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(AttnArgs a) {
     const size_t off = ((size_t)(row_base + my_lp) * a.hq + hq) * D + 8 * h;
 #pragma unroll
     for (int s = 0; s < NS; ++s) qf[s] = *(const bf16x8*)(qb + off + 16 * s);
+#pragma unroll
+    for (int s = 0; s < NS; ++s) settle(qf[s]);
   }
   f32x16 o[NDB];
 #pragma unroll
@@ -115,13 +117,15 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(AttnArgs a) {
 
   const bf16 *k_p = in_sgpr((const bf16*)a.k_p), *k_s = in_sgpr((const bf16*)a.k_s);
   const bf16 *v_p = in_sgpr((const bf16*)a.v_p), *v_s = in_sgpr((const bf16*)a.v_s);
+  TileLoader<D, 4, BK> tl;
+  tl.init(a.hkv, w, lane);
   auto issue = [&](int t, bf16* Kd, bf16* Vd) {
     const int seg = t < nt0 ? 0 : 1;
     const int k0 = (seg == 0 ? t : t - nt0) * BK;
     const int nk = min(BK, (seg == 0 ? nkeys0 : nkeys1) - k0);
     const int kbase = seg == 0 ? 0 : row_base;
-    load_tile<D>(Kd, pick(seg == 0, k_p, k_s), kbase + k0, nk, a.hkv, hk, w, lane);
-    load_tile<D>(Vd, pick(seg == 0, v_p, v_s), kbase + k0, nk, a.hkv, hk, w, lane);
+    tl.load(Kd, pick(seg == 0, k_p, k_s), kbase + k0, nk, a.hkv, hk);
+    tl.load(Vd, pick(seg == 0, v_p, v_s), kbase + k0, nk, a.hkv, hk);
   };
 
   auto compute = [&](int t, const bf16* Kc, const bf16* Vc) {

@@ -99,6 +99,16 @@ __device__ __forceinline__ void tile_barrier() {
   __syncthreads();
 }
 
+// Registers loaded from global memory before a tile loop pass through here
+// once the loads are issued.  The compiler then waits for those loads at
+// this point, before the loop.  Otherwise its waits stay at their first use
+// inside the loop, and since it does not count the untracked direct-to-LDS
+// loads, they would also wait, every iteration, for the next tile's loads.
+template <typename T>
+__device__ __forceinline__ void settle(T& x) {
+  asm volatile("" : "+v"(x));
+}
+
 // A kernel-argument pointer held in scalar registers from here on.  Without
 // it the compiler turns "c ? a.x : a.y" inside a loop into a load of the
 // selected argument slot on every iteration, each a scalar-memory round
@@ -139,6 +149,77 @@ __device__ __forceinline__ void dma_lds4(const void* gptr, unsigned lds) {
                : "v"(gptr), "s"(lds)
                : "memory", "m0");
 }
+// The same with a scalar base address and a 32-bit per-lane byte offset:
+// no per-lane 64-bit address arithmetic at the call site.
+__device__ __forceinline__ void dma_lds16_s(unsigned voff, const void* sbase, unsigned lds) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(voff), "s"(sbase), "s"(lds)
+               : "memory", "m0");
+}
+__device__ __forceinline__ void dma_lds4_s(unsigned voff, const void* sbase, unsigned lds) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %0, %1"
+               :
+               : "v"(voff), "s"(sbase), "s"(lds)
+               : "memory", "m0");
+}
+
+// Loads ROWS-row tiles of token-major [rows, H, D] tensors (one head) into
+// swizzled LDS tiles, this wave's share of the 1 KB instructions out of NW
+// loading waves.  The per-lane byte offsets within a tile depend only on
+// the lane, the wave and H, so they are computed once; a tile then costs a
+// scalar base address and one instruction per KB.  Rows at or past nvalid
+// (ragged end, nvalid >= 1) repeat the last valid row.
+template <int D, int NW, int ROWS>
+struct TileLoader {
+  static constexpr int CH = D / 8;      // 16-byte chunks per row
+  static constexpr int RPI = 64 / CH;   // rows per instruction
+  static constexpr int IPW = ROWS / RPI / NW;
+  static_assert(IPW * RPI * NW == ROWS, "loading waves must split the tile evenly");
+  unsigned off[IPW];
+  int lrow0, lane_row;  // first tile row of this wave's share, lane's row within an instruction
+  __device__ __forceinline__ void init(int H, int w, int lane) {
+    lrow0 = w * IPW * RPI;
+    lane_row = lane / CH;
+#pragma unroll
+    for (int i = 0; i < IPW; ++i) {
+      const int lrow = lrow0 + i * RPI + lane_row;
+      const int c = (lane % CH) ^ swz<D>(lrow);
+      off[i] = ((unsigned)lrow * H * D + 8 * c) * 2;
+    }
+  }
+  __device__ __forceinline__ void load(bf16* tile, const bf16* base, int row0, int nvalid, int H,
+                                       int hh) const {
+    const bf16* sb = base + ((size_t)row0 * H + hh) * D;
+    if (nvalid >= ROWS) {
+#pragma unroll
+      for (int i = 0; i < IPW; ++i) dma_lds16_s(off[i], sb, lds_addr(tile + (lrow0 + i * RPI) * D));
+    } else {
+#pragma unroll
+      for (int i = 0; i < IPW; ++i) {
+        const int lrow = lrow0 + i * RPI + lane_row;
+        const unsigned back = (unsigned)(lrow - min(lrow, nvalid - 1)) * H * D * 2;
+        dma_lds16_s(off[i] - back, sb, lds_addr(tile + (lrow0 + i * RPI) * D));
+      }
+    }
+  }
+};
+
+// 64 fp32 values v[(row0 + i) * stride] (i < 64; rows at or past nvalid
+// repeat the last valid one) into LDS, by one wave, offsets precomputed.
+struct RowVecLoader {
+  unsigned off;
+  int lane;
+  __device__ __forceinline__ void init(int stride, int lane_) {
+    lane = lane_;
+    off = (unsigned)lane * stride * 4;
+  }
+  __device__ __forceinline__ void load(float* dst, const float* src, int row0, int nvalid, int stride) const {
+    const float* sb = src + (size_t)row0 * stride;
+    const unsigned o = nvalid >= 64 ? off : (unsigned)min(lane, nvalid - 1) * stride * 4;
+    dma_lds4_s(o, sb, lds_addr(dst));
+  }
+};
 
 // Rows row0 .. row0 + ROWS - 1 of a token-major [rows, H, D] tensor, head
 // hh, into a swizzled LDS tile; rows at or past row0 + nvalid (nvalid >= 1)

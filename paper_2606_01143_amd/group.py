@@ -107,13 +107,20 @@ class DeviceGroup:
 
     # ------------------------------------------------------------------
     def run_schedule(self, microbatches: Optional[Sequence[Tuple[int, int]]] = None,
-                     use_gy: bool = True, stream=None) -> None:
-        """Three-phase schedule; results land in ``self.out``, ``self.gk``, ``self.gv``."""
+                     use_gy: bool = True, stream=None, mark=None) -> None:
+        """Three-phase schedule; results land in ``self.out``, ``self.gk``, ``self.gv``.
+
+        ``mark(name)``, if given, is called after each phase's launches are
+        issued ("zero", "A", "B_fwd", "B_bwd" per microbatch, "C"), e.g. to
+        record events for per-phase times."""
         dims, o = self.dims, self.out
+        mark = mark or (lambda name: None)
         mbs = list(microbatches) if microbatches is not None else self.default_microbatches()
         B.gkv_cache_zero(dims, self.gk, self.gv, stream)
+        mark("zero")
         # Phase A: prefix forward once
         B.prefix_fwd(dims, self.q_p, self.k_p, self.v_p, o["o_p"], o["lse_p"], stream)
+        mark("A")
         # Phase B: suffix microbatches read K_P/V_P and accumulate gK/gV
         for a, b in mbs:
             nmb, mx, tot = self._mb_sizes(a, b)
@@ -122,15 +129,18 @@ class DeviceGroup:
             B.suffix_attn_fwd(dims, self.k_p, self.v_p, self.q_s[r0:r1], self.k_s[r0:r1],
                               self.v_s[r0:r1], cu, nmb, mx, tot, o["o_s"][r0:r1],
                               o["lse_s"][r0:r1], self.ws, stream)
+            mark("B_fwd")
             B.suffix_attn_bwd_accum(dims, self.k_p, self.v_p, self.q_s[r0:r1], self.k_s[r0:r1],
                                     self.v_s[r0:r1], o["o_s"][r0:r1], o["lse_s"][r0:r1],
                                     self.do_s[r0:r1], cu, nmb, mx, tot, o["dq_s"][r0:r1],
                                     o["dk_s"][r0:r1], o["dv_s"][r0:r1], self.gk, self.gv,
                                     self.ws, stream)
+            mark("B_bwd")
         # Phase C: prefix backward once on the accumulated cache
         B.prefix_bwd(dims, self.q_p, self.k_p, self.v_p, o["o_p"], o["lse_p"],
                      self.g_y if use_gy else None, self.gk, self.gv, o["dq_p"], o["dk_p"],
                      o["dv_p"], self.ws, stream)
+        mark("C")
 
     def run_dense(self, use_dop: bool = True, stream=None) -> None:
         """Dense recompute baseline; results land in ``self.dense_out``."""

@@ -23,11 +23,11 @@ int aux_blocks(size_t n_vec) {
 
 }  // namespace
 
-// One wave per (row, head): each lane takes d/64 consecutive elements.
-// With cu != nullptr the rows are those of suffix `seq` only:
-// cu[seq] .. cu[seq+1]-1, and `rows` is an upper bound on their count.
-// Also converts the row's LSE to the log2 domain the backward kernels use:
-// lse2 = lse * log2(e).
+// LPR lanes per (row, head), each loading 16 consecutive bytes of dO and of
+// O, then a shuffle reduction over those lanes.  With cu != nullptr the rows
+// are those of suffix `seq` only: cu[seq] .. cu[seq+1]-1, and `rows` is an
+// upper bound on their count.  Also converts the row's LSE to the log2
+// domain the backward kernels use: lse2 = lse * log2(e).
 template <typename T, int D>
 __global__ __launch_bounds__(kAuxThreads) void row_dot_kernel(const T* __restrict__ dO,
                                                             const T* __restrict__ O, int rows,
@@ -36,27 +36,39 @@ __global__ __launch_bounds__(kAuxThreads) void row_dot_kernel(const T* __restric
                                                             float* __restrict__ dd,
                                                             const float* __restrict__ lse,
                                                             float* __restrict__ lse2) {
-  constexpr int PER = D / 64;
-  const int wave = (blockIdx.x * kAuxThreads + threadIdx.x) >> 6;
-  const int lane = threadIdx.x & 63;
+  constexpr int VEC = 16 / (int)sizeof(T);  // elements per 16-byte load
+  constexpr int LPR = D / VEC;              // lanes per (row, head): 8, 16 or 32
+  const long tid = (long)blockIdx.x * kAuxThreads + threadIdx.x;
+  const long item = tid / LPR;              // (row - row0) * hq + head
+  const int sub = (int)(tid % LPR);
   int row0 = 0, nrows = rows;
   if (cu != nullptr) {
     row0 = cu[seq];
     nrows = cu[seq + 1] - row0;
   }
-  if (wave >= nrows * hq) return;
-  const int row = row0 + wave / hq, h = wave % hq;
+  // items past the end still take part in the shuffles (a group of LPR
+  // lanes never straddles the end), but load and store nothing
+  const bool valid = item < (long)nrows * hq;
+  const size_t rh = (size_t)row0 * hq + (valid ? item : 0);
   float acc = 0.f;
-  if (dO != nullptr) {
-    const size_t off = ((size_t)row * hq + h) * D + lane * PER;
+  if (dO != nullptr && valid) {
+    const size_t off = rh * D + (size_t)sub * VEC;
+    if constexpr (sizeof(T) == 2) {
+      const bf16x8 a = *(const bf16x8*)(dO + off);
+      const bf16x8 b = *(const bf16x8*)(O + off);
 #pragma unroll
-    for (int j = 0; j < PER; ++j) acc += to_f32<T>(dO[off + j]) * to_f32<T>(O[off + j]);
+      for (int k = 0; k < 8; ++k) acc += (float)a[k] * (float)b[k];
+    } else {
+      const float4 a = *(const float4*)(dO + off);
+      const float4 b = *(const float4*)(O + off);
+      acc = a.x * b.x + a.y * b.y + a.z * b.z + a.w * b.w;
+    }
   }
 #pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) acc += __shfl_xor(acc, m);
-  if (lane == 0) {
-    dd[(size_t)row * hq + h] = acc;
-    lse2[(size_t)row * hq + h] = lse[(size_t)row * hq + h] * kLog2e;
+  for (int m = LPR / 2; m >= 1; m >>= 1) acc += __shfl_xor(acc, m);
+  if (valid && sub == 0) {
+    dd[rh] = acc;
+    lse2[rh] = lse[rh] * kLog2e;
   }
 }
 
@@ -102,8 +114,9 @@ hipError_t launch_row_dot(int dtype, const void* dO, const void* O, int rows, co
                           int seq, int hq, int head_dim, float* dd, const float* lse, float* lse2,
                           hipStream_t st) {
   if (rows <= 0) return hipSuccess;
-  const size_t waves = (size_t)rows * hq;
-  const int blocks = (int)((waves * 64 + kAuxThreads - 1) / kAuxThreads);
+  const size_t lpr = (size_t)head_dim * (dtype == 0 ? 4 : 2) / 16;  // lanes per (row, head)
+  const size_t threads = (size_t)rows * hq * lpr;
+  const int blocks = (int)((threads + kAuxThreads - 1) / kAuxThreads);
   ProfileScope ps("row_dot", st);
   if (dtype == 0) {
     if (head_dim == 64)

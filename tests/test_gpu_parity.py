@@ -198,3 +198,26 @@ def test_llama3_8b_full_size_on_one_kv_group(gpu, kv):
     sel.update({k: got[k][:, qh] for k in ("lse_p", "lse_s")})
     sel.update({k: got[k][:, kv:kv + 1] for k in kv_keys})
     _assert_close(sel, ref, SCHED_KEYS, TOL["bf16"], f"llama3 full kv={kv}")
+
+
+def test_qwen3_moe_ragged_full_size_on_one_kv_group(gpu):
+    """Qwen3-MoE attention at full size (GQA 32/4, so G = 8; d=128; P=8192;
+    16 ragged suffixes of 128..2048 tokens, packed without padding), one
+    suffix per microbatch, checked against the oracle on one kv head and its
+    8 q heads."""
+    from synthetic import NAMED_SHAPES
+    kv = 3
+    _announce(f"full-size qwen3-moe ragged kv={kv}")
+    inp = make_group(NAMED_SHAPES["qwen3_moe_p8192_n16_ragged"], seed=0, ragged=(128, 2048))
+    from paper_2606_01143_amd.group import DeviceGroup
+    grp = DeviceGroup(inp, dense=False)
+    grp.run_schedule()
+    got = grp.fetch("schedule")
+    sub, qh = _head_subset(inp, kv)
+    ref = three_phase_reference(sub)
+    q_keys = ["o_p", "o_s", "dq_p", "dq_s"]
+    kv_keys = ["dk_p", "dv_p", "dk_s", "dv_s", "g_k", "g_v"]
+    sel = {k: got[k][:, qh] for k in q_keys}
+    sel.update({k: got[k][:, qh] for k in ("lse_p", "lse_s")})
+    sel.update({k: got[k][:, kv:kv + 1] for k in kv_keys})
+    _assert_close(sel, ref, SCHED_KEYS, TOL["bf16"], f"qwen3-moe full kv={kv}")

@@ -273,36 +273,11 @@ struct FragOffsets {
   }
 };
 
-// The same offsets with half the registers.  The swizzle makes them XOR
-// images of each other: row[k + NS/2] = row[k] ^ (8 NS) and
-// trhi[db] = trlo[db] ^ (8 D + 16) for both head dims, so only row[k < NS/2]
-// and trlo are kept and the rest costs one XOR at the read.  For kernels
-// where eight VGPRs decide the occupancy.
-template <int D>
-struct FragOffsetsHalf {
-  int row[D / 32];
-  int trlo[D / 32];
-  __device__ __forceinline__ void init(int lane) {
-    FragOffsets<D> f;
-    f.init(lane);
-#pragma unroll
-    for (int k = 0; k < D / 32; ++k) row[k] = f.row[k];
-#pragma unroll
-    for (int db = 0; db < D / 32; ++db) trlo[db] = f.trlo[db];
-  }
-  __device__ __forceinline__ int row_at(int k) const { return k < D / 32 ? row[k] : row[k - D / 32] ^ (D / 2); }
-  __device__ __forceinline__ int trhi_at(int db) const { return trlo[db] ^ (8 * D + 16); }
-};
-
 // natural-k operand: tile row row0 + r (row0 a multiple of 16), columns
 // 16 k + 8 h .. + 7
 template <int D>
 __device__ __forceinline__ bf16x8 row_frag(const bf16* tile, const FragOffsets<D>& fo, int row0, int k) {
   return *(const bf16x8*)(tile + row0 * D + fo.row[k]);
-}
-template <int D>
-__device__ __forceinline__ bf16x8 row_frag(const bf16* tile, const FragOffsetsHalf<D>& fo, int row0, int k) {
-  return *(const bf16x8*)(tile + row0 * D + fo.row_at(k));
 }
 
 // C-order operand read transposed from a row-major tile: slot (h, j) of lane
@@ -311,12 +286,6 @@ template <int D>
 __device__ __forceinline__ bf16x8 tr_frag(const bf16* tile, const FragOffsets<D>& fo, int base, int db) {
   const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(tile + base * D + fo.trlo[db]));
   const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(tile + base * D + fo.trhi[db]));
-  return bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-}
-template <int D>
-__device__ __forceinline__ bf16x8 tr_frag(const bf16* tile, const FragOffsetsHalf<D>& fo, int base, int db) {
-  const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(tile + base * D + fo.trlo[db]));
-  const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(tile + base * D + fo.trhi_at(db)));
   return bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
 }
 

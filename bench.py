@@ -4,7 +4,9 @@ One step = the whole three-phase schedule over one prompt group with inputs
 already resident in HBM: zero the gK/gV cache, Phase A prefix forward, Phase
 B suffix forward + backward-with-cache-accumulation for every suffix
 microbatch (one suffix per microbatch, the paper's timing choice), Phase C
-prefix backward.  The dense-recompute baseline (full causal fwd+bwd over
+prefix backward.  Phase A and the suffix forwards run on side streams
+beside the in-order backwards (``DeviceGroup.run_schedule``); the per-phase
+times come from one extra step in serial order.  The dense-recompute baseline (full causal fwd+bwd over
 every [P||S(i)], one sequence at a time) is timed the same way on the same
 GPU for the speedup.
 
@@ -106,7 +108,8 @@ def committed_traffic():
 
 
 def phase_times(grp, mbs):
-    """Per-phase milliseconds of one schedule step (events between phases)."""
+    """Per-phase milliseconds of one schedule step in serial order (events
+    between phases; a mark implies the serial order)."""
     import torch
     marks = []
 

@@ -9,6 +9,15 @@ zero the gK/gV cache, Phase A ``prefix_fwd`` once, Phase B
 microbatch is a contiguous run of the packed suffixes; packed layout of
 Sec. 4.2), Phase C ``prefix_bwd`` once.  ``run_dense`` is the comparison:
 ``dense_recompute_baseline`` over every [P||S(i)].
+
+Streams: Phase A and the Phase B suffix forwards read only inputs, so by
+default they run on two side streams while the backward launches run in
+order on the caller's stream.  A suffix backward waits for its own
+forward, Phase C waits for Phase A and for every suffix backward (their
+gK/gV cache updates stay in microbatch order), and the caller's stream
+waits for all of it.  The work items are the same launches with the same
+arguments, so the results are identical to the serial order; the overlap
+only fills the idle compute units at the tail of each launch.
 """
 from __future__ import annotations
 
@@ -83,6 +92,14 @@ class DeviceGroup:
             need = max(need, B.workspace_size(B.OP_DENSE_BASELINE, self.dims, shp.n,
                                               max(self.lens), t))
         self.ws = torch.empty(max(need, 256), device=self.device, dtype=torch.uint8)
+        # the suffix forwards' own workspace: they run beside the backwards
+        need_f = 256
+        for mbs in splits:
+            for a, b in mbs:
+                nmb, mx, tot = self._mb_sizes(a, b)
+                need_f = max(need_f, B.workspace_size(B.OP_SUFFIX_FWD, self.dims, nmb, mx, tot))
+        self.ws_fwd = torch.empty(need_f, device=self.device, dtype=torch.uint8)
+        self._side = None  # (Phase A stream, suffix forward stream), made on first use
 
     # ------------------------------------------------------------------
     def default_microbatches(self) -> List[Tuple[int, int]]:
@@ -107,15 +124,21 @@ class DeviceGroup:
 
     # ------------------------------------------------------------------
     def run_schedule(self, microbatches: Optional[Sequence[Tuple[int, int]]] = None,
-                     use_gy: bool = True, stream=None, mark=None) -> None:
+                     use_gy: bool = True, stream=None, mark=None, overlap: bool = True) -> None:
         """Three-phase schedule; results land in ``self.out``, ``self.gk``, ``self.gv``.
 
-        ``mark(name)``, if given, is called after each phase's launches are
-        issued ("zero", "A", "B_fwd", "B_bwd" per microbatch, "C"), e.g. to
-        record events for per-phase times."""
+        ``overlap`` runs Phase A and the suffix forwards on side streams (see
+        the module docstring); ``overlap=False`` issues every launch in
+        order on ``stream``.  ``mark(name)``, if given, is called after each
+        phase's launches are issued ("zero", "A", "B_fwd", "B_bwd" per
+        microbatch, "C"), e.g. to record events for per-phase times; it
+        implies the serial order."""
+        mbs = list(microbatches) if microbatches is not None else self.default_microbatches()
+        if overlap and mark is None:
+            self._run_overlapped(mbs, use_gy, stream)
+            return
         dims, o = self.dims, self.out
         mark = mark or (lambda name: None)
-        mbs = list(microbatches) if microbatches is not None else self.default_microbatches()
         B.gkv_cache_zero(dims, self.gk, self.gv, stream)
         mark("zero")
         # Phase A: prefix forward once
@@ -123,24 +146,69 @@ class DeviceGroup:
         mark("A")
         # Phase B: suffix microbatches read K_P/V_P and accumulate gK/gV
         for a, b in mbs:
-            nmb, mx, tot = self._mb_sizes(a, b)
-            r0, r1 = self.cu_host[a], self.cu_host[b]
-            cu = self._mb_cu(a, b)
-            B.suffix_attn_fwd(dims, self.k_p, self.v_p, self.q_s[r0:r1], self.k_s[r0:r1],
-                              self.v_s[r0:r1], cu, nmb, mx, tot, o["o_s"][r0:r1],
-                              o["lse_s"][r0:r1], self.ws, stream)
+            self._suffix_fwd(a, b, self.ws, stream)
             mark("B_fwd")
-            B.suffix_attn_bwd_accum(dims, self.k_p, self.v_p, self.q_s[r0:r1], self.k_s[r0:r1],
-                                    self.v_s[r0:r1], o["o_s"][r0:r1], o["lse_s"][r0:r1],
-                                    self.do_s[r0:r1], cu, nmb, mx, tot, o["dq_s"][r0:r1],
-                                    o["dk_s"][r0:r1], o["dv_s"][r0:r1], self.gk, self.gv,
-                                    self.ws, stream)
+            self._suffix_bwd(a, b, stream)
             mark("B_bwd")
         # Phase C: prefix backward once on the accumulated cache
-        B.prefix_bwd(dims, self.q_p, self.k_p, self.v_p, o["o_p"], o["lse_p"],
+        self._prefix_bwd(use_gy, stream)
+        mark("C")
+
+    def _suffix_fwd(self, a: int, b: int, ws, stream) -> None:
+        nmb, mx, tot = self._mb_sizes(a, b)
+        r0, r1 = self.cu_host[a], self.cu_host[b]
+        o = self.out
+        B.suffix_attn_fwd(self.dims, self.k_p, self.v_p, self.q_s[r0:r1], self.k_s[r0:r1],
+                          self.v_s[r0:r1], self._mb_cu(a, b), nmb, mx, tot, o["o_s"][r0:r1],
+                          o["lse_s"][r0:r1], ws, stream)
+
+    def _suffix_bwd(self, a: int, b: int, stream) -> None:
+        nmb, mx, tot = self._mb_sizes(a, b)
+        r0, r1 = self.cu_host[a], self.cu_host[b]
+        o = self.out
+        B.suffix_attn_bwd_accum(self.dims, self.k_p, self.v_p, self.q_s[r0:r1], self.k_s[r0:r1],
+                                self.v_s[r0:r1], o["o_s"][r0:r1], o["lse_s"][r0:r1],
+                                self.do_s[r0:r1], self._mb_cu(a, b), nmb, mx, tot,
+                                o["dq_s"][r0:r1], o["dk_s"][r0:r1], o["dv_s"][r0:r1], self.gk,
+                                self.gv, self.ws, stream)
+
+    def _prefix_bwd(self, use_gy: bool, stream) -> None:
+        o = self.out
+        B.prefix_bwd(self.dims, self.q_p, self.k_p, self.v_p, o["o_p"], o["lse_p"],
                      self.g_y if use_gy else None, self.gk, self.gv, o["dq_p"], o["dk_p"],
                      o["dv_p"], self.ws, stream)
-        mark("C")
+
+    def _run_overlapped(self, mbs, use_gy: bool, stream) -> None:
+        main = stream if stream is not None else torch.cuda.current_stream(self.device)
+        if self._side is None:
+            # default priority: the side streams only fill idle compute units
+            self._side = (torch.cuda.Stream(self.device), torch.cuda.Stream(self.device))
+        s_a, s_f = self._side
+        with torch.cuda.stream(main):
+            self.prepare(mbs)  # any cu_seqlens upload is ordered before `start`
+        start = torch.cuda.Event()
+        start.record(main)
+        B.gkv_cache_zero(self.dims, self.gk, self.gv, main)
+        # Phase A on its own stream: only Phase C reads its outputs
+        s_a.wait_event(start)
+        o = self.out
+        B.prefix_fwd(self.dims, self.q_p, self.k_p, self.v_p, o["o_p"], o["lse_p"], s_a)
+        done_a = torch.cuda.Event()
+        done_a.record(s_a)
+        # suffix forwards in order on a second stream, one event each
+        s_f.wait_event(start)
+        fwd_done = []
+        for a, b in mbs:
+            self._suffix_fwd(a, b, self.ws_fwd, s_f)
+            e = torch.cuda.Event()
+            e.record(s_f)
+            fwd_done.append(e)
+        # backwards in microbatch order on the caller's stream
+        for (a, b), e in zip(mbs, fwd_done):
+            main.wait_event(e)
+            self._suffix_bwd(a, b, main)
+        main.wait_event(done_a)
+        self._prefix_bwd(use_gy, main)
 
     def run_dense(self, use_dop: bool = True, stream=None) -> None:
         """Dense recompute baseline; results land in ``self.dense_out``."""

@@ -127,6 +127,26 @@ def test_cache_is_bitwise_reproducible(gpu):
         assert torch.equal(grp.out["dk_s"], dk1) and torch.equal(grp.out["dv_s"], dv1)
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_overlapped_streams_match_serial_order_bitwise(gpu, dtype):
+    """Phase A and the suffix forwards on side streams give exactly the
+    serial order's outputs and cache, on repeated steps."""
+    import torch
+    shape = GroupShape(8, 2, 128, 1100, (200, 64, 129, 96), dtype)
+    _announce(f"stream overlap {shape}")
+    inp, grp = _group(shape, seed=6, dense=False)
+    grp.run_schedule(overlap=False)
+    ref = {k: v.clone() for k, v in grp.out.items()}
+    gk, gv = grp.gk.clone(), grp.gv.clone()
+    for _ in range(3):
+        for v in grp.out.values():
+            v.fill_(7)
+        grp.run_schedule(overlap=True)
+        for k in ref:
+            assert torch.equal(grp.out[k], ref[k]), k
+        assert torch.equal(grp.gk, gk) and torch.equal(grp.gv, gv)
+
+
 def test_microbatch_split_and_order_invariance(gpu):
     """Any split of the suffixes into packed microbatches, in any order, gives
     the same group gradients (paper Sec. 4.2; Prop. 1)."""

@@ -176,6 +176,28 @@ spr_status spr_prefix_bwd(const spr_dims* dims, const void* q_p, const void* k_p
                           hipStream_t stream);
 
 /*
+ * Phase C in two independent halves (same equations as spr_prefix_bwd).
+ * The prefix rows' dQ_1 = dS_11 K_1/sqrt(d) involves only prefix attention
+ * (App. A.3): it reads no cache and no Phase B output, so it may run as
+ * soon as spr_prefix_fwd is done, e.g. on another stream while Phase B
+ * runs.  spr_prefix_bwd_dkv computes dK_1 and dV_1 with the injected cache
+ * and must be ordered after every spr_suffix_attn_bwd_accum into that cache.
+ * Arguments mean what they mean in spr_prefix_bwd; each half takes a
+ * workspace of spr_workspace_size(SPR_OP_PREFIX_BWD) bytes, and two calls
+ * that may run concurrently need separate workspaces.  Together the two
+ * calls give exactly spr_prefix_bwd's outputs.
+ */
+spr_status spr_prefix_bwd_dq(const spr_dims* dims, const void* q_p, const void* k_p,
+                             const void* v_p, const void* o_p, const float* lse_p,
+                             const void* do_p, void* dq_p, void* ws, size_t ws_bytes,
+                             hipStream_t stream);
+spr_status spr_prefix_bwd_dkv(const spr_dims* dims, const void* q_p, const void* k_p,
+                              const void* v_p, const void* o_p, const float* lse_p,
+                              const void* do_p, const float* gk_cache, const float* gv_cache,
+                              void* dk_p, void* dv_p, void* ws, size_t ws_bytes,
+                              hipStream_t stream);
+
+/*
  * Dense recompute baseline (paper Sec. 2.1 and Sec. 3.2 cost model
  * T_base = N C_full): for i = 0..n-1, full causal forward and backward over
  * the sequence [P||S(i)], one sequence at a time, with upstream adjoint

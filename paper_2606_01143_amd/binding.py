@@ -38,6 +38,8 @@ _SIGNATURES = {
     "spr_suffix_attn_bwd_accum": ([_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, c_int32, c_int32, c_int32,
                                    _P, _P, _P, _P, _P, _P, c_size_t, _P], c_int32),
     "spr_prefix_bwd": ([_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, c_size_t, _P], c_int32),
+    "spr_prefix_bwd_dq": ([_P, _P, _P, _P, _P, _P, _P, _P, _P, c_size_t, _P], c_int32),
+    "spr_prefix_bwd_dkv": ([_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, c_size_t, _P], c_int32),
     "spr_dense_recompute_baseline": ([_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, c_int32, c_int32,
                                       c_int32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
                                       c_size_t, _P], c_int32),
@@ -157,6 +159,20 @@ def prefix_bwd(dims, q_p, k_p, v_p, o_p, lse_p, do_p, gk_cache, gv_cache, dq_p, 
                                 _ptr(lse_p), _ptr(do_p), _ptr(gk_cache), _ptr(gv_cache),
                                 _ptr(dq_p), _ptr(dk_p), _ptr(dv_p), _ptr(ws), _nbytes(ws),
                                 _stream(stream)))
+
+
+def prefix_bwd_dq(dims, q_p, k_p, v_p, o_p, lse_p, do_p, dq_p, ws=None, stream=None):
+    _check(lib().spr_prefix_bwd_dq(byref(dims), _ptr(q_p), _ptr(k_p), _ptr(v_p), _ptr(o_p),
+                                   _ptr(lse_p), _ptr(do_p), _ptr(dq_p), _ptr(ws), _nbytes(ws),
+                                   _stream(stream)))
+
+
+def prefix_bwd_dkv(dims, q_p, k_p, v_p, o_p, lse_p, do_p, gk_cache, gv_cache, dk_p, dv_p,
+                   ws=None, stream=None):
+    _check(lib().spr_prefix_bwd_dkv(byref(dims), _ptr(q_p), _ptr(k_p), _ptr(v_p), _ptr(o_p),
+                                    _ptr(lse_p), _ptr(do_p), _ptr(gk_cache), _ptr(gv_cache),
+                                    _ptr(dk_p), _ptr(dv_p), _ptr(ws), _nbytes(ws),
+                                    _stream(stream)))
 
 
 def dense_recompute_baseline(dims, q_p, k_p, v_p, do_p_seq, q_s, k_s, v_s, do_s, cu_seqlens, n,

@@ -454,12 +454,19 @@ spr_status spr_suffix_attn_bwd_accum(const spr_dims* dims, const void* k_p, cons
   return ok();
 }
 
-spr_status spr_prefix_bwd(const spr_dims* dims, const void* q_p, const void* k_p, const void* v_p,
-                          const void* o_p, const float* lse_p, const void* do_p,
-                          const float* gk_cache, const float* gv_cache, void* dq_p, void* dk_p,
-                          void* dv_p, void* ws, size_t ws_bytes, hipStream_t stream) {
+namespace {
+constexpr int kPartDq = 1, kPartDkv = 2;
+
+// Phase C (paper App. A.3-A.5); `parts` selects the prefix rows' dQ, the
+// prefix keys' dK/dV with the injected cache, or both in one launch.
+spr_status prefix_bwd_parts(const spr_dims* dims, const void* q_p, const void* k_p,
+                            const void* v_p, const void* o_p, const float* lse_p,
+                            const void* do_p, const float* gk_cache, const float* gv_cache,
+                            void* dq_p, void* dk_p, void* dv_p, void* ws, size_t ws_bytes,
+                            hipStream_t stream, int parts) {
   spr_status st = check_dims(dims);
   if (st != SPR_OK) return st;
+  const bool want_dq = parts & kPartDq, want_dkv = parts & kPartDkv;
   const size_t P = dims->prefix_len, hq = dims->num_q_heads, hkv = dims->num_kv_heads,
                hd = dims->head_dim, eb = dtype_bytes(dims->dtype);
   std::vector<Buf> bufs = {{q_p, P * hq * hd * eb, "q_p", true},
@@ -468,27 +475,30 @@ spr_status spr_prefix_bwd(const spr_dims* dims, const void* q_p, const void* k_p
                            {o_p, P * hq * hd * eb, "o_p", true},
                            {lse_p, hq * P * 4, "lse_p", true, 4},
                            {do_p, P * hq * hd * eb, "do_p", false},
-                           {gk_cache, P * hkv * hd * 4, "gk_cache", true},
-                           {gv_cache, P * hkv * hd * 4, "gv_cache", true},
-                           {dq_p, P * hq * hd * eb, "dq_p", true},
-                           {dk_p, P * hkv * hd * eb, "dk_p", true},
-                           {dv_p, P * hkv * hd * eb, "dv_p", true}};
+                           {gk_cache, P * hkv * hd * 4, "gk_cache", want_dkv},
+                           {gv_cache, P * hkv * hd * 4, "gv_cache", want_dkv},
+                           {dq_p, P * hq * hd * eb, "dq_p", want_dq},
+                           {dk_p, P * hkv * hd * eb, "dk_p", want_dkv},
+                           {dv_p, P * hkv * hd * eb, "dv_p", want_dkv}};
   if ((st = check_bufs(bufs)) != SPR_OK) return st;
   const WsLayout w = ws_layout(SPR_OP_PREFIX_BWD, dims, 0, 0, 0);
   if (do_p != nullptr && (st = check_ws(w, ws, ws_bytes)) != SPR_OK) return st;
   std::vector<Buf> all = bufs;
   if (do_p != nullptr) all.push_back({ws, w.total, "ws", false});
-  if ((st = check_aliasing({bufs[6], bufs[7]}, all)) != SPR_OK) return st;
+  if (want_dkv && (st = check_aliasing({bufs[6], bufs[7]}, all)) != SPR_OK) return st;
   if (P == 0) return ok();
   const float scale = eff_scale(dims);
   if (do_p == nullptr) {
     // G_Y = 0: dQ_P = 0, dK_P = G_K, dV_P = G_V (paper App. A.5)
-    if ((st = hip_check(launch_fill_zero((float*)dq_p, P * hq * hd * eb / 4, stream), "dq zero")) != SPR_OK)
+    if (want_dq &&
+        (st = hip_check(launch_fill_zero((float*)dq_p, P * hq * hd * eb / 4, stream), "dq zero")) != SPR_OK)
       return st;
-    if ((st = hip_check(launch_convert(dims->dtype, gk_cache, 1.f, nullptr, dk_p, P * hkv * hd, stream),
+    if (want_dkv &&
+        (st = hip_check(launch_convert(dims->dtype, gk_cache, 1.f, nullptr, dk_p, P * hkv * hd, stream),
                         "dk convert")) != SPR_OK)
       return st;
-    if ((st = hip_check(launch_convert(dims->dtype, gv_cache, 1.f, nullptr, dv_p, P * hkv * hd, stream),
+    if (want_dkv &&
+        (st = hip_check(launch_convert(dims->dtype, gv_cache, 1.f, nullptr, dv_p, P * hkv * hd, stream),
                         "dv convert")) != SPR_OK)
       return st;
     return ok();
@@ -496,29 +506,60 @@ spr_status spr_prefix_bwd(const spr_dims* dims, const void* q_p, const void* k_p
   const bool f32 = dims->dtype == SPR_F32;
   float* dd_p = at<float>(ws, w.dd_p);
   float* lse2_p = at<float>(ws, w.lse2_p);
-  float* dq_acc = f32 ? at<float>(ws, w.dq_acc_p) : nullptr;
+  float* dq_acc = f32 && want_dq ? at<float>(ws, w.dq_acc_p) : nullptr;
   if ((st = hip_check(launch_row_dot(dims->dtype, do_p, o_p, (int)P, nullptr, 0, (int)hq, (int)hd,
                                      dd_p, lse_p, lse2_p, stream), "row statistic")) != SPR_OK)
     return st;
-  if (f32 && (st = hip_check(launch_fill_zero(dq_acc, P * hq * hd, stream), "dq clear")) != SPR_OK)
+  if (dq_acc && (st = hip_check(launch_fill_zero(dq_acc, P * hq * hd, stream), "dq clear")) != SPR_OK)
     return st;
   AttnArgs a = base_args(dims);
-  a.dq_p = dq_p;
   a.q_p = q_p; a.k_p = k_p; a.v_p = v_p; a.do_p = do_p;
   a.lse_p = const_cast<float*>(lse_p);
-  a.dd_p = dd_p; a.lse2_p = lse2_p; a.dq_acc_p = dq_acc;
-  a.n_prefix_k_tiles = tiles(dims->prefix_len, block_k(dims->dtype));
+  a.dd_p = dd_p; a.lse2_p = lse2_p;
   a.prefix_rows = 1;
   a.suffix_rows = 0;
-  a.pk_mode = kPkInject;
-  a.gk = const_cast<float*>(gk_cache); a.gv = const_cast<float*>(gv_cache);
-  a.dk_p = dk_p; a.dv_p = dv_p;
-  a.n_prefix_q_tiles = tiles(dims->prefix_len, block_q(dims->dtype));
+  if (want_dq) {
+    a.dq_p = dq_p;
+    a.dq_acc_p = dq_acc;
+    a.n_prefix_q_tiles = tiles(dims->prefix_len, block_q(dims->dtype));
+  }
+  if (want_dkv) {
+    a.pk_mode = kPkInject;
+    a.gk = const_cast<float*>(gk_cache); a.gv = const_cast<float*>(gv_cache);
+    a.dk_p = dk_p; a.dv_p = dv_p;
+    a.n_prefix_k_tiles = tiles(dims->prefix_len, block_k(dims->dtype));
+  }
   if ((st = hip_check(launch_bwd(dims, a, 1, stream), "prefix backward")) != SPR_OK) return st;
-  if (f32 && (st = hip_check(launch_convert(dims->dtype, dq_acc, scale, nullptr, dq_p, P * hq * hd,
-                                            stream), "dq convert")) != SPR_OK)
+  if (dq_acc && (st = hip_check(launch_convert(dims->dtype, dq_acc, scale, nullptr, dq_p, P * hq * hd,
+                                               stream), "dq convert")) != SPR_OK)
     return st;
   return ok();
+}
+}  // namespace
+
+spr_status spr_prefix_bwd(const spr_dims* dims, const void* q_p, const void* k_p, const void* v_p,
+                          const void* o_p, const float* lse_p, const void* do_p,
+                          const float* gk_cache, const float* gv_cache, void* dq_p, void* dk_p,
+                          void* dv_p, void* ws, size_t ws_bytes, hipStream_t stream) {
+  return prefix_bwd_parts(dims, q_p, k_p, v_p, o_p, lse_p, do_p, gk_cache, gv_cache, dq_p, dk_p,
+                          dv_p, ws, ws_bytes, stream, kPartDq | kPartDkv);
+}
+
+spr_status spr_prefix_bwd_dq(const spr_dims* dims, const void* q_p, const void* k_p,
+                             const void* v_p, const void* o_p, const float* lse_p,
+                             const void* do_p, void* dq_p, void* ws, size_t ws_bytes,
+                             hipStream_t stream) {
+  return prefix_bwd_parts(dims, q_p, k_p, v_p, o_p, lse_p, do_p, nullptr, nullptr, dq_p, nullptr,
+                          nullptr, ws, ws_bytes, stream, kPartDq);
+}
+
+spr_status spr_prefix_bwd_dkv(const spr_dims* dims, const void* q_p, const void* k_p,
+                              const void* v_p, const void* o_p, const float* lse_p,
+                              const void* do_p, const float* gk_cache, const float* gv_cache,
+                              void* dk_p, void* dv_p, void* ws, size_t ws_bytes,
+                              hipStream_t stream) {
+  return prefix_bwd_parts(dims, q_p, k_p, v_p, o_p, lse_p, do_p, gk_cache, gv_cache, nullptr, dk_p,
+                          dv_p, ws, ws_bytes, stream, kPartDkv);
 }
 
 spr_status spr_dense_recompute_baseline(

@@ -130,21 +130,49 @@ def test_cache_is_bitwise_reproducible(gpu):
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_overlapped_streams_match_serial_order_bitwise(gpu, dtype):
     """Phase A and the suffix forwards on side streams give exactly the
-    serial order's outputs and cache, on repeated steps."""
+    serial order's outputs and cache, on repeated steps, with and without a
+    prefix-row adjoint."""
     import torch
     shape = GroupShape(8, 2, 128, 1100, (200, 64, 129, 96), dtype)
     _announce(f"stream overlap {shape}")
     inp, grp = _group(shape, seed=6, dense=False)
+    for use_gy in (True, False):
+        grp.run_schedule(overlap=False, use_gy=use_gy)
+        ref = {k: v.clone() for k, v in grp.out.items()}
+        gk, gv = grp.gk.clone(), grp.gv.clone()
+        for _ in range(3):
+            for v in grp.out.values():
+                v.fill_(7)
+            grp.run_schedule(overlap=True, use_gy=use_gy)
+            for k in ref:
+                assert torch.equal(grp.out[k], ref[k]), (use_gy, k)
+            assert torch.equal(grp.gk, gk) and torch.equal(grp.gv, gv)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_split_prefix_backward_equals_whole(gpu, dtype):
+    """spr_prefix_bwd_dq + spr_prefix_bwd_dkv give exactly spr_prefix_bwd's
+    outputs (the dQ half reads no cache), with and without G_Y."""
+    import torch
+    from paper_2606_01143_amd import binding as B
+    shape = GroupShape(8, 2, 128, 700, (64, 33), dtype)
+    _announce(f"split prefix backward {shape}")
+    inp, grp = _group(shape, seed=7, dense=False)
     grp.run_schedule(overlap=False)
-    ref = {k: v.clone() for k, v in grp.out.items()}
-    gk, gv = grp.gk.clone(), grp.gv.clone()
-    for _ in range(3):
-        for v in grp.out.values():
-            v.fill_(7)
-        grp.run_schedule(overlap=True)
-        for k in ref:
-            assert torch.equal(grp.out[k], ref[k]), k
-        assert torch.equal(grp.gk, gk) and torch.equal(grp.gv, gv)
+    o, d = grp.out, grp.dims
+    ws2 = torch.empty_like(grp.ws)
+    for use_gy in (True, False):
+        g_y = grp.g_y if use_gy else None
+        B.prefix_bwd(d, grp.q_p, grp.k_p, grp.v_p, o["o_p"], o["lse_p"], g_y, grp.gk, grp.gv,
+                     o["dq_p"], o["dk_p"], o["dv_p"], grp.ws)
+        ref = {k: o[k].clone() for k in ("dq_p", "dk_p", "dv_p")}
+        dq, dk, dv = (torch.full_like(ref[k], 3) for k in ("dq_p", "dk_p", "dv_p"))
+        B.prefix_bwd_dq(d, grp.q_p, grp.k_p, grp.v_p, o["o_p"], o["lse_p"], g_y, dq, ws2)
+        B.prefix_bwd_dkv(d, grp.q_p, grp.k_p, grp.v_p, o["o_p"], o["lse_p"], g_y, grp.gk, grp.gv,
+                         dk, dv, grp.ws)
+        torch.cuda.synchronize()
+        assert torch.equal(dq, ref["dq_p"]) and torch.equal(dk, ref["dk_p"])
+        assert torch.equal(dv, ref["dv_p"]), use_gy
 
 
 def test_microbatch_split_and_order_invariance(gpu):

@@ -12,8 +12,10 @@ Sec. 4.2), Phase C ``prefix_bwd`` once.  ``run_dense`` is the comparison:
 
 Streams: Phase A and the Phase B suffix forwards read only inputs, so by
 default they run on two side streams while the backward launches run in
-order on the caller's stream.  A suffix backward waits for its own
-forward, Phase C waits for Phase A and for every suffix backward (their
+order on the caller's stream.  Phase A starts once the first suffix forward
+is done (only Phase C needs it, and the first backward should not wait for
+it).  A suffix backward waits for its own forward, Phase C waits for Phase
+A and for every suffix backward (their
 gK/gV cache updates stay in microbatch order), and the caller's stream
 waits for all of it.  The work items are the same launches with the same
 arguments, so the results are identical to the serial order; the overlap
@@ -189,13 +191,7 @@ class DeviceGroup:
         start = torch.cuda.Event()
         start.record(main)
         B.gkv_cache_zero(self.dims, self.gk, self.gv, main)
-        # Phase A on its own stream: only Phase C reads its outputs
-        s_a.wait_event(start)
-        o = self.out
-        B.prefix_fwd(self.dims, self.q_p, self.k_p, self.v_p, o["o_p"], o["lse_p"], s_a)
-        done_a = torch.cuda.Event()
-        done_a.record(s_a)
-        # suffix forwards in order on a second stream, one event each
+        # suffix forwards in order on one side stream, one event each
         s_f.wait_event(start)
         fwd_done = []
         for a, b in mbs:
@@ -203,6 +199,13 @@ class DeviceGroup:
             e = torch.cuda.Event()
             e.record(s_f)
             fwd_done.append(e)
+        # Phase A on the other side stream, after the first suffix forward so
+        # that the first backward is not held up: only Phase C reads it
+        s_a.wait_event(fwd_done[0] if fwd_done else start)
+        o = self.out
+        B.prefix_fwd(self.dims, self.q_p, self.k_p, self.v_p, o["o_p"], o["lse_p"], s_a)
+        done_a = torch.cuda.Event()
+        done_a.record(s_a)
         # backwards in microbatch order on the caller's stream
         for (a, b), e in zip(mbs, fwd_done):
             main.wait_event(e)

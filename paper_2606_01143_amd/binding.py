@@ -46,6 +46,14 @@ _SIGNATURES = {
     "spr_workspace_size": ([c_int32, _P, c_int32, c_int32, c_int32, POINTER(c_size_t)], c_int32),
     "spr_gkv_cache_zero": ([_P, _P, _P, _P], c_int32),
     "spr_gkv_accumulate": ([_P, _P, _P, _P, _P, _P], c_int32),
+    "spr_moe_stats_bytes": ([c_int32, POINTER(c_size_t)], c_int32),
+    "spr_moe_stats_zero": ([c_int32, _P, _P], c_int32),
+    "spr_moe_aux_workspace_size": ([c_int32, c_int32, POINTER(c_size_t)], c_int32),
+    "spr_moe_aux_accumulate": ([c_int32, c_int32, c_int32, _P, _P, c_int32, _P, _P, _P, c_size_t, _P],
+                               c_int32),
+    "spr_moe_aux_loss": ([c_int32, c_int32, c_double, _P, _P, _P, _P, _P], c_int32),
+    "spr_moe_aux_grad": ([c_int32, c_int32, c_double, c_double, _P, c_int32, c_int32, _P, _P, _P],
+                         c_int32),
     "spr_profile_enable": ([c_int32, c_char_p], c_int32),
     "spr_profile_reset": ([], c_int32),
     "spr_profile_query": ([c_char_p, POINTER(c_double), POINTER(c_int32)], c_int32),
@@ -183,6 +191,43 @@ def dense_recompute_baseline(dims, q_p, k_p, v_p, do_p_seq, q_s, k_s, v_s, do_s,
         _ptr(v_s), _ptr(do_s), _ptr(cu_seqlens), n, max_len, total_len, _ptr(o_p), _ptr(lse_p),
         _ptr(o_s), _ptr(lse_s), _ptr(dq_s), _ptr(dk_s), _ptr(dv_s), _ptr(dq_p), _ptr(dk_p),
         _ptr(dv_p), _ptr(ws), _nbytes(ws), _stream(stream)))
+
+
+def moe_stats_bytes(n_experts: int) -> int:
+    out = c_size_t(0)
+    _check(lib().spr_moe_stats_bytes(n_experts, byref(out)))
+    return int(out.value)
+
+
+def moe_stats_zero(n_experts, stats, stream=None):
+    _check(lib().spr_moe_stats_zero(n_experts, _ptr(stats), _stream(stream)))
+
+
+def moe_aux_workspace_size(n_experts: int, n_tokens: int) -> int:
+    out = c_size_t(0)
+    _check(lib().spr_moe_aux_workspace_size(n_experts, n_tokens, byref(out)))
+    return int(out.value)
+
+
+def moe_aux_accumulate(n_experts, top_k, probs, experts, stats, multiplicity=1,
+                       token_multiplicity=None, ws=None, stream=None):
+    n = int(probs.shape[0]) if probs is not None else 0
+    _check(lib().spr_moe_aux_accumulate(n_experts, top_k, n, _ptr(probs), _ptr(experts),
+                                        multiplicity, _ptr(token_multiplicity), _ptr(stats),
+                                        _ptr(ws), _nbytes(ws), _stream(stream)))
+
+
+def moe_aux_loss(n_experts, top_k, aux_coef, stats, f, p, loss, stream=None):
+    _check(lib().spr_moe_aux_loss(n_experts, top_k, float(aux_coef), _ptr(stats), _ptr(f), _ptr(p),
+                                  _ptr(loss), _stream(stream)))
+
+
+def moe_aux_grad(n_experts, top_k, aux_coef, upstream, stats, dprobs, multiplicity=1,
+                 token_multiplicity=None, stream=None):
+    n = int(dprobs.shape[0])
+    _check(lib().spr_moe_aux_grad(n_experts, top_k, float(aux_coef), float(upstream), _ptr(stats), n,
+                                  multiplicity, _ptr(token_multiplicity), _ptr(dprobs),
+                                  _stream(stream)))
 
 
 def workspace_size(op, dims, n_mb=0, max_len=0, total_len=0) -> int:

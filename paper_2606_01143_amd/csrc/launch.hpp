@@ -78,4 +78,15 @@ hipError_t launch_convert(int dtype, const float* acc, float scale, const float*
 // dst += src
 hipError_t launch_accumulate(float* dst, const float* src, size_t n, hipStream_t st);
 
+// MoE router aux-loss accounting (kernels_moe.hip).  Statistics layout:
+// int64 count[E], double mass[E], int64 total, int64 invalid.
+int moe_blocks(int n_tokens);
+size_t moe_workspace_bytes(int E, int n_tokens);
+hipError_t launch_moe_accumulate(const float* p, const int* r, int n, int E, int k, int mult,
+                                 const int* mu, void* stats, void* ws, hipStream_t st);
+hipError_t launch_moe_loss(const void* stats, int E, int k, double coef, double* f, double* pe,
+                           double* loss, hipStream_t st);
+hipError_t launch_moe_grad(const void* stats, int E, int k, double scale, int n, int mult,
+                           const int* mu, float* dp, hipStream_t st);
+
 }  // namespace spr

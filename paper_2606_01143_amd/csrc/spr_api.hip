@@ -13,6 +13,7 @@
 #include <vector>
 
 #include "../../include/spr.h"
+#include "../../include/spr_moe.h"
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -678,6 +679,119 @@ spr_status spr_gkv_accumulate(const spr_dims* dims, float* gk_cache, float* gv_c
   if ((st = hip_check(launch_accumulate(gk_cache, dgk, n, stream), "cache accumulate")) != SPR_OK)
     return st;
   if ((st = hip_check(launch_accumulate(gv_cache, dgv, n, stream), "cache accumulate")) != SPR_OK)
+    return st;
+  return ok();
+}
+
+// ------------------------------------------------------ MoE aux accounting
+namespace {
+spr_status check_moe(int32_t E, int32_t k) {
+  if (E < 4 || E > 1024 || E % 4 != 0)
+    return fail(SPR_ERR_UNSUPPORTED, "n_experts must be a multiple of 4 in [4, 1024]");
+  if (k < 1 || k > E) return fail(SPR_ERR_INVALID_ARG, "top_k must be in [1, n_experts]");
+  return SPR_OK;
+}
+size_t moe_stats_size(int32_t E) { return 16 * (size_t)E + 16; }
+}  // namespace
+
+spr_status spr_moe_stats_bytes(int32_t n_experts, size_t* bytes) {
+  spr_status st = check_moe(n_experts, 1);
+  if (st != SPR_OK) return st;
+  if (bytes == nullptr) return fail(SPR_ERR_INVALID_ARG, "bytes is null");
+  *bytes = moe_stats_size(n_experts);
+  return ok();
+}
+
+spr_status spr_moe_stats_zero(int32_t n_experts, void* stats, hipStream_t stream) {
+  spr_status st = check_moe(n_experts, 1);
+  if (st != SPR_OK) return st;
+  if ((st = check_bufs({{stats, moe_stats_size(n_experts), "stats", true}})) != SPR_OK) return st;
+  if ((st = hip_check(launch_fill_zero((float*)stats, moe_stats_size(n_experts) / 4, stream), "stats zero")) !=
+      SPR_OK)
+    return st;
+  return ok();
+}
+
+spr_status spr_moe_aux_workspace_size(int32_t n_experts, int32_t n_tokens, size_t* bytes) {
+  spr_status st = check_moe(n_experts, 1);
+  if (st != SPR_OK) return st;
+  if (n_tokens < 0) return fail(SPR_ERR_INVALID_ARG, "n_tokens must be >= 0");
+  if (bytes == nullptr) return fail(SPR_ERR_INVALID_ARG, "bytes is null");
+  *bytes = moe_workspace_bytes(n_experts, n_tokens);
+  return ok();
+}
+
+spr_status spr_moe_aux_accumulate(int32_t n_experts, int32_t top_k, int32_t n_tokens,
+                                  const float* probs, const int32_t* experts,
+                                  int32_t multiplicity, const int32_t* token_multiplicity,
+                                  void* stats, void* ws, size_t ws_bytes, hipStream_t stream) {
+  spr_status st = check_moe(n_experts, top_k);
+  if (st != SPR_OK) return st;
+  if (n_tokens < 0) return fail(SPR_ERR_INVALID_ARG, "n_tokens must be >= 0");
+  if (token_multiplicity == nullptr && multiplicity < 0)
+    return fail(SPR_ERR_INVALID_ARG, "multiplicity must be >= 0");
+  const size_t n = (size_t)n_tokens, E = (size_t)n_experts, k = (size_t)top_k;
+  std::vector<Buf> bufs = {{probs, n * E * 4, "probs", true},
+                           {experts, n * k * 4, "experts", true, 4},
+                           {token_multiplicity, n * 4, "token_multiplicity", false, 4},
+                           {stats, moe_stats_size(n_experts), "stats", true}};
+  if ((st = check_bufs(bufs)) != SPR_OK) return st;
+  const size_t need = moe_workspace_bytes(n_experts, n_tokens);
+  if (need > 0) {
+    if (ws == nullptr) return fail(SPR_ERR_WORKSPACE, "workspace is null");
+    if (ws_bytes < need)
+      return fail(SPR_ERR_WORKSPACE, "workspace too small: need " + std::to_string(need) + " bytes, got " +
+                                         std::to_string(ws_bytes));
+    if (((uintptr_t)ws & 15u) != 0) return fail(SPR_ERR_MISALIGNED, "workspace is not 16-byte aligned");
+  }
+  std::vector<Buf> all = bufs;
+  all.push_back({ws, need, "ws", false});
+  if ((st = check_aliasing({bufs[3]}, all)) != SPR_OK) return st;
+  if (n_tokens == 0) return ok();
+  if ((st = hip_check(launch_moe_accumulate(probs, experts, n_tokens, n_experts, top_k, multiplicity,
+                                            token_multiplicity, stats, ws, stream),
+                      "moe accumulate")) != SPR_OK)
+    return st;
+  return ok();
+}
+
+spr_status spr_moe_aux_loss(int32_t n_experts, int32_t top_k, double aux_coef, const void* stats,
+                            double* f, double* p, double* loss, hipStream_t stream) {
+  spr_status st = check_moe(n_experts, top_k);
+  if (st != SPR_OK) return st;
+  if (!isfinite(aux_coef)) return fail(SPR_ERR_INVALID_ARG, "aux_coef must be finite");
+  const size_t E = (size_t)n_experts;
+  std::vector<Buf> bufs = {{stats, moe_stats_size(n_experts), "stats", true},
+                           {f, E * 8, "f", false, 8},
+                           {p, E * 8, "p", false, 8},
+                           {loss, 8, "loss", true, 8}};
+  if ((st = check_bufs(bufs)) != SPR_OK) return st;
+  if ((st = hip_check(launch_moe_loss(stats, n_experts, top_k, aux_coef, f, p, loss, stream), "moe loss")) !=
+      SPR_OK)
+    return st;
+  return ok();
+}
+
+spr_status spr_moe_aux_grad(int32_t n_experts, int32_t top_k, double aux_coef, double upstream,
+                            const void* stats, int32_t n_tokens, int32_t multiplicity,
+                            const int32_t* token_multiplicity, float* dprobs, hipStream_t stream) {
+  spr_status st = check_moe(n_experts, top_k);
+  if (st != SPR_OK) return st;
+  if (!isfinite(aux_coef) || !isfinite(upstream))
+    return fail(SPR_ERR_INVALID_ARG, "aux_coef and upstream must be finite");
+  if (n_tokens < 0) return fail(SPR_ERR_INVALID_ARG, "n_tokens must be >= 0");
+  if (token_multiplicity == nullptr && multiplicity < 0)
+    return fail(SPR_ERR_INVALID_ARG, "multiplicity must be >= 0");
+  const size_t n = (size_t)n_tokens, E = (size_t)n_experts;
+  std::vector<Buf> bufs = {{stats, moe_stats_size(n_experts), "stats", true},
+                           {token_multiplicity, n * 4, "token_multiplicity", false, 4},
+                           {dprobs, n * E * 4, "dprobs", true}};
+  if ((st = check_bufs(bufs)) != SPR_OK) return st;
+  if ((st = check_aliasing({bufs[2]}, bufs)) != SPR_OK) return st;
+  if (n_tokens == 0) return ok();
+  if ((st = hip_check(launch_moe_grad(stats, n_experts, top_k, upstream * aux_coef, n_tokens, multiplicity,
+                                      token_multiplicity, dprobs, stream),
+                      "moe grad")) != SPR_OK)
     return st;
   return ok();
 }

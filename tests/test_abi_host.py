@@ -14,12 +14,16 @@ from paper_2606_01143_amd import binding as B
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "spr.h")
+HEADERS = sorted(os.path.join(ROOT, "include", f) for f in os.listdir(os.path.join(ROOT, "include"))
+                 if f.endswith(".h"))
 
 
 def header_symbols():
-    text = open(HEADER).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(spr_[a-z_0-9]+)\s*\(", text)))
+    syms = set()
+    for h in HEADERS:
+        text = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        syms.update(re.findall(r"\b(spr_[a-z_0-9]+)\s*\(", text))
+    return sorted(syms)
 
 
 @pytest.fixture(scope="module")
@@ -137,3 +141,44 @@ def test_workspace_sizes_are_consistent(lib):
     assert dense >= 4096 * 32 * 128 * 4 + 4096 * 8 * 128 * 4 * 2
     with pytest.raises(B.SprError):
         B.workspace_size(99, dims)
+
+
+# ---------------------------------------------------------------- MoE accounting
+def _moe_status(fn, *args):
+    return getattr(B.lib(), fn)(*args)
+
+
+@pytest.mark.parametrize("E,k,status", [(128, 8, "SPR_OK"), (6, 1, "SPR_ERR_UNSUPPORTED"),
+                                        (2048, 8, "SPR_ERR_UNSUPPORTED"), (0, 1, "SPR_ERR_UNSUPPORTED"),
+                                        (16, 0, "SPR_ERR_INVALID_ARG"), (16, 17, "SPR_ERR_INVALID_ARG")])
+def test_moe_shape_validation(lib, E, k, status):
+    st = lib.spr_moe_aux_loss(E, k, 0.01, _addr(1), None, None, _addr(2) if status != "SPR_OK" else None,
+                              None)
+    if status == "SPR_OK":
+        # valid shape: the null loss pointer is what gets rejected, before any launch
+        assert B.STATUS[st] == "SPR_ERR_INVALID_ARG"
+    else:
+        assert B.STATUS[st] == status
+
+
+def test_moe_sizes(lib):
+    assert B.moe_stats_bytes(128) == 16 * 128 + 16
+    assert B.moe_aux_workspace_size(128, 0) == 0
+    a, b = B.moe_aux_workspace_size(128, 100), B.moe_aux_workspace_size(128, 100000)
+    assert 0 < a < b and b == 1024 * (128 * 16 + 16)
+
+
+def test_moe_accumulate_checks(lib):
+    f = lib.spr_moe_aux_accumulate
+    ws = _addr(9)
+    # null probs, misaligned probs, negative multiplicity, small workspace, aliasing stats
+    assert B.STATUS[f(16, 2, 10, None, _addr(2), 1, None, _addr(3), ws, 1 << 20, None)] == "SPR_ERR_INVALID_ARG"
+    assert B.STATUS[f(16, 2, 10, _addr(1) + 4, _addr(2), 1, None, _addr(3), ws, 1 << 20, None)] == \
+        "SPR_ERR_MISALIGNED"
+    assert B.STATUS[f(16, 2, 10, _addr(1), _addr(2), -1, None, _addr(3), ws, 1 << 20, None)] == \
+        "SPR_ERR_INVALID_ARG"
+    assert B.STATUS[f(16, 2, 10, _addr(1), _addr(2), 1, None, _addr(3), ws, 8, None)] == "SPR_ERR_WORKSPACE"
+    assert B.STATUS[f(16, 2, 10, _addr(1), _addr(2), 1, None, _addr(1), ws, 1 << 20, None)] == \
+        "SPR_ERR_ALIASING"
+    # zero tokens: nothing to do, no launch
+    assert B.STATUS[f(16, 2, 0, None, None, 1, None, _addr(3), None, 0, None)] == "SPR_OK"

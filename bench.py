@@ -22,7 +22,8 @@ from the kernel sources in the tree (else null).
 
 Prints ONE JSON line.  ``--sweep c3|c4|c5attn|all`` instead prints one JSON
 line per configuration of the speedup surface (schedule vs dense, no CPU
-baseline).  ``--gpus N`` with N > 1 exits: this build runs on one GPU.
+baseline); ``--moe-aux`` prints the MoE router aux-loss accounting line
+(App. B: reuse accounting against the materialized prefix copies).  ``--gpus N`` with N > 1 exits: this build runs on one GPU.
 """
 from __future__ import annotations
 
@@ -204,6 +205,8 @@ def main():
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--sweep", choices=["c3", "c4", "c5attn", "all"], default=None)
+    ap.add_argument("--moe-aux", action="store_true",
+                    help="time the MoE router aux-loss accounting instead (one JSON line)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (--gpus {args.gpus} requested); the multi-GPU "
@@ -215,6 +218,9 @@ def main():
     from paper_2606_01143_amd.group import DeviceGroup
 
     B.lib()  # fails loudly without the HIP library
+    if args.moe_aux:
+        moe_aux_bench(args)
+        return
     if args.sweep:
         names = sum(SWEEPS.values(), []) if args.sweep == "all" else SWEEPS[args.sweep]
         for name in names:
@@ -341,6 +347,144 @@ def sweep_one(name: str, args):
     print(json.dumps(rec), flush=True)
     del grp
     torch.cuda.empty_cache()
+
+
+def moe_aux_bench(args):
+    """MoE router aux-loss accounting (App. B) for one MoE layer of one prompt
+    group: the reuse accounting (prefix tokens once with multiplicity N, then
+    each suffix microbatch with multiplicity 1; loss; router gradients of
+    the prefix and of each suffix microbatch) against the materialized batch
+    (every prefix copy explicit: one accumulate and one gradient over all
+    logical tokens).  One JSON line; value = logical router tokens per second
+    of the reuse step."""
+    import numpy as np
+    import torch
+    from paper_2606_01143_amd import binding as B
+    from synthetic.moe import ROUTER_SHAPES, make_router_group
+    name = "qwen3_moe_router_p8192_n16_ragged"
+    inp = make_router_group(ROUTER_SHAPES[name], seed=args.seed, ragged=(128, 2048))
+    shp = inp["shape"]
+    E, k, n, P = shp.num_experts, shp.top_k, shp.n, shp.prefix_len
+    dev = torch.device("cuda:0")
+    up = lambda x, dt: torch.from_numpy(np.ascontiguousarray(x)).to(device=dev, dtype=dt)
+    p_p, r_p = up(inp["p_p"], torch.float32), up(inp["r_p"], torch.int32)
+    p_s, r_s = up(inp["p_s"], torch.float32), up(inp["r_s"], torch.int32)
+    cu = [int(x) for x in inp["cu_seqlens"]]
+    T = cu[-1]
+    # materialized batch: N prefix copies then the suffix tokens
+    p_m = torch.cat([p_p] * n + [p_s]).contiguous()
+    r_m = torch.cat([r_p] * n + [r_s]).contiguous()
+    stats = torch.empty(B.moe_stats_bytes(E), dtype=torch.uint8, device=dev)
+    ws = torch.empty(B.moe_aux_workspace_size(E, p_m.shape[0]), dtype=torch.uint8, device=dev)
+    f = torch.empty(E, dtype=torch.float64, device=dev)
+    pe = torch.empty_like(f)
+    loss = torch.empty(1, dtype=torch.float64, device=dev)
+    dp_p, dp_s, dp_m = torch.empty_like(p_p), torch.empty_like(p_s), torch.empty_like(p_m)
+    lam = 0.01
+    spans = [(cu[i], cu[i + 1]) for i in range(n)]
+
+    def reuse_step():
+        B.moe_stats_zero(E, stats)
+        B.moe_aux_accumulate(E, k, p_p, r_p, stats, multiplicity=n, ws=ws)
+        for a, b in spans:
+            B.moe_aux_accumulate(E, k, p_s[a:b], r_s[a:b], stats, multiplicity=1, ws=ws)
+        B.moe_aux_loss(E, k, lam, stats, f, pe, loss)
+        B.moe_aux_grad(E, k, lam, 1.0, stats, dp_p, multiplicity=n)
+        for a, b in spans:
+            B.moe_aux_grad(E, k, lam, 1.0, stats, dp_s[a:b], multiplicity=1)
+
+    def reuse_step_packed():
+        # the same accounting with the suffixes as one packed microbatch
+        B.moe_stats_zero(E, stats)
+        B.moe_aux_accumulate(E, k, p_p, r_p, stats, multiplicity=n, ws=ws)
+        B.moe_aux_accumulate(E, k, p_s, r_s, stats, multiplicity=1, ws=ws)
+        B.moe_aux_loss(E, k, lam, stats, f, pe, loss)
+        B.moe_aux_grad(E, k, lam, 1.0, stats, dp_p, multiplicity=n)
+        B.moe_aux_grad(E, k, lam, 1.0, stats, dp_s, multiplicity=1)
+
+    def materialized_step():
+        B.moe_stats_zero(E, stats)
+        B.moe_aux_accumulate(E, k, p_m, r_m, stats, multiplicity=1, ws=ws)
+        B.moe_aux_loss(E, k, lam, stats, f, pe, loss)
+        B.moe_aux_grad(E, k, lam, 1.0, stats, dp_m, multiplicity=1)
+
+    steps, warm = max(1, args.steps), max(1, args.warmup)
+    # per-kernel times of one untimed step
+    B.profile_reset()
+    B.profile_enable(True)
+    reuse_step()
+    torch.cuda.synchronize()
+    B.profile_enable(False)
+    per_kernel = {kk: round(B.profile_query(kk)[0] * 1e3, 2) for kk in B.profile_kernels()
+                  if B.profile_query(kk)[1]}
+    dominant = max(("moe_partial", "moe_grad"), key=lambda kk: per_kernel.get(kk, 0.0))
+    nb_bytes = lambda nt: B.moe_aux_workspace_size(E, nt)
+    if dominant == "moe_partial":
+        per_step_bytes = sum((nt * E * 4 + nt * k * 4 + nb_bytes(nt)) for nt in [P] + [b - a for a, b in spans])
+    else:
+        per_step_bytes = (P + T) * E * 4
+    for _ in range(warm):
+        reuse_step()
+    B.profile_reset()
+    B.profile_enable(True, dominant)
+    ms_eager = time_steps(reuse_step, steps, 0)
+    B.profile_enable(False)
+    dom_ms, dom_n = B.profile_query(dominant)
+    ms_mat_eager = time_steps(materialized_step, steps, warm)
+    # the step is a few dozen short launches: capture each in a HIP graph and
+    # time the replays (no host launch overhead)
+    graphs = {}
+    for key, fn in (("reuse", reuse_step), ("packed", reuse_step_packed), ("materialized", materialized_step)):
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            fn()
+        torch.cuda.current_stream().wait_stream(side)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            fn()
+        graphs[key] = g
+    ms = time_steps(graphs["reuse"].replay, steps, warm)
+    ms_mat = time_steps(graphs["materialized"].replay, steps, warm)
+    ms_packed = time_steps(graphs["packed"].replay, steps, warm)
+    # algorithmic HBM bytes of a step: probabilities and expert ids read, the
+    # gradient written (reuse: physical tokens; materialized: logical ones)
+    step_bytes = lambda nt: nt * (E * 4 + k * 4 + E * 4)
+    logical = n * P + T
+    achieved = per_step_bytes * steps / (dom_ms * 1e-3) / 1e9 if dom_ms > 0 else 0.0
+    # cpu baseline: the oracle's reuse accounting on the same inputs
+    from oracle.moe_aux import reuse_reference
+    t0 = time.perf_counter()
+    reps = 0
+    while True:
+        reuse_reference(inp, lam)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= min(args.cpu_seconds, 5.0) or reps >= 50:
+            break
+    out = {"metric": "MoE router aux-loss accounting, logical tokens/s (one MoE layer of one group)",
+           "value": round(logical / (ms * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1, "steps": steps,
+           "warmup": warm, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+           "config": {"workload": name, "num_experts": E, "top_k": k, "prefix_len": P, "n_suffixes": n,
+                      "total_suffix_tokens": T, "microbatching": "per_suffix"},
+           "timing": "HIP graph replay of the step",
+           "eager_ms_per_step": round(ms_eager, 4), "materialized_eager_ms_per_step": round(ms_mat_eager, 4),
+           "materialized_ms_per_step": round(ms_mat, 4), "speedup_vs_materialized": round(ms_mat / ms, 3),
+           "packed_suffix_ms_per_step": round(ms_packed, 4),
+           "packed_speedup_vs_materialized": round(ms_mat / ms_packed, 3),
+           "step_hbm_bytes": {"reuse": step_bytes(P + T), "materialized": step_bytes(logical)},
+           "token_ratio_materialized_over_reuse": round(logical / (P + T), 3),
+           "kernel_us_one_step": per_kernel,
+           "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                        "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None, "kernel": dominant,
+                        "launches_per_step": dom_n // steps,
+                        "avg_launch_us": round(dom_ms * 1e3 / max(dom_n, 1), 2),
+                        "measured": "HIP events around each launch of the eager step"},
+           "cpu_baseline": {"value": round(logical * reps / el, 1), "unit": "tokens/s", "cores": 1,
+                            "kind": "oracle", "sample": f"fp64 reuse accounting of the same group, {reps} "
+                                                        f"repetitions in {el:.1f} s"}}
+    print(json.dumps(out), flush=True)
 
 
 if __name__ == "__main__":

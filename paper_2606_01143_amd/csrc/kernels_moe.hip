@@ -60,13 +60,25 @@ __global__ __launch_bounds__(kMoeThreads) void moe_partial_kernel(
   const int tc = tid % cols, tr = tid / cols;
   double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
   if (tr < rows_par) {
-    for (int u = u0 + tr; u < u1; u += rows_par) {
-      const double m = (double)token_mult(u, mult, mu);
-      const float4 v = *(const float4*)(p + (size_t)u * E + 4 * tc);
-      a0 = fma(m, (double)v.x, a0);
-      a1 = fma(m, (double)v.y, a1);
-      a2 = fma(m, (double)v.z, a2);
-      a3 = fma(m, (double)v.w, a3);
+    // eight rows' loads in flight before their products are added (in row order)
+    constexpr int kRows = 8;
+    for (int ub = u0 + tr; ub < u1; ub += kRows * rows_par) {
+      float4 v[kRows];
+      double m[kRows];
+#pragma unroll
+      for (int q = 0; q < kRows; ++q) {
+        const int u = ub + q * rows_par;
+        const bool in = u < u1;
+        v[q] = in ? *(const float4*)(p + (size_t)u * E + 4 * tc) : make_float4(0.f, 0.f, 0.f, 0.f);
+        m[q] = in ? (double)token_mult(u, mult, mu) : 0.0;
+      }
+#pragma unroll
+      for (int q = 0; q < kRows; ++q) {
+        a0 = fma(m[q], (double)v[q].x, a0);
+        a1 = fma(m[q], (double)v[q].y, a1);
+        a2 = fma(m[q], (double)v[q].z, a2);
+        a3 = fma(m[q], (double)v[q].w, a3);
+      }
     }
   }
   red[4 * tid + 0] = a0;
@@ -89,34 +101,51 @@ __global__ __launch_bounds__(kMoeThreads) void moe_partial_kernel(
   }
 }
 
-// stats += the partials of blocks 0 .. nb - 1, in block order.  Thread e
-// owns expert e; the first thread also adds the totals.
+// stats += the partials of blocks 0 .. nb - 1.  Block e < E owns expert e,
+// block E the totals; thread t adds the partials of blocks t, t + 256, ...
+// in order, then a fixed-shape tree adds the threads' sums.
 __global__ __launch_bounds__(kMoeThreads) void moe_reduce_kernel(const double* __restrict__ part_mass,
                                                                  const long long* __restrict__ part_count,
                                                                  const long long* __restrict__ part_tot,
                                                                  int nb, int E, unsigned char* stats) {
+  __shared__ double rm[kMoeThreads];
+  __shared__ long long rc[kMoeThreads];
+  const int tid = threadIdx.x, e = blockIdx.x;
+  double s = 0.0;
+  long long c = 0;
+  if (e < E) {
+    for (int b = tid; b < nb; b += kMoeThreads) {
+      s += part_mass[(size_t)b * E + e];
+      c += part_count[(size_t)b * E + e];
+    }
+  } else {
+    long long inv = 0;
+    for (int b = tid; b < nb; b += kMoeThreads) {
+      c += part_tot[2 * b];
+      inv += part_tot[2 * b + 1];
+    }
+    s = (double)inv;  // exact: far below 2^53
+  }
+  rm[tid] = s;
+  rc[tid] = c;
+  __syncthreads();
+  for (int h = kMoeThreads / 2; h > 0; h >>= 1) {
+    if (tid < h) {
+      rm[tid] += rm[tid + h];
+      rc[tid] += rc[tid + h];
+    }
+    __syncthreads();
+  }
+  if (tid != 0) return;
   long long* count = (long long*)stats;
   double* mass = (double*)(stats + 8 * (size_t)E);
   long long* total = (long long*)(stats + 16 * (size_t)E);
-  const int e = blockIdx.x * kMoeThreads + threadIdx.x;
   if (e < E) {
-    long long c = 0;
-    double s = 0.0;
-    for (int b = 0; b < nb; ++b) {
-      c += part_count[(size_t)b * E + e];
-      s += part_mass[(size_t)b * E + e];
-    }
-    count[e] += c;
-    mass[e] += s;
-  }
-  if (e == 0) {
-    long long t = 0, inv = 0;
-    for (int b = 0; b < nb; ++b) {
-      t += part_tot[2 * b];
-      inv += part_tot[2 * b + 1];
-    }
-    total[0] += t;
-    total[1] += inv;
+    count[e] += rc[0];
+    mass[e] += rm[0];
+  } else {
+    total[0] += rc[0];
+    total[1] += (long long)rm[0];
   }
 }
 
@@ -172,8 +201,10 @@ __global__ __launch_bounds__(kMoeThreads) void moe_grad_kernel(const unsigned ch
 }
 
 int moe_blocks(int n_tokens) {
+  // 32 tokens per block (one load round trip per thread at E = 128), at
+  // most 2048 partials per expert
   if (n_tokens <= 0) return 0;
-  return std::min((n_tokens + 63) / 64, 1024);
+  return std::min((n_tokens + 31) / 32, 2048);
 }
 
 size_t moe_workspace_bytes(int E, int n_tokens) {
@@ -197,7 +228,7 @@ hipError_t launch_moe_accumulate(const float* p, const int* r, int n, int E, int
     if (e != hipSuccess) return e;
   }
   ProfileScope pr("moe_reduce", st);
-  hipLaunchKernelGGL(moe_reduce_kernel, dim3((E + kMoeThreads - 1) / kMoeThreads), dim3(kMoeThreads), 0, st,
+  hipLaunchKernelGGL(moe_reduce_kernel, dim3(E + 1), dim3(kMoeThreads), 0, st,
                      part_mass, part_count, part_tot, nb, E, (unsigned char*)stats);
   return hipGetLastError();
 }

@@ -170,3 +170,50 @@ def test_moe_zero_total_gives_zeros(gpu):
     got = dev.read()
     assert got["M"] == 0 and not got["C"].any() and got["L"] == 0.0
     assert not got["f"].any() and not got["P"].any() and not dp.cpu().numpy().any()
+
+
+@pytest.mark.gpu
+def test_moe_step_in_a_hip_graph_replays_exactly(gpu):
+    """The reuse step (stats zero, accumulates, loss, gradients) captured in a
+    HIP graph: every replay, with eager library work and synchronizations in
+    between, reproduces the eager result bitwise."""
+    import torch
+    from paper_2606_01143_amd import binding as B
+    shape = RouterShape(64, 4, 300, (70, 129, 33))
+    _announce(f"graph replay {shape}")
+    inp = make_router_group(shape, seed=19)
+    dev = _Dev(inp)
+    dp_p, dp_s = torch.empty_like(dev.p_p), torch.empty_like(dev.p_s)
+
+    def step():
+        B.moe_stats_zero(dev.E, dev.stats)
+        B.moe_aux_accumulate(dev.E, dev.k, dev.p_p, dev.r_p, dev.stats, multiplicity=dev.n, ws=dev.ws)
+        for i in range(dev.n):
+            a, b = dev.cu[i], dev.cu[i + 1]
+            B.moe_aux_accumulate(dev.E, dev.k, dev.p_s[a:b], dev.r_s[a:b], dev.stats, ws=dev.ws)
+        B.moe_aux_loss(dev.E, dev.k, LAM, dev.stats, dev.f, dev.pe, dev.loss)
+        B.moe_aux_grad(dev.E, dev.k, LAM, 1.0, dev.stats, dp_p, multiplicity=dev.n)
+        B.moe_aux_grad(dev.E, dev.k, LAM, 1.0, dev.stats, dp_s)
+
+    step()
+    torch.cuda.synchronize()
+    ref = (dev.stats.clone(), dev.loss.clone(), dp_p.clone(), dp_s.clone())
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    other = torch.empty_like(dev.stats)
+    for rep in range(3):
+        # eager work on the same buffers between replays
+        dp_p.fill_(5.0)
+        B.moe_stats_zero(dev.E, other)
+        B.moe_aux_accumulate(dev.E, dev.k, dev.p_s, dev.r_s, other, ws=dev.ws)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        got = (dev.stats, dev.loss, dp_p, dp_s)
+        assert all(torch.equal(x, y) for x, y in zip(got, ref)), rep

@@ -110,7 +110,9 @@ typedef enum spr_op {
   SPR_OP_SUFFIX_FWD = 1,
   SPR_OP_SUFFIX_BWD = 2,
   SPR_OP_PREFIX_BWD = 3,
-  SPR_OP_DENSE_BASELINE = 4
+  SPR_OP_DENSE_BASELINE = 4,
+  SPR_OP_SUFFIX_FWD_PADDED = 5,
+  SPR_OP_SUFFIX_BWD_PADDED = 6
 } spr_op;
 
 /*
@@ -157,6 +159,32 @@ spr_status spr_suffix_attn_bwd_accum(const spr_dims* dims, const void* k_p, cons
                                      int32_t total_len, void* dq_s, void* dk_s, void* dv_s,
                                      float* gk_cache, float* gv_cache, void* ws, size_t ws_bytes,
                                      hipStream_t stream);
+
+/*
+ * Phase B with batch-plus-padding suffixes (paper Sec. 2.1, Sec. 4.2: the
+ * schedule is transparent to the suffix organisation).  Suffix tensors are
+ * [n, s_max, H, d] (LSE [n, s_max, Hq]); suffix i holds seq_lens[i] valid
+ * rows (a DEVICE int32 array of n entries, each in [1, s_max]; the library
+ * clamps values into [0, s_max] so that no access leaves the buffers) and
+ * rows t >= seq_lens[i] are padding: they attend to nothing, nothing attends
+ * to them, and every output row of padding is set to zero.  The valid rows
+ * are gathered into the packed layout inside the workspace, run through the
+ * packed calls above, and scattered back, so the results (and the cache
+ * update) are bitwise those of the packed calls on the same suffixes.
+ * Workspace: spr_workspace_size(SPR_OP_SUFFIX_{FWD,BWD}_PADDED, dims, n,
+ * s_max, 0).  Other arguments as in the packed calls.
+ */
+spr_status spr_suffix_attn_fwd_padded(const spr_dims* dims, const void* k_p, const void* v_p,
+                                      const void* q_s, const void* k_s, const void* v_s,
+                                      const int32_t* seq_lens, int32_t n, int32_t s_max, void* o_s,
+                                      float* lse_s, void* ws, size_t ws_bytes, hipStream_t stream);
+spr_status spr_suffix_attn_bwd_accum_padded(const spr_dims* dims, const void* k_p, const void* v_p,
+                                            const void* q_s, const void* k_s, const void* v_s,
+                                            const void* o_s, const float* lse_s, const void* do_s,
+                                            const int32_t* seq_lens, int32_t n, int32_t s_max,
+                                            void* dq_s, void* dk_s, void* dv_s, float* gk_cache,
+                                            float* gv_cache, void* ws, size_t ws_bytes,
+                                            hipStream_t stream);
 
 /*
  * Phase C (paper App. A.3-A.5): one prefix backward with the injected cache,

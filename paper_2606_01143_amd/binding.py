@@ -24,6 +24,8 @@ OP_SUFFIX_FWD = 1
 OP_SUFFIX_BWD = 2
 OP_PREFIX_BWD = 3
 OP_DENSE_BASELINE = 4
+OP_SUFFIX_FWD_PADDED = 5
+OP_SUFFIX_BWD_PADDED = 6
 
 STATUS = {0: "SPR_OK", 1: "SPR_ERR_INVALID_ARG", 2: "SPR_ERR_UNSUPPORTED",
           3: "SPR_ERR_MISALIGNED", 4: "SPR_ERR_ALIASING", 5: "SPR_ERR_WORKSPACE",
@@ -38,6 +40,10 @@ _SIGNATURES = {
     "spr_suffix_attn_bwd_accum": ([_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, c_int32, c_int32, c_int32,
                                    _P, _P, _P, _P, _P, _P, c_size_t, _P], c_int32),
     "spr_prefix_bwd": ([_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, c_size_t, _P], c_int32),
+    "spr_suffix_attn_fwd_padded": ([_P, _P, _P, _P, _P, _P, _P, c_int32, c_int32, _P, _P, _P, c_size_t, _P],
+                                   c_int32),
+    "spr_suffix_attn_bwd_accum_padded": ([_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, c_int32, c_int32, _P, _P,
+                                          _P, _P, _P, _P, c_size_t, _P], c_int32),
     "spr_prefix_bwd_dq": ([_P, _P, _P, _P, _P, _P, _P, _P, _P, c_size_t, _P], c_int32),
     "spr_prefix_bwd_dkv": ([_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, c_size_t, _P], c_int32),
     "spr_dense_recompute_baseline": ([_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, c_int32, c_int32,
@@ -167,6 +173,21 @@ def prefix_bwd(dims, q_p, k_p, v_p, o_p, lse_p, do_p, gk_cache, gv_cache, dq_p, 
                                 _ptr(lse_p), _ptr(do_p), _ptr(gk_cache), _ptr(gv_cache),
                                 _ptr(dq_p), _ptr(dk_p), _ptr(dv_p), _ptr(ws), _nbytes(ws),
                                 _stream(stream)))
+
+
+def suffix_attn_fwd_padded(dims, k_p, v_p, q_s, k_s, v_s, seq_lens, n, s_max, o_s, lse_s, ws=None,
+                           stream=None):
+    _check(lib().spr_suffix_attn_fwd_padded(byref(dims), _ptr(k_p), _ptr(v_p), _ptr(q_s), _ptr(k_s),
+                                            _ptr(v_s), _ptr(seq_lens), n, s_max, _ptr(o_s), _ptr(lse_s),
+                                            _ptr(ws), _nbytes(ws), _stream(stream)))
+
+
+def suffix_attn_bwd_accum_padded(dims, k_p, v_p, q_s, k_s, v_s, o_s, lse_s, do_s, seq_lens, n, s_max,
+                                 dq_s, dk_s, dv_s, gk_cache, gv_cache, ws=None, stream=None):
+    _check(lib().spr_suffix_attn_bwd_accum_padded(
+        byref(dims), _ptr(k_p), _ptr(v_p), _ptr(q_s), _ptr(k_s), _ptr(v_s), _ptr(o_s), _ptr(lse_s),
+        _ptr(do_s), _ptr(seq_lens), n, s_max, _ptr(dq_s), _ptr(dk_s), _ptr(dv_s), _ptr(gk_cache),
+        _ptr(gv_cache), _ptr(ws), _nbytes(ws), _stream(stream)))
 
 
 def prefix_bwd_dq(dims, q_p, k_p, v_p, o_p, lse_p, do_p, dq_p, ws=None, stream=None):

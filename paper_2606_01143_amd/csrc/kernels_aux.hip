@@ -5,6 +5,7 @@
 // All of them stream memory once with 16-byte vector accesses; the fill and
 // accumulate kernels are grid-stride loops sized to a few waves per CU.
 #include "common.hpp"
+
 #include "launch.hpp"
 
 namespace spr {
@@ -164,6 +165,105 @@ hipError_t launch_convert(int dtype, const float* acc, float scale, const float*
   else
     hipLaunchKernelGGL(convert_kernel<bf16>, aux_blocks(n4), kAuxThreads, 0, st,
                        (const float4*)acc, scale, (const float4*)add, (bf16*)out, n4);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------- padded suffix layout
+// Batch-plus-padding suffix tensors [n, s_max, row] are gathered into the
+// packed layout [sum len, row] the attention kernels take, and the packed
+// outputs scattered back (padding rows set to zero).
+
+// cu[0..n] = exclusive prefix sum of the lengths clamped into [0, s_max]
+// (clamped so that no gather or scatter can leave its buffers), lens_c the
+// clamped lengths.  One block: the lengths go through LDS in chunks, one
+// thread adds them in order.
+__global__ __launch_bounds__(kAuxThreads) void seq_offsets_kernel(const int32_t* __restrict__ lens, int n,
+                                                                  int s_max, int32_t* __restrict__ cu,
+                                                                  int32_t* __restrict__ lens_c) {
+  __shared__ int32_t chunk[kAuxThreads];
+  int32_t run = 0;
+  for (int base = 0; base < n; base += kAuxThreads) {
+    const int i = base + (int)threadIdx.x;
+    if (i < n) {
+      const int32_t l = min(max(lens[i], 0), s_max);
+      chunk[threadIdx.x] = l;
+      lens_c[i] = l;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      const int m = min(kAuxThreads, n - base);
+      for (int j = 0; j < m; ++j) {
+        cu[base + j] = run;
+        run += chunk[j];
+      }
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) cu[n] = run;
+}
+
+// packed[cu[i] + t] = padded[i, t] for t < lens_c[i]; V-sized units
+template <typename V>
+__global__ __launch_bounds__(kAuxThreads) void gather_rows_kernel(const V* __restrict__ src, V* __restrict__ dst,
+                                                                  const int32_t* __restrict__ cu,
+                                                                  const int32_t* __restrict__ lens_c, int s_max,
+                                                                  int units, long total) {
+  const long idx = (long)blockIdx.x * kAuxThreads + threadIdx.x;
+  if (idx >= total) return;
+  const long pr = idx / units;
+  const int u = (int)(idx % units);
+  const int i = (int)(pr / s_max), t = (int)(pr % s_max);
+  if (t < lens_c[i]) dst[((long)cu[i] + t) * units + u] = src[idx];
+}
+
+__device__ __forceinline__ float4 zero_unit(float4) { return make_float4(0.f, 0.f, 0.f, 0.f); }
+__device__ __forceinline__ float zero_unit(float) { return 0.f; }
+
+// padded[i, t] = packed[cu[i] + t] for t < lens_c[i], else zero
+template <typename V>
+__global__ __launch_bounds__(kAuxThreads) void scatter_rows_kernel(const V* __restrict__ src, V* __restrict__ dst,
+                                                                   const int32_t* __restrict__ cu,
+                                                                   const int32_t* __restrict__ lens_c,
+                                                                   int s_max, int units, long total) {
+  const long idx = (long)blockIdx.x * kAuxThreads + threadIdx.x;
+  if (idx >= total) return;
+  const long pr = idx / units;
+  const int u = (int)(idx % units);
+  const int i = (int)(pr / s_max), t = (int)(pr % s_max);
+  dst[idx] = t < lens_c[i] ? src[((long)cu[i] + t) * units + u] : zero_unit(V());
+}
+
+hipError_t launch_seq_offsets(const int32_t* lens, int n, int s_max, int32_t* cu, int32_t* lens_c,
+                              hipStream_t st) {
+  ProfileScope ps("seq_offsets", st);
+  hipLaunchKernelGGL(seq_offsets_kernel, dim3(1), dim3(kAuxThreads), 0, st, lens, n, s_max, cu, lens_c);
+  return hipGetLastError();
+}
+
+hipError_t launch_rows_move(bool gather, const void* src, void* dst, const int32_t* cu, const int32_t* lens_c,
+                            int n, int s_max, size_t row_bytes, hipStream_t st) {
+  // 16-byte units when rows and pointers allow, else 4-byte units
+  const bool wide = row_bytes % 16 == 0 && ((uintptr_t)src & 15) == 0 && ((uintptr_t)dst & 15) == 0;
+  const int units = (int)(row_bytes / (wide ? 16 : 4));
+  const long total = (long)n * s_max * units;
+  if (total == 0) return hipSuccess;
+  const unsigned nb = (unsigned)((total + kAuxThreads - 1) / kAuxThreads);
+  ProfileScope ps(gather ? "rows_gather" : "rows_scatter", st);
+  if (wide) {
+    if (gather)
+      hipLaunchKernelGGL(gather_rows_kernel<float4>, dim3(nb), dim3(kAuxThreads), 0, st, (const float4*)src,
+                         (float4*)dst, cu, lens_c, s_max, units, total);
+    else
+      hipLaunchKernelGGL(scatter_rows_kernel<float4>, dim3(nb), dim3(kAuxThreads), 0, st, (const float4*)src,
+                         (float4*)dst, cu, lens_c, s_max, units, total);
+  } else {
+    if (gather)
+      hipLaunchKernelGGL(gather_rows_kernel<float>, dim3(nb), dim3(kAuxThreads), 0, st, (const float*)src,
+                         (float*)dst, cu, lens_c, s_max, units, total);
+    else
+      hipLaunchKernelGGL(scatter_rows_kernel<float>, dim3(nb), dim3(kAuxThreads), 0, st, (const float*)src,
+                         (float*)dst, cu, lens_c, s_max, units, total);
+  }
   return hipGetLastError();
 }
 

@@ -77,6 +77,12 @@ hipError_t launch_convert(int dtype, const float* acc, float scale, const float*
                           void* out, size_t n, hipStream_t st);
 // dst += src
 hipError_t launch_accumulate(float* dst, const float* src, size_t n, hipStream_t st);
+// padded suffix layout: cu/lens_c from device lengths, and row gather
+// (padded -> packed) or scatter (packed -> padded, padding rows zeroed)
+hipError_t launch_seq_offsets(const int32_t* lens, int n, int s_max, int32_t* cu, int32_t* lens_c,
+                              hipStream_t st);
+hipError_t launch_rows_move(bool gather, const void* src, void* dst, const int32_t* cu,
+                            const int32_t* lens_c, int n, int s_max, size_t row_bytes, hipStream_t st);
 
 // MoE router aux-loss accounting (kernels_moe.hip).  Statistics layout:
 // int64 count[E], double mass[E], int64 total, int64 invalid.

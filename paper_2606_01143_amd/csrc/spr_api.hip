@@ -58,6 +58,13 @@ spr_status check_dims(const spr_dims* d) {
   return SPR_OK;
 }
 
+spr_status check_padded_sizes(int32_t n, int32_t s_max) {
+  if (n < 1) return fail(SPR_ERR_INVALID_ARG, "number of suffixes must be >= 1");
+  if (s_max < 1) return fail(SPR_ERR_INVALID_ARG, "s_max must be >= 1");
+  if ((int64_t)n * s_max > INT32_MAX) return fail(SPR_ERR_INVALID_ARG, "n * s_max exceeds 2^31 - 1");
+  return SPR_OK;
+}
+
 spr_status check_suffix_sizes(int32_t n, int32_t max_len, int32_t total_len) {
   if (n < 1) return fail(SPR_ERR_INVALID_ARG, "number of suffixes must be >= 1");
   if (max_len < 1) return fail(SPR_ERR_INVALID_ARG, "max_len must be >= 1");
@@ -165,6 +172,9 @@ struct WsLayout {
   size_t dd_p = 0, dq_acc_p = 0, dd_s = 0, dq_acc_s = 0, dk_acc_p = 0, dv_acc_p = 0;
   size_t lse2_p = 0, lse2_s = 0;
   size_t part_o = 0, part_lse = 0, part_dq = 0;
+  // padded layout: offsets, clamped lengths, packed copies, inner workspace
+  size_t cu = 0, lens_c = 0, pq = 0, pk = 0, pv = 0, po = 0, plse = 0, pdo = 0;
+  size_t pdq = 0, pdk = 0, pdv = 0, inner = 0, inner_bytes = 0;
   size_t total = 0;
 };
 
@@ -205,6 +215,29 @@ WsLayout ws_layout(int op, const spr_dims* d, int32_t n_mb, int32_t max_len, int
       w.lse2_p = take(hq * P * 4);
       if (f32) w.dq_acc_p = take(P * hq * hd * 4);
       break;
+    case SPR_OP_SUFFIX_FWD_PADDED:
+    case SPR_OP_SUFFIX_BWD_PADDED: {
+      // packed copies for the worst case of n_mb full suffixes
+      const size_t R = (size_t)(n_mb > 0 ? n_mb : 0) * (size_t)(max_len > 0 ? max_len : 0);
+      const size_t eb = dtype_bytes(d->dtype);
+      const bool bwd = op == SPR_OP_SUFFIX_BWD_PADDED;
+      w.cu = take((size_t)(n_mb + 1) * 4);
+      w.lens_c = take((size_t)(n_mb > 0 ? n_mb : 0) * 4);
+      w.pq = take(R * hq * hd * eb);
+      w.pk = take(R * hkv * hd * eb);
+      w.pv = take(R * hkv * hd * eb);
+      w.po = take(R * hq * hd * eb);
+      w.plse = take(R * hq * 4);
+      if (bwd) {
+        w.pdo = take(R * hq * hd * eb);
+        w.pdq = take(R * hq * hd * eb);
+        w.pdk = take(R * hkv * hd * eb);
+        w.pdv = take(R * hkv * hd * eb);
+      }
+      w.inner_bytes = ws_layout(bwd ? SPR_OP_SUFFIX_BWD : SPR_OP_SUFFIX_FWD, d, n_mb, max_len, (int32_t)R).total;
+      w.inner = take(w.inner_bytes);
+      break;
+    }
     case SPR_OP_DENSE_BASELINE:
       w.dd_p = take(hq * P * 4);
       w.lse2_p = take(hq * P * 4);
@@ -318,9 +351,11 @@ spr_status spr_workspace_size(int32_t op, const spr_dims* dims, int32_t n_mb, in
   spr_status st = check_dims(dims);
   if (st != SPR_OK) return st;
   if (bytes == nullptr) return fail(SPR_ERR_INVALID_ARG, "bytes is null");
-  if (op < SPR_OP_PREFIX_FWD || op > SPR_OP_DENSE_BASELINE)
+  if (op < SPR_OP_PREFIX_FWD || op > SPR_OP_SUFFIX_BWD_PADDED)
     return fail(SPR_ERR_INVALID_ARG, "unknown op");
-  if (op != SPR_OP_PREFIX_FWD && op != SPR_OP_PREFIX_BWD) {
+  if (op == SPR_OP_SUFFIX_FWD_PADDED || op == SPR_OP_SUFFIX_BWD_PADDED) {
+    if ((st = check_padded_sizes(n_mb, max_len)) != SPR_OK) return st;
+  } else if (op != SPR_OP_PREFIX_FWD && op != SPR_OP_PREFIX_BWD) {
     st = check_suffix_sizes(n_mb, max_len, total_len);
     if (st != SPR_OK) return st;
   }
@@ -452,6 +487,120 @@ spr_status spr_suffix_attn_bwd_accum(const spr_dims* dims, const void* k_p, cons
   if (f32 && (st = hip_check(launch_convert(dims->dtype, dq_acc, a.scale, nullptr, dq_s,
                                             T * hq * hd, stream), "dq convert")) != SPR_OK)
     return st;
+  return ok();
+}
+
+// ------------------------------------------------- padded suffix layout
+spr_status spr_suffix_attn_fwd_padded(const spr_dims* dims, const void* k_p, const void* v_p,
+                                      const void* q_s, const void* k_s, const void* v_s,
+                                      const int32_t* seq_lens, int32_t n, int32_t s_max, void* o_s,
+                                      float* lse_s, void* ws, size_t ws_bytes, hipStream_t stream) {
+  spr_status st = check_dims(dims);
+  if (st != SPR_OK) return st;
+  if ((st = check_padded_sizes(n, s_max)) != SPR_OK) return st;
+  const size_t P = dims->prefix_len, hq = dims->num_q_heads, hkv = dims->num_kv_heads,
+               hd = dims->head_dim, eb = dtype_bytes(dims->dtype), R = (size_t)n * s_max;
+  std::vector<Buf> bufs = {{k_p, P * hkv * hd * eb, "k_p", true},
+                           {v_p, P * hkv * hd * eb, "v_p", true},
+                           {q_s, R * hq * hd * eb, "q_s", true},
+                           {k_s, R * hkv * hd * eb, "k_s", true},
+                           {v_s, R * hkv * hd * eb, "v_s", true},
+                           {seq_lens, (size_t)n * 4, "seq_lens", true, 4},
+                           {o_s, R * hq * hd * eb, "o_s", true},
+                           {lse_s, R * hq * 4, "lse_s", true, 4}};
+  if ((st = check_bufs(bufs)) != SPR_OK) return st;
+  const WsLayout w = ws_layout(SPR_OP_SUFFIX_FWD_PADDED, dims, n, s_max, 0);
+  if ((st = check_ws(w, ws, ws_bytes)) != SPR_OK) return st;
+  std::vector<Buf> all = bufs;
+  all.push_back({ws, w.total, "ws", false});
+  if ((st = check_aliasing({bufs[6], bufs[7], all.back()}, all)) != SPR_OK) return st;
+  int32_t* cu = at<int32_t>(ws, w.cu);
+  int32_t* lens_c = at<int32_t>(ws, w.lens_c);
+  void *pq = at<char>(ws, w.pq), *pk = at<char>(ws, w.pk), *pv = at<char>(ws, w.pv), *po = at<char>(ws, w.po);
+  float* plse = at<float>(ws, w.plse);
+  if ((st = hip_check(launch_seq_offsets(seq_lens, n, s_max, cu, lens_c, stream), "offsets")) != SPR_OK) return st;
+  const struct {
+    const void* src;
+    void* dst;
+    size_t row;
+  } in[] = {{q_s, pq, hq * hd * eb}, {k_s, pk, hkv * hd * eb}, {v_s, pv, hkv * hd * eb}};
+  for (const auto& x : in)
+    if ((st = hip_check(launch_rows_move(true, x.src, x.dst, cu, lens_c, n, s_max, x.row, stream), "gather")) !=
+        SPR_OK)
+      return st;
+  if ((st = spr_suffix_attn_fwd(dims, k_p, v_p, pq, pk, pv, cu, n, s_max, (int32_t)R, po, plse,
+                                at<char>(ws, w.inner), w.inner_bytes, stream)) != SPR_OK)
+    return st;
+  if ((st = hip_check(launch_rows_move(false, po, o_s, cu, lens_c, n, s_max, hq * hd * eb, stream), "scatter")) !=
+      SPR_OK)
+    return st;
+  if ((st = hip_check(launch_rows_move(false, plse, lse_s, cu, lens_c, n, s_max, hq * 4, stream), "scatter")) !=
+      SPR_OK)
+    return st;
+  return ok();
+}
+
+spr_status spr_suffix_attn_bwd_accum_padded(const spr_dims* dims, const void* k_p, const void* v_p,
+                                            const void* q_s, const void* k_s, const void* v_s,
+                                            const void* o_s, const float* lse_s, const void* do_s,
+                                            const int32_t* seq_lens, int32_t n, int32_t s_max,
+                                            void* dq_s, void* dk_s, void* dv_s, float* gk_cache,
+                                            float* gv_cache, void* ws, size_t ws_bytes,
+                                            hipStream_t stream) {
+  spr_status st = check_dims(dims);
+  if (st != SPR_OK) return st;
+  if ((st = check_padded_sizes(n, s_max)) != SPR_OK) return st;
+  const size_t P = dims->prefix_len, hq = dims->num_q_heads, hkv = dims->num_kv_heads,
+               hd = dims->head_dim, eb = dtype_bytes(dims->dtype), R = (size_t)n * s_max;
+  std::vector<Buf> bufs = {{k_p, P * hkv * hd * eb, "k_p", true},
+                           {v_p, P * hkv * hd * eb, "v_p", true},
+                           {q_s, R * hq * hd * eb, "q_s", true},
+                           {k_s, R * hkv * hd * eb, "k_s", true},
+                           {v_s, R * hkv * hd * eb, "v_s", true},
+                           {o_s, R * hq * hd * eb, "o_s", true},
+                           {lse_s, R * hq * 4, "lse_s", true, 4},
+                           {do_s, R * hq * hd * eb, "do_s", true},
+                           {seq_lens, (size_t)n * 4, "seq_lens", true, 4},
+                           {dq_s, R * hq * hd * eb, "dq_s", true},
+                           {dk_s, R * hkv * hd * eb, "dk_s", true},
+                           {dv_s, R * hkv * hd * eb, "dv_s", true},
+                           {gk_cache, P * hkv * hd * 4, "gk_cache", true},
+                           {gv_cache, P * hkv * hd * 4, "gv_cache", true}};
+  if ((st = check_bufs(bufs)) != SPR_OK) return st;
+  const WsLayout w = ws_layout(SPR_OP_SUFFIX_BWD_PADDED, dims, n, s_max, 0);
+  if ((st = check_ws(w, ws, ws_bytes)) != SPR_OK) return st;
+  std::vector<Buf> all = bufs;
+  all.push_back({ws, w.total, "ws", false});
+  if ((st = check_aliasing({bufs[12], bufs[13], all.back()}, all)) != SPR_OK) return st;
+  int32_t* cu = at<int32_t>(ws, w.cu);
+  int32_t* lens_c = at<int32_t>(ws, w.lens_c);
+  void *pq = at<char>(ws, w.pq), *pk = at<char>(ws, w.pk), *pv = at<char>(ws, w.pv), *po = at<char>(ws, w.po);
+  void *pdo = at<char>(ws, w.pdo), *pdq = at<char>(ws, w.pdq), *pdk = at<char>(ws, w.pdk), *pdv = at<char>(ws, w.pdv);
+  float* plse = at<float>(ws, w.plse);
+  if ((st = hip_check(launch_seq_offsets(seq_lens, n, s_max, cu, lens_c, stream), "offsets")) != SPR_OK) return st;
+  const struct {
+    const void* src;
+    void* dst;
+    size_t row;
+  } in[] = {{q_s, pq, hq * hd * eb}, {k_s, pk, hkv * hd * eb}, {v_s, pv, hkv * hd * eb},
+            {o_s, po, hq * hd * eb}, {lse_s, plse, hq * 4},      {do_s, pdo, hq * hd * eb}};
+  for (const auto& x : in)
+    if ((st = hip_check(launch_rows_move(true, x.src, x.dst, cu, lens_c, n, s_max, x.row, stream), "gather")) !=
+        SPR_OK)
+      return st;
+  if ((st = spr_suffix_attn_bwd_accum(dims, k_p, v_p, pq, pk, pv, po, plse, pdo, cu, n, s_max, (int32_t)R, pdq,
+                                      pdk, pdv, gk_cache, gv_cache, at<char>(ws, w.inner), w.inner_bytes,
+                                      stream)) != SPR_OK)
+    return st;
+  const struct {
+    const void* src;
+    void* dst;
+    size_t row;
+  } out[] = {{pdq, dq_s, hq * hd * eb}, {pdk, dk_s, hkv * hd * eb}, {pdv, dv_s, hkv * hd * eb}};
+  for (const auto& x : out)
+    if ((st = hip_check(launch_rows_move(false, x.src, x.dst, cu, lens_c, n, s_max, x.row, stream), "scatter")) !=
+        SPR_OK)
+      return st;
   return ok();
 }
 

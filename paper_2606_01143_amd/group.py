@@ -34,16 +34,53 @@ _TORCH_DT = {"bf16": torch.bfloat16, "f32": torch.float32}
 OUTPUT_KEYS = ["o_p", "lse_p", "o_s", "lse_s", "dq_p", "dk_p", "dv_p", "dq_s", "dk_s", "dv_s"]
 
 
+def plan_suffix_waves(lens: Sequence[int], budget_tokens: int,
+                      layout: str = "packed") -> List[Tuple[int, int]]:
+    """Split the suffixes, in order, into microbatches ("suffix waves", paper
+    Sec. 4.2) whose token footprint stays within ``budget_tokens``: the sum of
+    the lengths for the packed layout, the count times the longest length
+    for the padded layout.  Greedy: each wave takes suffixes while the next
+    one still fits; a suffix larger than the budget gets a wave of its own.
+    Any split gives the same group gradients (Prop. 1), so the split only
+    trades memory for launch count."""
+    if layout not in ("packed", "padded"):
+        raise ValueError(f"unknown layout {layout!r}")
+    if budget_tokens < 1:
+        raise ValueError("budget_tokens must be >= 1")
+    waves, a = [], 0
+    n = len(lens)
+    while a < n:
+        b, tot, mx = a, 0, 0
+        while b < n:
+            t2, m2 = tot + lens[b], max(mx, lens[b])
+            cost = t2 if layout == "packed" else (b + 1 - a) * m2
+            if b > a and cost > budget_tokens:
+                break
+            tot, mx, b = t2, m2, b + 1
+        waves.append((a, b))
+        a = b
+    return waves
+
+
 class DeviceGroup:
     """Inputs, outputs, cache and workspace of one prompt group on one GPU.
 
     ``inp`` is a synthetic group (see ``synthetic.make_group``): float32
     arrays holding values exactly representable in the storage dtype.
+    ``layout="padded"`` runs Phase B through the batch-plus-padding calls:
+    each microbatch's suffixes are held as [n, longest, H, d] tensors (built
+    once per microbatch) and the padded outputs are kept per microbatch
+    (``gather_padded_outputs`` copies their valid rows into ``self.out``).
     """
 
     def __init__(self, inp: Dict, device="cuda:0", softmax_scale: float = 0.0,
                  deterministic: bool = False, dense: bool = True,
-                 microbatch_splits: Optional[Sequence[Sequence[Tuple[int, int]]]] = None):
+                 microbatch_splits: Optional[Sequence[Sequence[Tuple[int, int]]]] = None,
+                 layout: str = "packed"):
+        if layout not in ("packed", "padded"):
+            raise ValueError(f"unknown layout {layout!r}")
+        self.layout = layout
+        self._padded: Dict[Tuple[int, int], Dict[str, torch.Tensor]] = {}
         shp = inp["shape"]
         self.shape = shp
         self.device = torch.device(device)
@@ -100,6 +137,14 @@ class DeviceGroup:
             for a, b in mbs:
                 nmb, mx, tot = self._mb_sizes(a, b)
                 need_f = max(need_f, B.workspace_size(B.OP_SUFFIX_FWD, self.dims, nmb, mx, tot))
+        if layout == "padded":
+            for mbs in splits:
+                for a, b in mbs:
+                    nmb, mx, _ = self._mb_sizes(a, b)
+                    need = max(need, B.workspace_size(B.OP_SUFFIX_BWD_PADDED, self.dims, nmb, mx),
+                               B.workspace_size(B.OP_SUFFIX_FWD_PADDED, self.dims, nmb, mx))
+                    need_f = max(need_f, B.workspace_size(B.OP_SUFFIX_FWD_PADDED, self.dims, nmb, mx))
+            self.ws = torch.empty(max(need, 256), device=self.device, dtype=torch.uint8)
         self.ws_fwd = torch.empty(need_f, device=self.device, dtype=torch.uint8)
         self._side = None  # (Phase A stream, suffix forward stream), made on first use
 
@@ -120,9 +165,46 @@ class DeviceGroup:
         return self._cu_cache[key]
 
     def prepare(self, microbatches: Sequence[Tuple[int, int]]) -> None:
-        """Build the per-microbatch cu_seqlens tensors ahead of a timed run."""
+        """Build the per-microbatch cu_seqlens tensors (and, for the padded
+        layout, the padded tensors) ahead of a timed run."""
         for a, b in microbatches:
             self._mb_cu(a, b)
+            if self.layout == "padded":
+                self._mb_padded(a, b)
+
+    def _mb_padded(self, a: int, b: int) -> Dict[str, torch.Tensor]:
+        key = (a, b)
+        if key not in self._padded:
+            shp = self.shape
+            nmb, mx, _ = self._mb_sizes(a, b)
+            hq, hkv, d = shp.num_q_heads, shp.num_kv_heads, shp.head_dim
+
+            def pad(x, h):
+                y = torch.zeros(nmb, mx, h, d, device=self.device, dtype=self.dtype)
+                for i in range(a, b):
+                    y[i - a, :self.lens[i]] = x[self.cu_host[i]:self.cu_host[i + 1]]
+                return y
+
+            def empty(h, dtype=None):
+                return torch.empty(nmb, mx, h, d, device=self.device, dtype=dtype or self.dtype)
+
+            self._padded[key] = {
+                "q": pad(self.q_s, hq), "k": pad(self.k_s, hkv), "v": pad(self.v_s, hkv),
+                "do": pad(self.do_s, hq),
+                "lens": torch.tensor(self.lens[a:b], dtype=torch.int32, device=self.device),
+                "o": empty(hq), "lse": torch.empty(nmb, mx, hq, device=self.device, dtype=torch.float32),
+                "dq": empty(hq), "dk": empty(hkv), "dv": empty(hkv)}
+        return self._padded[key]
+
+    def gather_padded_outputs(self) -> None:
+        """Copy the valid rows of every padded microbatch output into the
+        packed ``self.out`` tensors."""
+        for (a, b), t in self._padded.items():
+            for i in range(a, b):
+                r0, r1, L = self.cu_host[i], self.cu_host[i + 1], self.lens[i]
+                for src, dst in (("o", "o_s"), ("lse", "lse_s"), ("dq", "dq_s"), ("dk", "dk_s"),
+                                 ("dv", "dv_s")):
+                    self.out[dst][r0:r1] = t[src][i - a, :L]
 
     # ------------------------------------------------------------------
     def run_schedule(self, microbatches: Optional[Sequence[Tuple[int, int]]] = None,
@@ -158,6 +240,11 @@ class DeviceGroup:
 
     def _suffix_fwd(self, a: int, b: int, ws, stream) -> None:
         nmb, mx, tot = self._mb_sizes(a, b)
+        if self.layout == "padded":
+            t = self._mb_padded(a, b)
+            B.suffix_attn_fwd_padded(self.dims, self.k_p, self.v_p, t["q"], t["k"], t["v"], t["lens"],
+                                     nmb, mx, t["o"], t["lse"], ws, stream)
+            return
         r0, r1 = self.cu_host[a], self.cu_host[b]
         o = self.out
         B.suffix_attn_fwd(self.dims, self.k_p, self.v_p, self.q_s[r0:r1], self.k_s[r0:r1],
@@ -166,6 +253,12 @@ class DeviceGroup:
 
     def _suffix_bwd(self, a: int, b: int, stream) -> None:
         nmb, mx, tot = self._mb_sizes(a, b)
+        if self.layout == "padded":
+            t = self._mb_padded(a, b)
+            B.suffix_attn_bwd_accum_padded(self.dims, self.k_p, self.v_p, t["q"], t["k"], t["v"], t["o"],
+                                           t["lse"], t["do"], t["lens"], nmb, mx, t["dq"], t["dk"],
+                                           t["dv"], self.gk, self.gv, self.ws, stream)
+            return
         r0, r1 = self.cu_host[a], self.cu_host[b]
         o = self.out
         B.suffix_attn_bwd_accum(self.dims, self.k_p, self.v_p, self.q_s[r0:r1], self.k_s[r0:r1],

@@ -182,3 +182,31 @@ def test_moe_accumulate_checks(lib):
         "SPR_ERR_ALIASING"
     # zero tokens: nothing to do, no launch
     assert B.STATUS[f(16, 2, 0, None, None, 1, None, _addr(3), None, 0, None)] == "SPR_OK"
+
+
+# ------------------------------------------------------ padded suffix layout
+def _fwd_padded(dims, n=2, s_max=10, lens=7, out=8, ws=20, ws_bytes=1 << 40):
+    args = [_addr(1), _addr(2), _addr(3), _addr(4), _addr(5)]
+    return B.lib().spr_suffix_attn_fwd_padded(ctypes.byref(dims), *args, _addr(lens) if lens else None, n, s_max,
+                                              _addr(out), _addr(9), _addr(ws) if ws else None, ws_bytes, None)
+
+
+def test_padded_validation(lib):
+    dims = _dims()
+    need = B.workspace_size(B.OP_SUFFIX_FWD_PADDED, dims, 2, 10)
+    assert B.STATUS[_fwd_padded(dims, n=0)] == "SPR_ERR_INVALID_ARG"
+    assert B.STATUS[_fwd_padded(dims, s_max=0)] == "SPR_ERR_INVALID_ARG"
+    assert B.STATUS[_fwd_padded(dims, lens=None)] == "SPR_ERR_INVALID_ARG"
+    assert B.STATUS[_fwd_padded(dims, ws_bytes=need - 1)] == "SPR_ERR_WORKSPACE"
+    assert B.STATUS[_fwd_padded(dims, out=3)] == "SPR_ERR_ALIASING"  # o_s on q_s
+    assert B.STATUS[_fwd_padded(dims, ws=1)] == "SPR_ERR_ALIASING"   # workspace on k_p
+
+
+def test_padded_workspace_holds_packed_copies_and_inner_workspace(lib):
+    dims = _dims(prefix_len=4096, num_q_heads=32, num_kv_heads=8)
+    n, s = 8, 512
+    fwd = B.workspace_size(B.OP_SUFFIX_FWD_PADDED, dims, n, s)
+    bwd = B.workspace_size(B.OP_SUFFIX_BWD_PADDED, dims, n, s)
+    rows = n * s
+    assert fwd >= B.workspace_size(B.OP_SUFFIX_FWD, dims, n, s, rows) + rows * (2 * 32 + 2 * 8) * 128 * 2
+    assert bwd >= B.workspace_size(B.OP_SUFFIX_BWD, dims, n, s, rows) + rows * (4 * 32 + 4 * 8) * 128 * 2

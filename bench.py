@@ -205,6 +205,8 @@ def main():
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--sweep", choices=["c3", "c4", "c5attn", "all"], default=None)
+    ap.add_argument("--layout", choices=["packed", "padded"], default="packed",
+                    help="suffix layout of Phase B (padded: batch-plus-padding calls)")
     ap.add_argument("--moe-aux", action="store_true",
                     help="time the MoE router aux-loss accounting instead (one JSON line)")
     args = ap.parse_args()
@@ -231,7 +233,8 @@ def main():
     shape = inp["shape"]
     n = shape.n
     mbs = [(i, i + 1) for i in range(n)] if args.policy == "per_suffix" else [(0, n)]
-    grp = DeviceGroup(inp, device="cuda:0", dense=not args.no_dense, microbatch_splits=[mbs])
+    grp = DeviceGroup(inp, device="cuda:0", dense=not args.no_dense, microbatch_splits=[mbs],
+                      layout=args.layout)
     grp.prepare(mbs)
     torch.cuda.synchronize()
 
@@ -283,7 +286,7 @@ def main():
                    "prefix_len": shape.prefix_len, "n_suffixes": n,
                    "suffix_lens": list(shape.suffix_lens) if len(set(shape.suffix_lens)) > 1
                    else shape.suffix_lens[0],
-                   "microbatching": args.policy},
+                   "microbatching": args.policy, "layout": args.layout},
         "pct_mfma_peak": round(100 * value / BF16_PEAK_TFLOPS, 2),
         "schedule_tflop_per_step": round(sched_flops / 1e12, 4),
         "kernel_ms_one_step": per_kernel,

@@ -202,35 +202,47 @@ __global__ __launch_bounds__(kAuxThreads) void seq_offsets_kernel(const int32_t*
   if (threadIdx.x == 0) cu[n] = run;
 }
 
-// packed[cu[i] + t] = padded[i, t] for t < lens_c[i]; V-sized units
-template <typename V>
-__global__ __launch_bounds__(kAuxThreads) void gather_rows_kernel(const V* __restrict__ src, V* __restrict__ dst,
-                                                                  const int32_t* __restrict__ cu,
-                                                                  const int32_t* __restrict__ lens_c, int s_max,
-                                                                  int units, long total) {
+// Several tensors' rows in one launch.  Tensor j moves row_units[j] units
+// of 16 bytes (wide[j]) or 4 bytes per row; thread idx takes one unit of one
+// padded row.  Gather: packed[cu[i] + t] = padded[i, t] for t < lens_c[i].
+// Scatter: padded[i, t] = packed[cu[i] + t], or zero for padding rows.
+struct RowMoves {
+  const void* src[kMaxRowMoves];
+  void* dst[kMaxRowMoves];
+  int units[kMaxRowMoves];
+  int wide[kMaxRowMoves];
+  int count, units_per_row;
+};
+
+__global__ __launch_bounds__(kAuxThreads) void rows_move_kernel(RowMoves m, const int32_t* __restrict__ cu,
+                                                                const int32_t* __restrict__ lens_c, int s_max,
+                                                                long total, int gather) {
   const long idx = (long)blockIdx.x * kAuxThreads + threadIdx.x;
   if (idx >= total) return;
-  const long pr = idx / units;
-  const int u = (int)(idx % units);
+  const long pr = idx / m.units_per_row;
+  int u = (int)(idx % m.units_per_row);
+  int j = 0;
+  while (u >= m.units[j]) {
+    u -= m.units[j];
+    ++j;
+  }
   const int i = (int)(pr / s_max), t = (int)(pr % s_max);
-  if (t < lens_c[i]) dst[((long)cu[i] + t) * units + u] = src[idx];
-}
-
-__device__ __forceinline__ float4 zero_unit(float4) { return make_float4(0.f, 0.f, 0.f, 0.f); }
-__device__ __forceinline__ float zero_unit(float) { return 0.f; }
-
-// padded[i, t] = packed[cu[i] + t] for t < lens_c[i], else zero
-template <typename V>
-__global__ __launch_bounds__(kAuxThreads) void scatter_rows_kernel(const V* __restrict__ src, V* __restrict__ dst,
-                                                                   const int32_t* __restrict__ cu,
-                                                                   const int32_t* __restrict__ lens_c,
-                                                                   int s_max, int units, long total) {
-  const long idx = (long)blockIdx.x * kAuxThreads + threadIdx.x;
-  if (idx >= total) return;
-  const long pr = idx / units;
-  const int u = (int)(idx % units);
-  const int i = (int)(pr / s_max), t = (int)(pr % s_max);
-  dst[idx] = t < lens_c[i] ? src[((long)cu[i] + t) * units + u] : zero_unit(V());
+  const bool valid = t < lens_c[i];
+  const long prow = valid ? (long)cu[i] + t : 0;
+  const long pad_off = pr * m.units[j] + u, pack_off = prow * m.units[j] + u;
+  if (m.wide[j]) {
+    if (gather) {
+      if (valid) ((float4*)m.dst[j])[pack_off] = ((const float4*)m.src[j])[pad_off];
+    } else {
+      ((float4*)m.dst[j])[pad_off] = valid ? ((const float4*)m.src[j])[pack_off] : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  } else {
+    if (gather) {
+      if (valid) ((float*)m.dst[j])[pack_off] = ((const float*)m.src[j])[pad_off];
+    } else {
+      ((float*)m.dst[j])[pad_off] = valid ? ((const float*)m.src[j])[pack_off] : 0.f;
+    }
+  }
 }
 
 hipError_t launch_seq_offsets(const int32_t* lens, int n, int s_max, int32_t* cu, int32_t* lens_c,
@@ -240,30 +252,34 @@ hipError_t launch_seq_offsets(const int32_t* lens, int n, int s_max, int32_t* cu
   return hipGetLastError();
 }
 
-hipError_t launch_rows_move(bool gather, const void* src, void* dst, const int32_t* cu, const int32_t* lens_c,
-                            int n, int s_max, size_t row_bytes, hipStream_t st) {
-  // 16-byte units when rows and pointers allow, else 4-byte units
-  const bool wide = row_bytes % 16 == 0 && ((uintptr_t)src & 15) == 0 && ((uintptr_t)dst & 15) == 0;
-  const int units = (int)(row_bytes / (wide ? 16 : 4));
-  const long total = (long)n * s_max * units;
+hipError_t launch_rows_move(bool gather, const RowMove* moves, int count, const int32_t* cu, const int32_t* lens_c,
+                            int n, int s_max, hipStream_t st) {
+  if (count < 1 || count > kMaxRowMoves) return hipErrorInvalidValue;
+  RowMoves m;
+  m.count = count;
+  m.units_per_row = 0;
+  for (int j = 0; j < count; ++j) {
+    const RowMove& x = moves[j];
+    // 16-byte units when rows and pointers allow, else 4-byte units
+    const bool wide = x.row_bytes % 16 == 0 && ((uintptr_t)x.src & 15) == 0 && ((uintptr_t)x.dst & 15) == 0;
+    m.src[j] = x.src;
+    m.dst[j] = x.dst;
+    m.wide[j] = wide ? 1 : 0;
+    m.units[j] = (int)(x.row_bytes / (wide ? 16 : 4));
+    m.units_per_row += m.units[j];
+  }
+  for (int j = count; j < kMaxRowMoves; ++j) {
+    m.src[j] = nullptr;
+    m.dst[j] = nullptr;
+    m.units[j] = 0;
+    m.wide[j] = 0;
+  }
+  const long total = (long)n * s_max * m.units_per_row;
   if (total == 0) return hipSuccess;
   const unsigned nb = (unsigned)((total + kAuxThreads - 1) / kAuxThreads);
   ProfileScope ps(gather ? "rows_gather" : "rows_scatter", st);
-  if (wide) {
-    if (gather)
-      hipLaunchKernelGGL(gather_rows_kernel<float4>, dim3(nb), dim3(kAuxThreads), 0, st, (const float4*)src,
-                         (float4*)dst, cu, lens_c, s_max, units, total);
-    else
-      hipLaunchKernelGGL(scatter_rows_kernel<float4>, dim3(nb), dim3(kAuxThreads), 0, st, (const float4*)src,
-                         (float4*)dst, cu, lens_c, s_max, units, total);
-  } else {
-    if (gather)
-      hipLaunchKernelGGL(gather_rows_kernel<float>, dim3(nb), dim3(kAuxThreads), 0, st, (const float*)src,
-                         (float*)dst, cu, lens_c, s_max, units, total);
-    else
-      hipLaunchKernelGGL(scatter_rows_kernel<float>, dim3(nb), dim3(kAuxThreads), 0, st, (const float*)src,
-                         (float*)dst, cu, lens_c, s_max, units, total);
-  }
+  hipLaunchKernelGGL(rows_move_kernel, dim3(nb), dim3(kAuxThreads), 0, st, m, cu, lens_c, s_max, total,
+                     gather ? 1 : 0);
   return hipGetLastError();
 }
 

@@ -81,8 +81,14 @@ hipError_t launch_accumulate(float* dst, const float* src, size_t n, hipStream_t
 // (padded -> packed) or scatter (packed -> padded, padding rows zeroed)
 hipError_t launch_seq_offsets(const int32_t* lens, int n, int s_max, int32_t* cu, int32_t* lens_c,
                               hipStream_t st);
-hipError_t launch_rows_move(bool gather, const void* src, void* dst, const int32_t* cu,
-                            const int32_t* lens_c, int n, int s_max, size_t row_bytes, hipStream_t st);
+constexpr int kMaxRowMoves = 6;
+struct RowMove {
+  const void* src;
+  void* dst;
+  size_t row_bytes;  // a multiple of 4
+};
+hipError_t launch_rows_move(bool gather, const RowMove* moves, int count, const int32_t* cu,
+                            const int32_t* lens_c, int n, int s_max, hipStream_t st);
 
 // MoE router aux-loss accounting (kernels_moe.hip).  Statistics layout:
 // int64 count[E], double mass[E], int64 total, int64 invalid.

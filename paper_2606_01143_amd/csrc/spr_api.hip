@@ -519,23 +519,13 @@ spr_status spr_suffix_attn_fwd_padded(const spr_dims* dims, const void* k_p, con
   void *pq = at<char>(ws, w.pq), *pk = at<char>(ws, w.pk), *pv = at<char>(ws, w.pv), *po = at<char>(ws, w.po);
   float* plse = at<float>(ws, w.plse);
   if ((st = hip_check(launch_seq_offsets(seq_lens, n, s_max, cu, lens_c, stream), "offsets")) != SPR_OK) return st;
-  const struct {
-    const void* src;
-    void* dst;
-    size_t row;
-  } in[] = {{q_s, pq, hq * hd * eb}, {k_s, pk, hkv * hd * eb}, {v_s, pv, hkv * hd * eb}};
-  for (const auto& x : in)
-    if ((st = hip_check(launch_rows_move(true, x.src, x.dst, cu, lens_c, n, s_max, x.row, stream), "gather")) !=
-        SPR_OK)
-      return st;
+  const RowMove in[] = {{q_s, pq, hq * hd * eb}, {k_s, pk, hkv * hd * eb}, {v_s, pv, hkv * hd * eb}};
+  if ((st = hip_check(launch_rows_move(true, in, 3, cu, lens_c, n, s_max, stream), "gather")) != SPR_OK) return st;
   if ((st = spr_suffix_attn_fwd(dims, k_p, v_p, pq, pk, pv, cu, n, s_max, (int32_t)R, po, plse,
                                 at<char>(ws, w.inner), w.inner_bytes, stream)) != SPR_OK)
     return st;
-  if ((st = hip_check(launch_rows_move(false, po, o_s, cu, lens_c, n, s_max, hq * hd * eb, stream), "scatter")) !=
-      SPR_OK)
-    return st;
-  if ((st = hip_check(launch_rows_move(false, plse, lse_s, cu, lens_c, n, s_max, hq * 4, stream), "scatter")) !=
-      SPR_OK)
+  const RowMove out[] = {{po, o_s, hq * hd * eb}, {plse, lse_s, hq * 4}};
+  if ((st = hip_check(launch_rows_move(false, out, 2, cu, lens_c, n, s_max, stream), "scatter")) != SPR_OK)
     return st;
   return ok();
 }
@@ -578,29 +568,16 @@ spr_status spr_suffix_attn_bwd_accum_padded(const spr_dims* dims, const void* k_
   void *pdo = at<char>(ws, w.pdo), *pdq = at<char>(ws, w.pdq), *pdk = at<char>(ws, w.pdk), *pdv = at<char>(ws, w.pdv);
   float* plse = at<float>(ws, w.plse);
   if ((st = hip_check(launch_seq_offsets(seq_lens, n, s_max, cu, lens_c, stream), "offsets")) != SPR_OK) return st;
-  const struct {
-    const void* src;
-    void* dst;
-    size_t row;
-  } in[] = {{q_s, pq, hq * hd * eb}, {k_s, pk, hkv * hd * eb}, {v_s, pv, hkv * hd * eb},
-            {o_s, po, hq * hd * eb}, {lse_s, plse, hq * 4},      {do_s, pdo, hq * hd * eb}};
-  for (const auto& x : in)
-    if ((st = hip_check(launch_rows_move(true, x.src, x.dst, cu, lens_c, n, s_max, x.row, stream), "gather")) !=
-        SPR_OK)
-      return st;
+  const RowMove in[] = {{q_s, pq, hq * hd * eb}, {k_s, pk, hkv * hd * eb}, {v_s, pv, hkv * hd * eb},
+                        {o_s, po, hq * hd * eb},  {lse_s, plse, hq * 4},      {do_s, pdo, hq * hd * eb}};
+  if ((st = hip_check(launch_rows_move(true, in, 6, cu, lens_c, n, s_max, stream), "gather")) != SPR_OK) return st;
   if ((st = spr_suffix_attn_bwd_accum(dims, k_p, v_p, pq, pk, pv, po, plse, pdo, cu, n, s_max, (int32_t)R, pdq,
                                       pdk, pdv, gk_cache, gv_cache, at<char>(ws, w.inner), w.inner_bytes,
                                       stream)) != SPR_OK)
     return st;
-  const struct {
-    const void* src;
-    void* dst;
-    size_t row;
-  } out[] = {{pdq, dq_s, hq * hd * eb}, {pdk, dk_s, hkv * hd * eb}, {pdv, dv_s, hkv * hd * eb}};
-  for (const auto& x : out)
-    if ((st = hip_check(launch_rows_move(false, x.src, x.dst, cu, lens_c, n, s_max, x.row, stream), "scatter")) !=
-        SPR_OK)
-      return st;
+  const RowMove out[] = {{pdq, dq_s, hq * hd * eb}, {pdk, dk_s, hkv * hd * eb}, {pdv, dv_s, hkv * hd * eb}};
+  if ((st = hip_check(launch_rows_move(false, out, 3, cu, lens_c, n, s_max, stream), "scatter")) != SPR_OK)
+    return st;
   return ok();
 }
 

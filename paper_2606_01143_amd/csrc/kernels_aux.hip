@@ -214,9 +214,39 @@ struct RowMoves {
   int count, units_per_row;
 };
 
-__global__ __launch_bounds__(kAuxThreads) void rows_move_kernel(RowMoves m, const int32_t* __restrict__ cu,
-                                                                const int32_t* __restrict__ lens_c, int s_max,
+// With few suffixes (n <= kLdsSeqs) each block derives the offsets itself
+// from the raw lengths (clamped as in seq_offsets_kernel), and block 0 of a
+// gather also stores them to cu_pre / lens_pre for the packed kernels that
+// follow, so no separate offsets launch is needed; otherwise cu / lens_c
+// come precomputed.
+constexpr int kLdsSeqs = 1024;
+__global__ __launch_bounds__(kAuxThreads) void rows_move_kernel(RowMoves m, const int32_t* __restrict__ lens,
+                                                                int n, const int32_t* __restrict__ cu_pre,
+                                                                const int32_t* __restrict__ lens_pre, int s_max,
                                                                 long total, int gather) {
+  __shared__ int32_t cu_s[kLdsSeqs + 1], len_s[kLdsSeqs];
+  const int32_t *cu = cu_pre, *lens_c = lens_pre;
+  if (lens != nullptr) {
+    for (int i = threadIdx.x; i < n; i += kAuxThreads) len_s[i] = min(max(lens[i], 0), s_max);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      int32_t run = 0;
+      for (int i = 0; i < n; ++i) {
+        cu_s[i] = run;
+        run += len_s[i];
+      }
+      cu_s[n] = run;
+    }
+    __syncthreads();
+    cu = cu_s;
+    lens_c = len_s;
+    if (gather && blockIdx.x == 0) {
+      int32_t* cu_out = const_cast<int32_t*>(cu_pre);
+      int32_t* len_out = const_cast<int32_t*>(lens_pre);
+      for (int i = threadIdx.x; i <= n; i += kAuxThreads) cu_out[i] = cu_s[i];
+      for (int i = threadIdx.x; i < n; i += kAuxThreads) len_out[i] = len_s[i];
+    }
+  }
   const long idx = (long)blockIdx.x * kAuxThreads + threadIdx.x;
   if (idx >= total) return;
   const long pr = idx / m.units_per_row;
@@ -252,8 +282,10 @@ hipError_t launch_seq_offsets(const int32_t* lens, int n, int s_max, int32_t* cu
   return hipGetLastError();
 }
 
-hipError_t launch_rows_move(bool gather, const RowMove* moves, int count, const int32_t* cu, const int32_t* lens_c,
-                            int n, int s_max, hipStream_t st) {
+bool rows_move_needs_offsets(int n) { return n > kLdsSeqs; }
+
+hipError_t launch_rows_move(bool gather, const RowMove* moves, int count, const int32_t* lens, const int32_t* cu,
+                            const int32_t* lens_c, int n, int s_max, hipStream_t st) {
   if (count < 1 || count > kMaxRowMoves) return hipErrorInvalidValue;
   RowMoves m;
   m.count = count;
@@ -278,8 +310,8 @@ hipError_t launch_rows_move(bool gather, const RowMove* moves, int count, const 
   if (total == 0) return hipSuccess;
   const unsigned nb = (unsigned)((total + kAuxThreads - 1) / kAuxThreads);
   ProfileScope ps(gather ? "rows_gather" : "rows_scatter", st);
-  hipLaunchKernelGGL(rows_move_kernel, dim3(nb), dim3(kAuxThreads), 0, st, m, cu, lens_c, s_max, total,
-                     gather ? 1 : 0);
+  hipLaunchKernelGGL(rows_move_kernel, dim3(nb), dim3(kAuxThreads), 0, st, m, n <= kLdsSeqs ? lens : nullptr, n,
+                     cu, lens_c, s_max, total, gather ? 1 : 0);
   return hipGetLastError();
 }
 

@@ -87,8 +87,11 @@ struct RowMove {
   void* dst;
   size_t row_bytes;  // a multiple of 4
 };
-hipError_t launch_rows_move(bool gather, const RowMove* moves, int count, const int32_t* cu,
-                            const int32_t* lens_c, int n, int s_max, hipStream_t st);
+// few suffixes: the move kernels derive the offsets from `lens` themselves;
+// many: cu / lens_c must come from launch_seq_offsets first
+bool rows_move_needs_offsets(int n);
+hipError_t launch_rows_move(bool gather, const RowMove* moves, int count, const int32_t* lens,
+                            const int32_t* cu, const int32_t* lens_c, int n, int s_max, hipStream_t st);
 
 // MoE router aux-loss accounting (kernels_moe.hip).  Statistics layout:
 // int64 count[E], double mass[E], int64 total, int64 invalid.

@@ -518,14 +518,18 @@ spr_status spr_suffix_attn_fwd_padded(const spr_dims* dims, const void* k_p, con
   int32_t* lens_c = at<int32_t>(ws, w.lens_c);
   void *pq = at<char>(ws, w.pq), *pk = at<char>(ws, w.pk), *pv = at<char>(ws, w.pv), *po = at<char>(ws, w.po);
   float* plse = at<float>(ws, w.plse);
-  if ((st = hip_check(launch_seq_offsets(seq_lens, n, s_max, cu, lens_c, stream), "offsets")) != SPR_OK) return st;
+  // the offsets in workspace, for the packed calls: written by the gather
+  // itself unless there are too many suffixes for it
+  if (rows_move_needs_offsets(n) &&
+      (st = hip_check(launch_seq_offsets(seq_lens, n, s_max, cu, lens_c, stream), "offsets")) != SPR_OK)
+    return st;
   const RowMove in[] = {{q_s, pq, hq * hd * eb}, {k_s, pk, hkv * hd * eb}, {v_s, pv, hkv * hd * eb}};
-  if ((st = hip_check(launch_rows_move(true, in, 3, cu, lens_c, n, s_max, stream), "gather")) != SPR_OK) return st;
+  if ((st = hip_check(launch_rows_move(true, in, 3, seq_lens, cu, lens_c, n, s_max, stream), "gather")) != SPR_OK) return st;
   if ((st = spr_suffix_attn_fwd(dims, k_p, v_p, pq, pk, pv, cu, n, s_max, (int32_t)R, po, plse,
                                 at<char>(ws, w.inner), w.inner_bytes, stream)) != SPR_OK)
     return st;
   const RowMove out[] = {{po, o_s, hq * hd * eb}, {plse, lse_s, hq * 4}};
-  if ((st = hip_check(launch_rows_move(false, out, 2, cu, lens_c, n, s_max, stream), "scatter")) != SPR_OK)
+  if ((st = hip_check(launch_rows_move(false, out, 2, seq_lens, cu, lens_c, n, s_max, stream), "scatter")) != SPR_OK)
     return st;
   return ok();
 }
@@ -567,16 +571,20 @@ spr_status spr_suffix_attn_bwd_accum_padded(const spr_dims* dims, const void* k_
   void *pq = at<char>(ws, w.pq), *pk = at<char>(ws, w.pk), *pv = at<char>(ws, w.pv), *po = at<char>(ws, w.po);
   void *pdo = at<char>(ws, w.pdo), *pdq = at<char>(ws, w.pdq), *pdk = at<char>(ws, w.pdk), *pdv = at<char>(ws, w.pdv);
   float* plse = at<float>(ws, w.plse);
-  if ((st = hip_check(launch_seq_offsets(seq_lens, n, s_max, cu, lens_c, stream), "offsets")) != SPR_OK) return st;
+  // the offsets in workspace, for the packed calls: written by the gather
+  // itself unless there are too many suffixes for it
+  if (rows_move_needs_offsets(n) &&
+      (st = hip_check(launch_seq_offsets(seq_lens, n, s_max, cu, lens_c, stream), "offsets")) != SPR_OK)
+    return st;
   const RowMove in[] = {{q_s, pq, hq * hd * eb}, {k_s, pk, hkv * hd * eb}, {v_s, pv, hkv * hd * eb},
                         {o_s, po, hq * hd * eb},  {lse_s, plse, hq * 4},      {do_s, pdo, hq * hd * eb}};
-  if ((st = hip_check(launch_rows_move(true, in, 6, cu, lens_c, n, s_max, stream), "gather")) != SPR_OK) return st;
+  if ((st = hip_check(launch_rows_move(true, in, 6, seq_lens, cu, lens_c, n, s_max, stream), "gather")) != SPR_OK) return st;
   if ((st = spr_suffix_attn_bwd_accum(dims, k_p, v_p, pq, pk, pv, po, plse, pdo, cu, n, s_max, (int32_t)R, pdq,
                                       pdk, pdv, gk_cache, gv_cache, at<char>(ws, w.inner), w.inner_bytes,
                                       stream)) != SPR_OK)
     return st;
   const RowMove out[] = {{pdq, dq_s, hq * hd * eb}, {pdk, dk_s, hkv * hd * eb}, {pdv, dv_s, hkv * hd * eb}};
-  if ((st = hip_check(launch_rows_move(false, out, 3, cu, lens_c, n, s_max, stream), "scatter")) != SPR_OK)
+  if ((st = hip_check(launch_rows_move(false, out, 3, seq_lens, cu, lens_c, n, s_max, stream), "scatter")) != SPR_OK)
     return st;
   return ok();
 }

@@ -12,10 +12,11 @@ def _announce(what):
     print(f"\n[gpu padded] {what}", flush=True)
 
 
-def _run_packed_and_padded(shape, seed):
+def _run_packed_and_padded(shape, seed, ragged=None):
     import torch
     from paper_2606_01143_amd import binding as B
-    inp = make_group(shape, seed=seed)
+    inp = make_group(shape, seed=seed, ragged=ragged)
+    shape = inp["shape"]
     dev = torch.device("cuda:0")
     dt = torch.bfloat16 if shape.dtype == "bf16" else torch.float32
     up = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(device=dev, dtype=dt)
@@ -82,6 +83,15 @@ CASES = [
 def test_padded_layout_is_bitwise_the_packed_layout(gpu, name, shape):
     _announce(f"{name} {shape}")
     _run_packed_and_padded(shape, seed=31)
+
+
+@pytest.mark.gpu
+def test_padded_layout_with_many_suffixes(gpu):
+    """1100 suffixes of 1..3 tokens: more than the gather derives offsets
+    for by itself, so the separate offsets launch runs."""
+    shape = GroupShape(2, 1, 64, 40, (0,) * 1100, "bf16")
+    _announce(f"many suffixes {shape}")
+    _run_packed_and_padded(shape, seed=41, ragged=(1, 3))
 
 
 @pytest.mark.gpu

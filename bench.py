@@ -207,6 +207,9 @@ def main():
     ap.add_argument("--sweep", choices=["c3", "c4", "c5attn", "all"], default=None)
     ap.add_argument("--layout", choices=["packed", "padded"], default="packed",
                     help="suffix layout of Phase B (padded: batch-plus-padding calls)")
+    ap.add_argument("--stack", action="store_true",
+                    help="Phase-B HBM with and without dormant-prefix offload over a layer stack")
+    ap.add_argument("--layers", type=int, default=32)
     ap.add_argument("--moe-aux", action="store_true",
                     help="time the MoE router aux-loss accounting instead (one JSON line)")
     args = ap.parse_args()
@@ -222,6 +225,9 @@ def main():
     B.lib()  # fails loudly without the HIP library
     if args.moe_aux:
         moe_aux_bench(args)
+        return
+    if args.stack:
+        stack_bench(args)
         return
     if args.sweep:
         names = sum(SWEEPS.values(), []) if args.sweep == "all" else SWEEPS[args.sweep]
@@ -350,6 +356,55 @@ def sweep_one(name: str, args):
     print(json.dumps(rec), flush=True)
     del grp
     torch.cuda.empty_cache()
+
+
+def stack_bench(args):
+    """Phase-B HBM with and without offloading the dormant prefix state (the
+    measurement of the paper's Table 6, Sec. 5.5): a stack of Llama3-8B
+    attention layers (GQA 32/8, d = 128), N = 16 suffixes, total length
+    12288 split between prefix and suffix.  One JSON line per split."""
+    import torch
+    from paper_2606_01143_amd.stack import StackedGroup, StackShape
+    L = args.layers
+    gib = float(1 << 30)
+    for P, S in ((2048, 10240), (6144, 6144), (8192, 4096), (10240, 2048)):
+        shape = StackShape(L, 32, 8, 128, P, (S,) * 16)
+        rec = {"workload": f"llama3_8b_attn_stack{L}_p{P}_s{S}_n16", "layers": L, "prefix_len": P,
+               "suffix_len": S, "n_suffixes": 16, "dtype": "bf16", "data": "synthetic"}
+        for offload in (False, True):
+            sg = StackedGroup(shape, seed=args.seed, offload=offload)
+            sg.run()  # warm: allocator pools, pinned pool, kernels
+            torch.cuda.synchronize()
+            marks = {}
+
+            def mark(name):
+                e = torch.cuda.Event(enable_timing=True)
+                e.record()
+                marks[name] = e
+                if name == "A":
+                    torch.cuda.reset_peak_memory_stats()
+                if name == "B":
+                    marks["peak_b"] = torch.cuda.max_memory_allocated()
+
+            start = torch.cuda.Event(enable_timing=True)
+            start.record()
+            sg.run(on_phase=mark)
+            torch.cuda.synchronize()
+            key = "offload" if offload else "no_offload"
+            rec[f"phase_b_peak_gib_{key}"] = round(marks["peak_b"] / gib, 3)
+            rec[f"step_ms_{key}"] = round(start.elapsed_time(marks["C"]), 2)
+            rec[f"phase_ms_{key}"] = {"A": round(start.elapsed_time(marks["A"]), 2),
+                                      "B": round(marks["A"].elapsed_time(marks["B"]), 2),
+                                      "C": round(marks["B"].elapsed_time(marks["C"]), 2)}
+            if offload:
+                rec["dormant_gib"] = round(sg.dormant_bytes / gib, 3)
+                rec["restores"] = {k: v for k, v in sg.stats.items()}
+            del sg
+            torch.cuda.empty_cache()
+        red = rec["phase_b_peak_gib_no_offload"] - rec["phase_b_peak_gib_offload"]
+        rec["reduction_gib"] = round(red, 3)
+        rec["reduction_pct"] = round(100 * red / rec["phase_b_peak_gib_no_offload"], 1)
+        print(json.dumps(rec), flush=True)
 
 
 def moe_aux_bench(args):

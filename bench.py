@@ -27,7 +27,9 @@ from the kernel sources in the tree (else null).
 Prints ONE JSON line.  ``--sweep c3|c4|c5attn|all`` instead prints one JSON
 line per configuration of the speedup surface (schedule vs dense, no CPU
 baseline); ``--moe-aux`` prints the MoE router aux-loss accounting line
-(App. B: reuse accounting against the materialized prefix copies).  ``--gpus N`` with N > 1 exits: this build runs on one GPU.
+(App. B: reuse accounting against the materialized prefix copies); ``--layer``
+the long-context decoder layer through the schedule against the dense
+layer; ``--stack`` the Phase-B HBM with and without dormant-prefix offload.  ``--gpus N`` with N > 1 exits: this build runs on one GPU.
 """
 from __future__ import annotations
 
@@ -211,6 +213,8 @@ def main():
     ap.add_argument("--sweep", choices=["c3", "c4", "c5attn", "all"], default=None)
     ap.add_argument("--layout", choices=["packed", "padded"], default="packed",
                     help="suffix layout of Phase B (padded: batch-plus-padding calls)")
+    ap.add_argument("--layer", action="store_true",
+                    help="a long-context Llama3-8B decoder layer through the schedule vs dense")
     ap.add_argument("--stack", action="store_true",
                     help="Phase-B HBM with and without dormant-prefix offload over a layer stack")
     ap.add_argument("--layers", type=int, default=32)
@@ -232,6 +236,9 @@ def main():
         return
     if args.stack:
         stack_bench(args)
+        return
+    if args.layer:
+        layer_bench(args)
         return
     if args.sweep:
         names = sum(SWEEPS.values(), []) if args.sweep == "all" else SWEEPS[args.sweep]
@@ -387,6 +394,44 @@ def sweep_one(name: str, args):
     print(json.dumps(rec), flush=True)
     del grp
     torch.cuda.empty_cache()
+
+
+def layer_bench(args):
+    """A long-context Llama3-8B decoder layer (hidden 4096, GQA 32/8, d 128,
+    RoPE theta 5e5, SwiGLU 14336, RMSNorm; weights N(0, 0.02)) over a group
+    with P = 28672 and N = 8 suffixes of 128: the three-phase schedule
+    against the dense per-trajectory layer, forward and backward with weight
+    gradients.  One JSON line."""
+    import torch
+    from paper_2606_01143_amd.layer import DecoderLayer
+    from synthetic.layer import LAYER_SHAPES, make_layer_group
+    name = "llama3_8b_layer_p28672_n8_s128"
+    shp = LAYER_SHAPES[name]
+    layer = DecoderLayer(make_layer_group(shp, seed=args.seed))
+    steps, warm = max(1, min(args.steps, 5)), max(1, min(args.warmup, 2))
+    ms = time_steps(layer.run_schedule, steps, warm)
+    ms_dense = time_steps(layer.run_dense, max(1, steps // 2), 1)
+    P, S, n = shp.prefix_len, shp.suffix_lens[0], shp.n
+    per_tok = 2 * (shp.hidden * (shp.num_q_heads + 2 * shp.num_kv_heads) * shp.head_dim
+                   + shp.num_q_heads * shp.head_dim * shp.hidden + 3 * shp.hidden * shp.intermediate)
+    gemm = 3 * per_tok  # forward, input gradient, weight gradient
+    d, hq = shp.head_dim, shp.num_q_heads
+    pairs_sched = P * (P + 1) // 2 + n * (S * P + S * (S + 1) // 2)
+    pairs_dense = n * (P + S) * (P + S + 1) // 2
+    flop = gemm * (P + n * S) + 14 * d * hq * pairs_sched
+    flop_dense = gemm * n * (P + S) + 14 * d * hq * pairs_dense
+    out = {"metric": "decoder layer fwd+bwd through the schedule, useful TFLOP/s + speedup vs dense",
+           "value": round(flop / (ms * 1e-3) / 1e12, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": steps,
+           "warmup": warm, "ms_per_step": round(ms, 2), "higher_is_better": True, "dtype": "bf16",
+           "data": "synthetic", "config": {"workload": name, "hidden": shp.hidden, "num_q_heads": hq,
+                                           "num_kv_heads": shp.num_kv_heads, "head_dim": d,
+                                           "intermediate": shp.intermediate, "prefix_len": P,
+                                           "n_suffixes": n, "suffix_len": S},
+           "dense_ms_per_step": round(ms_dense, 2), "speedup_vs_dense": round(ms_dense / ms, 3),
+           "flop_ratio_dense_over_schedule": round(flop_dense / flop, 3),
+           "schedule_tflop_per_step": round(flop / 1e12, 2),
+           "dense_equiv_tflops": round(flop_dense / (ms_dense * 1e-3) / 1e12, 2)}
+    print(json.dumps(out), flush=True)
 
 
 def stack_bench(args):

@@ -11,7 +11,7 @@ from __future__ import annotations
 
 import ctypes
 import os
-from ctypes import POINTER, byref, c_char_p, c_double, c_float, c_int32, c_size_t, c_uint32, c_void_p
+from ctypes import POINTER, byref, c_char_p, c_double, c_float, c_int32, c_int64, c_size_t, c_uint32, c_void_p
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "lib", "libspr.so")
 
@@ -52,6 +52,12 @@ _SIGNATURES = {
     "spr_workspace_size": ([c_int32, _P, c_int32, c_int32, c_int32, POINTER(c_size_t)], c_int32),
     "spr_gkv_cache_zero": ([_P, _P, _P, _P], c_int32),
     "spr_gkv_accumulate": ([_P, _P, _P, _P, _P, _P], c_int32),
+    "spr_rmsnorm_fwd": ([c_int32, c_int32, c_float, _P, _P, _P, _P], c_int32),
+    "spr_rmsnorm_bwd": ([c_int32, c_int32, _P, _P, _P, _P, _P, _P], c_int32),
+    "spr_rope_fwd": ([c_int32, c_int32, c_int32, c_int32, c_double, _P, _P, _P], c_int32),
+    "spr_rope_bwd": ([c_int32, c_int32, c_int32, c_int32, c_double, _P, _P, _P], c_int32),
+    "spr_swiglu_fwd": ([c_int64, _P, _P, _P, _P], c_int32),
+    "spr_swiglu_bwd": ([c_int64, _P, _P, _P, _P, _P, _P], c_int32),
     "spr_moe_stats_bytes": ([c_int32, POINTER(c_size_t)], c_int32),
     "spr_moe_stats_zero": ([c_int32, _P, _P], c_int32),
     "spr_moe_aux_workspace_size": ([c_int32, c_int32, POINTER(c_size_t)], c_int32),
@@ -212,6 +218,36 @@ def dense_recompute_baseline(dims, q_p, k_p, v_p, do_p_seq, q_s, k_s, v_s, do_s,
         _ptr(v_s), _ptr(do_s), _ptr(cu_seqlens), n, max_len, total_len, _ptr(o_p), _ptr(lse_p),
         _ptr(o_s), _ptr(lse_s), _ptr(dq_s), _ptr(dk_s), _ptr(dv_s), _ptr(dq_p), _ptr(dk_p),
         _ptr(dv_p), _ptr(ws), _nbytes(ws), _stream(stream)))
+
+
+def rmsnorm_fwd(x, y, rstd, eps=1e-5, stream=None):
+    rows, width = int(x.shape[0]), int(x.shape[-1])
+    _check(lib().spr_rmsnorm_fwd(rows, width, eps, _ptr(x), _ptr(y), _ptr(rstd), _stream(stream)))
+
+
+def rmsnorm_bwd(x, rstd, dy, dx, add=None, stream=None):
+    rows, width = int(x.shape[0]), int(x.shape[-1])
+    _check(lib().spr_rmsnorm_bwd(rows, width, _ptr(x), _ptr(rstd), _ptr(dy), _ptr(add), _ptr(dx),
+                                 _stream(stream)))
+
+
+def rope_fwd(x, y, pos0, theta, stream=None):
+    t, h, d = (int(v) for v in x.shape)
+    _check(lib().spr_rope_fwd(t, h, d, pos0, float(theta), _ptr(x), _ptr(y), _stream(stream)))
+
+
+def rope_bwd(dy, dx, pos0, theta, stream=None):
+    t, h, d = (int(v) for v in dy.shape)
+    _check(lib().spr_rope_bwd(t, h, d, pos0, float(theta), _ptr(dy), _ptr(dx), _stream(stream)))
+
+
+def swiglu_fwd(g, u, m, stream=None):
+    _check(lib().spr_swiglu_fwd(int(g.numel()), _ptr(g), _ptr(u), _ptr(m), _stream(stream)))
+
+
+def swiglu_bwd(g, u, dm, dg, du, stream=None):
+    _check(lib().spr_swiglu_bwd(int(g.numel()), _ptr(g), _ptr(u), _ptr(dm), _ptr(dg), _ptr(du),
+                                _stream(stream)))
 
 
 def moe_stats_bytes(n_experts: int) -> int:

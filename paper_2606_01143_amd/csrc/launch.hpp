@@ -93,6 +93,17 @@ bool rows_move_needs_offsets(int n);
 hipError_t launch_rows_move(bool gather, const RowMove* moves, int count, const int32_t* lens,
                             const int32_t* cu, const int32_t* lens_c, int n, int s_max, hipStream_t st);
 
+// decoder-layer token-wise operations (kernels_layer.hip)
+hipError_t launch_rmsnorm_fwd(int rows, int width, float eps, const void* x, void* y, float* rstd,
+                              hipStream_t st);
+hipError_t launch_rmsnorm_bwd(int rows, int width, const void* x, const float* rstd, const void* dy,
+                              const void* add, void* dx, hipStream_t st);
+hipError_t launch_rope(int tokens, int heads, int d, int pos0, double theta, const void* x, void* y,
+                       bool inverse, hipStream_t st);
+hipError_t launch_swiglu_fwd(long n, const void* g, const void* u, void* m, hipStream_t st);
+hipError_t launch_swiglu_bwd(long n, const void* g, const void* u, const void* dm, void* dg, void* du,
+                             hipStream_t st);
+
 // MoE router aux-loss accounting (kernels_moe.hip).  Statistics layout:
 // int64 count[E], double mass[E], int64 total, int64 invalid.
 int moe_blocks(int n_tokens);

@@ -14,6 +14,7 @@
 
 #include "../../include/spr.h"
 #include "../../include/spr_moe.h"
+#include "../../include/spr_layer.h"
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -814,6 +815,100 @@ spr_status spr_gkv_accumulate(const spr_dims* dims, float* gk_cache, float* gv_c
     return st;
   if ((st = hip_check(launch_accumulate(gv_cache, dgv, n, stream), "cache accumulate")) != SPR_OK)
     return st;
+  return ok();
+}
+
+// ------------------------------------------------ decoder-layer token ops
+namespace {
+spr_status check_rows(int32_t rows, int32_t width) {
+  if (rows < 0) return fail(SPR_ERR_INVALID_ARG, "rows must be >= 0");
+  if (width < 8 || width % 8 != 0 || width > 16384)
+    return fail(SPR_ERR_UNSUPPORTED, "width must be a multiple of 8 in [8, 16384]");
+  return SPR_OK;
+}
+spr_status check_rope(int32_t tokens, int32_t heads, int32_t d, int32_t pos0, double theta) {
+  if (tokens < 0 || heads < 1 || pos0 < 0) return fail(SPR_ERR_INVALID_ARG, "tokens/pos0 >= 0, heads >= 1");
+  if (d < 2 || d % 2 != 0 || d > 256) return fail(SPR_ERR_UNSUPPORTED, "head_dim must be even, at most 256");
+  if (!(theta > 1.0) || !isfinite(theta)) return fail(SPR_ERR_INVALID_ARG, "theta must be finite and > 1");
+  return SPR_OK;
+}
+}  // namespace
+
+spr_status spr_rmsnorm_fwd(int32_t rows, int32_t width, float eps, const void* x, void* y, float* rstd,
+                           hipStream_t stream) {
+  spr_status st = check_rows(rows, width);
+  if (st != SPR_OK) return st;
+  if (!(eps >= 0.f) || isinf(eps)) return fail(SPR_ERR_INVALID_ARG, "eps must be finite and >= 0");
+  const size_t n = (size_t)rows * width * 2;
+  std::vector<Buf> bufs = {{x, n, "x", true}, {y, n, "y", true}, {rstd, (size_t)rows * 4, "rstd", true, 4}};
+  if ((st = check_bufs(bufs)) != SPR_OK) return st;
+  if ((st = check_aliasing({bufs[2]}, bufs)) != SPR_OK) return st;
+  if ((st = hip_check(launch_rmsnorm_fwd(rows, width, eps, x, y, rstd, stream), "rmsnorm")) != SPR_OK) return st;
+  return ok();
+}
+
+spr_status spr_rmsnorm_bwd(int32_t rows, int32_t width, const void* x, const float* rstd, const void* dy,
+                           const void* add, void* dx, hipStream_t stream) {
+  spr_status st = check_rows(rows, width);
+  if (st != SPR_OK) return st;
+  const size_t n = (size_t)rows * width * 2;
+  std::vector<Buf> bufs = {{x, n, "x", true}, {rstd, (size_t)rows * 4, "rstd", true, 4}, {dy, n, "dy", true},
+                           {add, n, "add", false}, {dx, n, "dx", true}};
+  if ((st = check_bufs(bufs)) != SPR_OK) return st;
+  if ((st = check_aliasing({bufs[4]}, {bufs[0], bufs[1], bufs[2]})) != SPR_OK) return st;
+  if ((st = hip_check(launch_rmsnorm_bwd(rows, width, x, rstd, dy, add, dx, stream), "rmsnorm bwd")) != SPR_OK)
+    return st;
+  return ok();
+}
+
+spr_status spr_rope_fwd(int32_t tokens, int32_t heads, int32_t head_dim, int32_t pos0, double theta,
+                        const void* x, void* y, hipStream_t stream) {
+  spr_status st = check_rope(tokens, heads, head_dim, pos0, theta);
+  if (st != SPR_OK) return st;
+  const size_t n = (size_t)tokens * heads * head_dim * 2;
+  std::vector<Buf> bufs = {{x, n, "x", true}, {y, n, "y", true}};
+  if ((st = check_bufs(bufs)) != SPR_OK) return st;
+  if (x != y && (st = check_aliasing({bufs[1]}, bufs)) != SPR_OK) return st;
+  if ((st = hip_check(launch_rope(tokens, heads, head_dim, pos0, theta, x, y, false, stream), "rope")) != SPR_OK)
+    return st;
+  return ok();
+}
+
+spr_status spr_rope_bwd(int32_t tokens, int32_t heads, int32_t head_dim, int32_t pos0, double theta,
+                        const void* dy, void* dx, hipStream_t stream) {
+  spr_status st = check_rope(tokens, heads, head_dim, pos0, theta);
+  if (st != SPR_OK) return st;
+  const size_t n = (size_t)tokens * heads * head_dim * 2;
+  std::vector<Buf> bufs = {{dy, n, "dy", true}, {dx, n, "dx", true}};
+  if ((st = check_bufs(bufs)) != SPR_OK) return st;
+  if (dy != dx && (st = check_aliasing({bufs[1]}, bufs)) != SPR_OK) return st;
+  if ((st = hip_check(launch_rope(tokens, heads, head_dim, pos0, theta, dy, dx, true, stream), "rope bwd")) !=
+      SPR_OK)
+    return st;
+  return ok();
+}
+
+spr_status spr_swiglu_fwd(int64_t n, const void* g, const void* u, void* m, hipStream_t stream) {
+  if (n < 0 || n % 8 != 0) return fail(SPR_ERR_INVALID_ARG, "n must be a non-negative multiple of 8");
+  const size_t b = (size_t)n * 2;
+  std::vector<Buf> bufs = {{g, b, "g", true}, {u, b, "u", true}, {m, b, "m", true}};
+  spr_status st;
+  if ((st = check_bufs(bufs)) != SPR_OK) return st;
+  if ((st = check_aliasing({bufs[2]}, bufs)) != SPR_OK) return st;
+  if ((st = hip_check(launch_swiglu_fwd(n, g, u, m, stream), "swiglu")) != SPR_OK) return st;
+  return ok();
+}
+
+spr_status spr_swiglu_bwd(int64_t n, const void* g, const void* u, const void* dm, void* dg, void* du,
+                          hipStream_t stream) {
+  if (n < 0 || n % 8 != 0) return fail(SPR_ERR_INVALID_ARG, "n must be a non-negative multiple of 8");
+  const size_t b = (size_t)n * 2;
+  std::vector<Buf> bufs = {{g, b, "g", true}, {u, b, "u", true}, {dm, b, "dm", true}, {dg, b, "dg", true},
+                           {du, b, "du", true}};
+  spr_status st;
+  if ((st = check_bufs(bufs)) != SPR_OK) return st;
+  if ((st = check_aliasing({bufs[3], bufs[4]}, bufs)) != SPR_OK) return st;
+  if ((st = hip_check(launch_swiglu_bwd(n, g, u, dm, dg, du, stream), "swiglu bwd")) != SPR_OK) return st;
   return ok();
 }
 

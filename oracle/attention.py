@@ -103,6 +103,39 @@ def causal_attention(q, k, v, do, scale, *, first_query_pos=0):
     return o, lse, dq, dk, dv
 
 
+def sampled_rows_reference(inp: Dict[str, np.ndarray], prefix_rows, suffix_rows,
+                           scale: Optional[float] = None) -> Dict[str, Dict]:
+    """O, LSE and dQ of a few query rows of a group, each from its own
+    sequence's definition (Sec. 2.1: trajectory i is [P||S(i)], causal).
+
+    prefix_rows: prefix positions r; a prefix row sees prefix keys 0..r in
+    every trajectory, so O and LSE are the same for all i and the group's
+    dQ is the sum over the trajectories of each one's dQ with dO_P(i).
+    suffix_rows: pairs (i, t), row t of suffix i, seeing all prefix keys and
+    keys 0..t of its own suffix.  For groups too large for the full oracle:
+    each row costs one row of attention."""
+    shp = inp["shape"]
+    sc = _default_scale(shp.head_dim, scale)
+    P, cu = shp.prefix_len, inp["cu_seqlens"]
+    out = {"prefix": {}, "suffix": {}}
+    for r in prefix_rows:
+        kk, vv = inp["k_p"][:r + 1], inp["v_p"][:r + 1]
+        dq = 0.0
+        for i in range(shp.n):
+            o, lse, dqi, _, _ = causal_attention(inp["q_p"][r:r + 1], kk, vv, inp["do_p"][i][r:r + 1], sc,
+                                                 first_query_pos=r)
+            dq = dq + dqi
+        out["prefix"][r] = {"o": o[0], "lse": lse[:, 0], "dq": dq[0]}
+    for i, t in suffix_rows:
+        a = int(cu[i])
+        kk = np.concatenate([inp["k_p"], inp["k_s"][a:a + t + 1]], axis=0)
+        vv = np.concatenate([inp["v_p"], inp["v_s"][a:a + t + 1]], axis=0)
+        o, lse, dq, _, _ = causal_attention(inp["q_s"][a + t:a + t + 1], kk, vv, inp["do_s"][a + t:a + t + 1], sc,
+                                            first_query_pos=P + t)
+        out["suffix"][(i, t)] = {"o": o[0], "lse": lse[:, 0], "dq": dq[0]}
+    return out
+
+
 def _default_scale(d: int, scale: Optional[float]) -> float:
     return 1.0 / np.sqrt(d) if not scale else float(scale)
 

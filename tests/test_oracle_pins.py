@@ -321,3 +321,21 @@ def test_planted_mistakes_are_caught(monkeypatch, mutation):
     one = make_group(GroupShape(4, 2, 4, 5, (3,), "f32"), seed=29)
     caught.append(pin_sdpa_n1(one) > 1e-6)
     assert any(caught), f"mutation {mutation} escaped every pin"
+
+
+def test_sampled_rows_equal_full_oracle_rows():
+    """The per-row reference used at full size equals the full oracle's rows."""
+    from oracle.attention import sampled_rows_reference
+    inp = make_group(GroupShape(4, 2, 16, 20, (5, 9), "f32"), seed=2)
+    ref = dense_group_reference(inp)
+    smp = sampled_rows_reference(inp, [0, 7, 19], [(0, 0), (1, 8), (1, 3)])
+    for r, v in smp["prefix"].items():
+        assert np.abs(v["o"] - ref["o_p"][r]).max() < 1e-12
+        assert np.abs(v["dq"] - ref["dq_p"][r]).max() < 1e-12
+        assert np.abs(v["lse"] - ref["lse_p"][:, r]).max() < 1e-12
+    cu = inp["cu_seqlens"]
+    for (i, t), v in smp["suffix"].items():
+        row = cu[i] + t
+        assert np.abs(v["o"] - ref["o_s"][row]).max() < 1e-12
+        assert np.abs(v["dq"] - ref["dq_s"][row]).max() < 1e-12
+        assert np.abs(v["lse"] - ref["lse_s"][:, row]).max() < 1e-12

@@ -4,9 +4,9 @@ One step = the whole three-phase schedule over one prompt group with inputs
 already resident in HBM: zero the gK/gV cache, Phase A prefix forward, Phase
 B suffix forward + backward-with-cache-accumulation for every suffix
 microbatch (one suffix per microbatch, the paper's timing choice), Phase C
-prefix backward.  Phase A and the suffix forwards run on side streams
-beside the in-order backwards (``DeviceGroup.run_schedule``); the per-phase
-times come from one extra step in serial order.  The dense-recompute baseline (full causal fwd+bwd over
+prefix backward.  The suffix forwards run on a side stream beside the
+in-order backwards (``DeviceGroup.run_schedule``); the per-phase times come
+from one extra step in serial order.  The dense-recompute baseline (full causal fwd+bwd over
 every [P||S(i)], one sequence at a time) is timed the same way on the same
 GPU for the speedup.
 

@@ -10,16 +10,17 @@ microbatch is a contiguous run of the packed suffixes; packed layout of
 Sec. 4.2), Phase C ``prefix_bwd`` once.  ``run_dense`` is the comparison:
 ``dense_recompute_baseline`` over every [P||S(i)].
 
-Streams: Phase A and the Phase B suffix forwards read only inputs, so by
-default they run on two side streams while the backward launches run in
-order on the caller's stream.  Phase A starts once the first suffix forward
-is done (only Phase C needs it, and the first backward should not wait for
-it).  A suffix backward waits for its own forward, Phase C waits for Phase
-A and for every suffix backward (their
-gK/gV cache updates stay in microbatch order), and the caller's stream
-waits for all of it.  The work items are the same launches with the same
-arguments, so the results are identical to the serial order; the overlap
-only fills the idle compute units at the tail of each launch.
+Streams: the Phase B suffix forwards read only inputs, so by default they
+run in order on a side stream while the backwards run in order on the
+caller's stream.  A suffix backward waits for its own forward.  Phase A and
+Phase C run on the caller's stream after the last backward; the gK/gV
+cache updates therefore stay in microbatch order.  The work items are the
+same launches with the same arguments, so the results are identical to the
+serial order.  The overlap only fills the idle compute units at the tail of
+each launch.  Phase A stays off the side stream: beside the backwards it
+competes for the L2 their row-tile order relies on.  Measured, that made
+the step up to 3% slower than the serial order at long prefixes, and never
+faster than running Phase A just before Phase C.
 """
 from __future__ import annotations
 
@@ -146,7 +147,7 @@ class DeviceGroup:
                     need_f = max(need_f, B.workspace_size(B.OP_SUFFIX_FWD_PADDED, self.dims, nmb, mx))
             self.ws = torch.empty(max(need, 256), device=self.device, dtype=torch.uint8)
         self.ws_fwd = torch.empty(need_f, device=self.device, dtype=torch.uint8)
-        self._side = None  # (Phase A stream, suffix forward stream), made on first use
+        self._side = None  # suffix forward stream, made on first use
 
     # ------------------------------------------------------------------
     def default_microbatches(self) -> List[Tuple[int, int]]:
@@ -211,8 +212,8 @@ class DeviceGroup:
                      use_gy: bool = True, stream=None, mark=None, overlap: bool = True) -> None:
         """Three-phase schedule; results land in ``self.out``, ``self.gk``, ``self.gv``.
 
-        ``overlap`` runs Phase A and the suffix forwards on side streams (see
-        the module docstring); ``overlap=False`` issues every launch in
+        ``overlap`` runs the suffix forwards on a side stream (see the
+        module docstring); ``overlap=False`` issues every launch in
         order on ``stream``.  ``mark(name)``, if given, is called after each
         phase's launches are issued ("zero", "A", "B_fwd", "B_bwd" per
         microbatch, "C"), e.g. to record events for per-phase times; it
@@ -276,15 +277,15 @@ class DeviceGroup:
     def _run_overlapped(self, mbs, use_gy: bool, stream) -> None:
         main = stream if stream is not None else torch.cuda.current_stream(self.device)
         if self._side is None:
-            # default priority: the side streams only fill idle compute units
-            self._side = (torch.cuda.Stream(self.device), torch.cuda.Stream(self.device))
-        s_a, s_f = self._side
+            # default priority: the side stream only fills idle compute units
+            self._side = torch.cuda.Stream(self.device)
+        s_f = self._side
         with torch.cuda.stream(main):
             self.prepare(mbs)  # any cu_seqlens upload is ordered before `start`
         start = torch.cuda.Event()
         start.record(main)
         B.gkv_cache_zero(self.dims, self.gk, self.gv, main)
-        # suffix forwards in order on one side stream, one event each
+        # suffix forwards in order on the side stream, one event each
         s_f.wait_event(start)
         fwd_done = []
         for a, b in mbs:
@@ -292,18 +293,13 @@ class DeviceGroup:
             e = torch.cuda.Event()
             e.record(s_f)
             fwd_done.append(e)
-        # Phase A on the other side stream, after the first suffix forward so
-        # that the first backward is not held up: only Phase C reads it
-        s_a.wait_event(fwd_done[0] if fwd_done else start)
-        o = self.out
-        B.prefix_fwd(self.dims, self.q_p, self.k_p, self.v_p, o["o_p"], o["lse_p"], s_a)
-        done_a = torch.cuda.Event()
-        done_a.record(s_a)
         # backwards in microbatch order on the caller's stream
         for (a, b), e in zip(mbs, fwd_done):
             main.wait_event(e)
             self._suffix_bwd(a, b, main)
-        main.wait_event(done_a)
+        # Phase A, then Phase C (only Phase C reads Phase A's outputs)
+        o = self.out
+        B.prefix_fwd(self.dims, self.q_p, self.k_p, self.v_p, o["o_p"], o["lse_p"], main)
         self._prefix_bwd(use_gy, main)
 
     def run_dense(self, use_dop: bool = True, stream=None) -> None:

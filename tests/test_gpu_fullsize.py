@@ -22,6 +22,8 @@ CASES = [
     ("qwen3_8b_p16384_n16_kvgroup", GroupShape(4, 1, 128, 16384, (1024,) * 16, "bf16"), None),
     ("llama3_8b_p28672_n8_s128_kvgroup", GroupShape(4, 1, 128, 28672, (128,) * 8, "bf16"), None),
     ("qwen3_moe_p8192_n16_ragged_kvgroup", GroupShape(8, 1, 128, 8192, (0,) * 16, "bf16"), (128, 2048)),
+    # the longest prefix tested: 128k tokens, two ragged suffixes
+    ("longest_prefix_p131072_n2_kvgroup", GroupShape(4, 1, 128, 131072, (1000, 37), "bf16"), None),
 ]
 
 

@@ -29,7 +29,9 @@ line per configuration of the speedup surface (schedule vs dense, no CPU
 baseline); ``--moe-aux`` prints the MoE router aux-loss accounting line
 (App. B: reuse accounting against the materialized prefix copies); ``--layer``
 the long-context decoder layer through the schedule against the dense
-layer; ``--stack`` the Phase-B HBM with and without dormant-prefix offload.  ``--gpus N`` with N > 1 exits: this build runs on one GPU.
+layer; ``--stack`` the Phase-B HBM with and without dormant-prefix offload;
+``--shard`` one GPU's kv-head share of the Qwen3-8B sweep groups.
+``--gpus N`` with N > 1 exits: the path runs on one GPU.
 """
 from __future__ import annotations
 
@@ -218,12 +220,15 @@ def main():
     ap.add_argument("--stack", action="store_true",
                     help="Phase-B HBM with and without dormant-prefix offload over a layer stack")
     ap.add_argument("--layers", type=int, default=32)
+    ap.add_argument("--shard", action="store_true",
+                    help="the Qwen3-8B sweep kernels on one GPU's kv-head share (Hkv = 8/g, g = 1, 2, 4, 8)")
     ap.add_argument("--moe-aux", action="store_true",
                     help="time the MoE router aux-loss accounting instead (one JSON line)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (--gpus {args.gpus} requested); the multi-GPU "
-              "sharding of this path is described in DESIGN.md but not built.", file=sys.stderr)
+              "sharding of this path (by kv head, or by suffix with one cache reduce) is not built.",
+              file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -239,6 +244,9 @@ def main():
         return
     if args.layer:
         layer_bench(args)
+        return
+    if args.shard:
+        shard_bench(args)
         return
     if args.sweep:
         names = sum(SWEEPS.values(), []) if args.sweep == "all" else SWEEPS[args.sweep]
@@ -394,6 +402,44 @@ def sweep_one(name: str, args):
     print(json.dumps(rec), flush=True)
     del grp
     torch.cuda.empty_cache()
+
+
+def shard_bench(args):
+    """One GPU's share of a kv-head-sharded group: the Qwen3-8B sweep shape
+    (GQA 32/8, d 128, suffixes of 1024) with Hq = 32/g and Hkv = 8/g for
+    g = 1, 2, 4, 8, i.e. what each of g GPUs would run.  One JSON line per
+    (P, N, g): step time, TFLOP/s of the shard, its efficiency against the
+    unsharded group (TFLOP/s ratio), and the speedup over the dense baseline
+    on the same shard."""
+    import torch
+    from paper_2606_01143_amd.group import DeviceGroup
+    from synthetic import GroupShape, make_group
+    steps, warm = max(1, args.steps), max(1, args.warmup)
+    for p, n in ((2048, 4), (8192, 8), (16384, 16)):
+        base = None
+        for g in (1, 2, 4, 8):
+            shape = GroupShape(32 // g, 8 // g, 128, p, (1024,) * n, "bf16")
+            log(f"shard P={p} N={n} g={g}: generating")
+            inp = make_group(shape, seed=args.seed)
+            mbs = [(i, i + 1) for i in range(n)]
+            grp = DeviceGroup(inp, device="cuda:0", dense=True)
+            del inp
+            grp.prepare(mbs)
+            pre, suf, _ = pair_counts(shape)
+            flops = 14 * shape.head_dim * shape.num_q_heads * (pre + sum(suf))
+            ms = time_steps(lambda: grp.run_schedule(mbs), steps, warm)
+            ms_dense = time_steps(lambda: grp.run_dense(), max(1, steps // 4), 1)
+            tf = flops / (ms * 1e-3) / 1e12
+            base = tf if g == 1 else base
+            rec = {"workload": f"qwen3_8b_p{p}_n{n}", "shard_g": g, "num_q_heads": shape.num_q_heads,
+                   "num_kv_heads": shape.num_kv_heads, "ms_per_step": round(ms, 4),
+                   "value_tflops": round(tf, 2), "pct_mfma_peak": round(100 * tf / BF16_PEAK_TFLOPS, 2),
+                   "efficiency_vs_unsharded": round(tf / base, 3), "dense_ms_per_step": round(ms_dense, 4),
+                   "speedup_vs_dense": round(ms_dense / ms, 3), "steps": steps, "dtype": "bf16",
+                   "data": "synthetic"}
+            print(json.dumps(rec), flush=True)
+            del grp
+            torch.cuda.empty_cache()
 
 
 def layer_bench(args):

@@ -87,6 +87,14 @@ struct AttnArgs {
                          // seq_base .. seq_base+n_seq-1 (all visible)
   int32_t pk_mode;       // prefix-key epilogue: 0 => gk/gv += fp32 gradient;
                          // 1 => dk_p/dv_p = gradient + gk/gv in storage dtype
+  // bf16 backward launches with few key tiles may cut each key tile's row
+  // sweep into kv_rsplit contiguous shares.  Share j writes its scaled fp32
+  // partial dK/dV to part_dk/part_dv[j][key row][Hkv][d], where the key row
+  // is the prefix key, or P + the packed row of a suffix key; a combine
+  // kernel then sums the shares in index order and applies the epilogue.
+  int32_t kv_rsplit;
+  float* part_dk;
+  float* part_dv;
   float* gk;             // [P, Hkv, d] fp32
   float* gv;
   void* dk_p;

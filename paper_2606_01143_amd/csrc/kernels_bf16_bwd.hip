@@ -30,6 +30,7 @@
 // are invisible to the compiler's wait tracking: every tile is read only
 // after tile_barrier (vmcnt(0) + workgroup barrier).
 #include <algorithm>
+#include <cmath>
 
 #include "common.hpp"
 #include "launch.hpp"
@@ -88,8 +89,9 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
   const int r = lane & 31, h = lane >> 5;
   FragOffsets<D> fo;
   fo.init(lane);
-  // block b -> kv head b % Hkv (one XCD per kv head), key tile b / Hkv
-  const int hk = bid % a.hkv, x = bid / a.hkv;
+  // block b -> kv head b % Hkv (one XCD per kv head), row share, key tile
+  const int R = a.kv_rsplit > 1 ? a.kv_rsplit : 1;
+  const int hk = bid % a.hkv, rs = (bid / a.hkv) % R, x = bid / a.hkv / R;
   const int G = a.hq / a.hkv;
 
   // ---- which 64 keys: a prefix tile, or a tile of suffix s.  Launches
@@ -149,7 +151,9 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
     n_sr = (kseg - k0 + BQ - 1) / BQ;
   }
   const int per_head = n_pr + n_sr;
-  const int ntiles = G * per_head;
+  // this block's contiguous share of the (row tile, head) sequence below
+  const int t_lo = (int)((long)G * per_head * rs / R);
+  const int ntiles = (int)((long)G * per_head * (rs + 1) / R) - t_lo;
   struct RowTile {
     int hh, row0, nr, lp_first;
     bool prefix, causal;
@@ -312,8 +316,8 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
 
   // iteration t: the P-wave takes tile t, the dS-wave tile t - 1; tile t + 1
   // loads meanwhile
-  Cursor cl = {0, 0, 0};  // next tile to load
-  Cursor cc = {0, 0, 0};  // next tile this wave computes
+  Cursor cl = {t_lo / G, t_lo % G, 0};  // next tile to load
+  Cursor cc = cl;                        // next tile this wave computes
   if (ntiles > 0) {
     issue(cl);
     advance(cl);
@@ -339,6 +343,20 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
   if (wave_k0 + r >= kseg) return;
   const int key = wave_k0 + r;
   const float sc = pw ? 1.f : a.scale;
+  if (R > 1) {
+    // this share's scaled partial; bwd_kv_combine applies the epilogue
+    const size_t krow = kpre ? (size_t)key : (size_t)a.P + kbase + key;
+    const size_t nrows = (size_t)a.P + a.total_len;
+    float* part = (pw ? a.part_dv : a.part_dk) + (((size_t)rs * nrows + krow) * a.hkv + hk) * D + 4 * h;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4)
+        *(float4*)(part + 32 * db + 8 * g4) =
+            make_float4(acc[db][4 * g4] * sc, acc[db][4 * g4 + 1] * sc, acc[db][4 * g4 + 2] * sc,
+                        acc[db][4 * g4 + 3] * sc);
+    return;
+  }
   if (kpre) {
     const size_t off = ((size_t)key * a.hkv + hk) * D + 4 * h;
     float* cache = pw ? a.gv : a.gk;
@@ -635,11 +653,69 @@ __global__ __launch_bounds__(256) void bwd_dq_combine_kernel(AttnArgs a) {
   *(bf16x4*)((bf16*)a.dq_s + rh * D + 4 * c) = o;
 }
 
+// dK/dV of every key of a launch whose key-outer role split its row sweeps:
+// the kv_rsplit partials summed in share order, then the launch's epilogue
+// (prefix keys: cache += sum, or storage = sum + cache; suffix keys:
+// storage = sum).  Keys: the n_pre prefix keys, then the packed rows
+// cu[seq_base] .. cu[seq_base + n_seq] - 1 (at most n_sfx of them).  One
+// group of D / 4 threads per (key, kv head), 16-byte accesses.
+template <int D>
+__global__ __launch_bounds__(256) void bwd_kv_combine_kernel(AttnArgs a, int n_pre, int n_sfx) {
+  constexpr int TPR = D / 4;
+  const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+  const long kh = idx / TPR;  // (key index) * hkv + kv head
+  const int c = (int)(idx % TPR);
+  const long n_pre_kh = (long)n_pre * a.hkv;
+  if (kh >= n_pre_kh + (long)n_sfx * a.hkv) return;
+  const bool pre = kh < n_pre_kh;
+  const int hk = (int)(kh % a.hkv);
+  long key;
+  if (pre) {
+    key = kh / a.hkv;
+  } else {
+    const int r0 = a.cu[a.seq_base], r1 = a.cu[a.seq_base + a.n_seq];
+    key = r0 + (kh - n_pre_kh) / a.hkv;
+    if (key >= r1) return;
+  }
+  const size_t nrows = (size_t)a.P + a.total_len;
+  const size_t krow = pre ? (size_t)key : (size_t)a.P + key;
+  const size_t off = (krow * a.hkv + hk) * D + 4 * c;
+  const size_t stride = nrows * a.hkv * D;
+  float4 sk = *(const float4*)(a.part_dk + off), sv = *(const float4*)(a.part_dv + off);
+  for (int j = 1; j < a.kv_rsplit; ++j) {
+    const float4 k4 = *(const float4*)(a.part_dk + j * stride + off);
+    const float4 v4 = *(const float4*)(a.part_dv + j * stride + off);
+    sk.x += k4.x; sk.y += k4.y; sk.z += k4.z; sk.w += k4.w;
+    sv.x += v4.x; sv.y += v4.y; sv.z += v4.z; sv.w += v4.w;
+  }
+  const size_t o = ((size_t)key * a.hkv + hk) * D + 4 * c;
+  if (pre) {
+    float4* gk = (float4*)(a.gk + o);
+    float4* gv = (float4*)(a.gv + o);
+    const float4 ck = *gk, cv = *gv;
+    if (a.pk_mode == kPkAccumulate) {
+      *gk = make_float4(ck.x + sk.x, ck.y + sk.y, ck.z + sk.z, ck.w + sk.w);
+      *gv = make_float4(cv.x + sv.x, cv.y + sv.y, cv.z + sv.z, cv.w + sv.w);
+    } else {
+      *(bf16x4*)((bf16*)a.dk_p + o) = bf16x4{(bf16)(sk.x + ck.x), (bf16)(sk.y + ck.y),
+                                             (bf16)(sk.z + ck.z), (bf16)(sk.w + ck.w)};
+      *(bf16x4*)((bf16*)a.dv_p + o) = bf16x4{(bf16)(sv.x + cv.x), (bf16)(sv.y + cv.y),
+                                             (bf16)(sv.z + cv.z), (bf16)(sv.w + cv.w)};
+    }
+  } else {
+    *(bf16x4*)((bf16*)a.dk_s + o) = bf16x4{(bf16)sk.x, (bf16)sk.y, (bf16)sk.z, (bf16)sk.w};
+    *(bf16x4*)((bf16*)a.dv_s + o) = bf16x4{(bf16)sv.x, (bf16)sv.y, (bf16)sv.z, (bf16)sv.w};
+  }
+}
+
 hipError_t launch_bwd_bf16(const AttnArgs& a, int head_dim, int n_qz, bool deterministic,
                            hipStream_t st) {
   (void)deterministic;  // both roles are deterministic: no atomics anywhere
   if (a.n_split > 1 && (a.prefix_rows || a.part_dq == nullptr)) return hipErrorInvalidValue;
-  const long n_kv = (long)(a.n_prefix_k_tiles + a.n_seq * a.n_suffix_k_tiles) * a.hkv;
+  const int R = a.kv_rsplit > 1 ? a.kv_rsplit : 1;
+  if (R > 1 && (a.part_dk == nullptr || a.part_dv == nullptr)) return hipErrorInvalidValue;
+  const long n_kt = (long)a.n_prefix_k_tiles + (long)a.n_seq * a.n_suffix_k_tiles;
+  const long n_kv = n_kt * a.hkv * R;
   const long n_q = (long)(a.n_prefix_q_tiles + a.n_suffix_q_tiles) * a.hq * n_qz * a.n_split;
   if (n_kv + n_q == 0) return hipSuccess;
   // Phase C / dense prefix: the causal key tiles near the start of the prefix
@@ -657,7 +733,20 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, int head_dim, int n_qz, bool deter
     hipLaunchKernelGGL(bwd_bf16_kernel<128>, dim3((unsigned)nb), dim3(kThreads), 0, st, a, (int)n_first,
                        (int)n_kv, (int)n_q, kv_first);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || a.n_split <= 1) return e;
+  if (e != hipSuccess) return e;
+  if (R > 1 && n_kt > 0) {
+    const int n_pre = a.n_prefix_k_tiles > 0 ? a.P : 0;
+    const int n_sfx = a.n_seq * a.n_suffix_k_tiles > 0 ? a.total_len : 0;
+    const long kthreads = ((long)n_pre + n_sfx) * a.hkv * (head_dim / 4);
+    const unsigned kb = (unsigned)((kthreads + 255) / 256);
+    ProfileScope pk("bwd_kv_combine", st);
+    if (head_dim == 64)
+      hipLaunchKernelGGL(bwd_kv_combine_kernel<64>, dim3(kb), dim3(256), 0, st, a, n_pre, n_sfx);
+    else
+      hipLaunchKernelGGL(bwd_kv_combine_kernel<128>, dim3(kb), dim3(256), 0, st, a, n_pre, n_sfx);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  if (a.n_split <= 1) return hipSuccess;
   const long threads = (long)a.total_len * a.hq * (head_dim / 4);
   const unsigned cb = (unsigned)((threads + 255) / 256);
   ProfileScope pc("bwd_dq_combine", st);
@@ -669,6 +758,22 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, int head_dim, int n_qz, bool deter
 }
 
 int bwd_bf16_block_q() { return kQBQ; }
+
+int bwd_bf16_kvsplit(long kv_tiles, long max_tiles) {
+  // kv_tiles: the key-outer role's (32-row tile, q head) steps over all its
+  // blocks; max_tiles: the longest block's.  The query-outer role adds about
+  // 3/4 of that work (three products per visible block instead of four),
+  // spread over two slots per CU on 256 CUs.  A block longer than 1.5x that
+  // average per slot would end the launch alone: then every key tile's
+  // sweep is cut into R contiguous shares, about the average each, at most
+  // 8 and at least 16 steps each.
+  if (kv_tiles <= 0 || max_tiles <= 0) return 1;
+  const double per_slot = 1.75 * (double)kv_tiles / 512.0;
+  if ((double)max_tiles <= 1.5 * per_slot) return 1;
+  long r = (long)std::ceil((double)max_tiles / per_slot);
+  r = std::min(r, max_tiles / 16);
+  return (int)std::max(1L, std::min(r, 8L));
+}
 
 int bwd_bf16_qsplit(int n_row_blocks, int n_key_tiles) {
   // Only when the query-outer blocks alone cannot fill two slots per CU on

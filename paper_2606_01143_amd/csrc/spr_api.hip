@@ -135,6 +135,7 @@ AttnArgs base_args(const spr_dims* d) {
   a.scale = eff_scale(d);
   a.scale_log2 = a.scale * kLog2e;
   a.n_split = 1;
+  a.kv_rsplit = 1;
   return a;
 }
 
@@ -152,6 +153,43 @@ int suffix_bwd_splits(const spr_dims* d, int32_t n_mb, int32_t max_len) {
   const int nrb = tiles(max_len, bwd_bf16_block_q()) * d->num_q_heads * n_mb;
   const int nkt = tiles(d->prefix_len, bwd_bf16_block_k()) + tiles(max_len, bwd_bf16_block_k());
   return bwd_bf16_qsplit(nrb, nkt);
+}
+
+// row shares of the backward's key-outer role (bf16 path only), see
+// bwd_bf16_kvsplit.  Work is counted in (32-row tile, q head) steps of the
+// 64-key tiles, from the sizes alone (so that packed and padded calls of
+// the same sizes agree): a causal key range of len keys costs
+// g * ceil((len - k0) / 32) steps for the tile at k0.
+long causal_steps(long len, long g) {
+  long s = 0;
+  for (long k0 = 0; k0 < len; k0 += 64) s += g * ((len - k0 + 31) / 32);
+  return s;
+}
+int bwd_kv_splits(const spr_dims* d, long kv_steps, long max_steps) {
+  if (d->dtype != SPR_BF16) return 1;
+  return bwd_bf16_kvsplit(kv_steps * d->num_kv_heads, max_steps);
+}
+// Phase B: prefix key tiles see every suffix row (at most n_mb * max_len),
+// suffix key tiles their own causal rows
+int suffix_bwd_kv_splits(const spr_dims* d, int32_t n_mb, int32_t max_len) {
+  const long g = d->num_q_heads / d->num_kv_heads, rows = (long)n_mb * max_len;
+  const long pre = (long)tiles(d->prefix_len, bwd_bf16_block_k()) * g * ((rows + 31) / 32);
+  const long kv = pre + (long)n_mb * causal_steps(max_len, g);
+  return bwd_kv_splits(d, kv, d->prefix_len > 0 ? g * ((rows + 31) / 32) : g * ((max_len + 31) / 32));
+}
+// Phase C: causal prefix rows; key tile 0 sweeps all P
+int prefix_bwd_kv_splits(const spr_dims* d) {
+  const long g = d->num_q_heads / d->num_kv_heads;
+  return bwd_kv_splits(d, causal_steps(d->prefix_len, g), g * ((d->prefix_len + 31) / 32));
+}
+// the dense baseline's per-trajectory launch: prefix key tiles see the
+// causal prefix rows and the suffix rows, suffix key tiles their own rows
+int dense_bwd_kv_splits(const spr_dims* d, int32_t max_len) {
+  const long g = d->num_q_heads / d->num_kv_heads, P = d->prefix_len;
+  const long sr = g * ((max_len + 31) / 32);
+  const long kv = causal_steps(P, g) + (long)tiles(d->prefix_len, bwd_bf16_block_k()) * sr +
+                  causal_steps(max_len, g);
+  return bwd_kv_splits(d, kv, g * ((P + 31) / 32) + sr);
 }
 
 int block_q(int dtype) { return dtype == SPR_BF16 ? fwd_bf16_block_q() : f32_block_q(); }
@@ -172,7 +210,7 @@ hipError_t launch_bwd(const spr_dims* d, const AttnArgs& a, int n_qz, hipStream_
 struct WsLayout {
   size_t dd_p = 0, dq_acc_p = 0, dd_s = 0, dq_acc_s = 0, dk_acc_p = 0, dv_acc_p = 0;
   size_t lse2_p = 0, lse2_s = 0;
-  size_t part_o = 0, part_lse = 0, part_dq = 0;
+  size_t part_o = 0, part_lse = 0, part_dq = 0, part_dk = 0, part_dv = 0;
   // padded layout: offsets, clamped lengths, packed copies, inner workspace
   size_t cu = 0, lens_c = 0, pq = 0, pk = 0, pv = 0, po = 0, plse = 0, pdo = 0;
   size_t pdq = 0, pdk = 0, pdv = 0, inner = 0, inner_bytes = 0;
@@ -209,13 +247,24 @@ WsLayout ws_layout(int op, const spr_dims* d, int32_t n_mb, int32_t max_len, int
       if (f32) w.dq_acc_s = take(T * hq * hd * 4);
       const size_t ns = suffix_bwd_splits(d, n_mb, max_len);
       if (ns > 1) w.part_dq = take(ns * T * hq * hd * 4);
+      const size_t rs = suffix_bwd_kv_splits(d, n_mb, max_len);
+      if (rs > 1) {
+        w.part_dk = take(rs * (P + T) * hkv * hd * 4);
+        w.part_dv = take(rs * (P + T) * hkv * hd * 4);
+      }
       break;
     }
-    case SPR_OP_PREFIX_BWD:
+    case SPR_OP_PREFIX_BWD: {
       w.dd_p = take(hq * P * 4);
       w.lse2_p = take(hq * P * 4);
       if (f32) w.dq_acc_p = take(P * hq * hd * 4);
+      const size_t rs = prefix_bwd_kv_splits(d);
+      if (rs > 1) {
+        w.part_dk = take(rs * P * hkv * hd * 4);
+        w.part_dv = take(rs * P * hkv * hd * 4);
+      }
       break;
+    }
     case SPR_OP_SUFFIX_FWD_PADDED:
     case SPR_OP_SUFFIX_BWD_PADDED: {
       // packed copies for the worst case of n_mb full suffixes
@@ -248,6 +297,13 @@ WsLayout ws_layout(int op, const spr_dims* d, int32_t n_mb, int32_t max_len, int
       if (f32) w.dq_acc_s = take(T * hq * hd * 4);
       w.dk_acc_p = take(P * hkv * hd * 4);
       w.dv_acc_p = take(P * hkv * hd * 4);
+      {
+        const size_t rs = dense_bwd_kv_splits(d, max_len);
+        if (rs > 1) {
+          w.part_dk = take(rs * (P + T) * hkv * hd * 4);
+          w.part_dv = take(rs * (P + T) * hkv * hd * 4);
+        }
+      }
       break;
     default:
       break;
@@ -484,6 +540,11 @@ spr_status spr_suffix_attn_bwd_accum(const spr_dims* dims, const void* k_p, cons
   a.n_suffix_q_tiles = tiles(max_len, block_q(dims->dtype));
   a.n_split = suffix_bwd_splits(dims, n_mb, max_len);
   if (a.n_split > 1) a.part_dq = at<float>(ws, w.part_dq);
+  a.kv_rsplit = suffix_bwd_kv_splits(dims, n_mb, max_len);
+  if (a.kv_rsplit > 1) {
+    a.part_dk = at<float>(ws, w.part_dk);
+    a.part_dv = at<float>(ws, w.part_dv);
+  }
   if ((st = hip_check(launch_bwd(dims, a, n_mb, stream), "suffix backward")) != SPR_OK) return st;
   if (f32 && (st = hip_check(launch_convert(dims->dtype, dq_acc, a.scale, nullptr, dq_s,
                                             T * hq * hd, stream), "dq convert")) != SPR_OK)
@@ -664,6 +725,11 @@ spr_status prefix_bwd_parts(const spr_dims* dims, const void* q_p, const void* k
     a.gk = const_cast<float*>(gk_cache); a.gv = const_cast<float*>(gv_cache);
     a.dk_p = dk_p; a.dv_p = dv_p;
     a.n_prefix_k_tiles = tiles(dims->prefix_len, block_k(dims->dtype));
+    a.kv_rsplit = prefix_bwd_kv_splits(dims);
+    if (a.kv_rsplit > 1) {
+      a.part_dk = at<float>(ws, w.part_dk);
+      a.part_dv = at<float>(ws, w.part_dv);
+    }
   }
   if ((st = hip_check(launch_bwd(dims, a, 1, stream), "prefix backward")) != SPR_OK) return st;
   if (dq_acc && (st = hip_check(launch_convert(dims->dtype, dq_acc, scale, nullptr, dq_p, P * hq * hd,
@@ -778,6 +844,11 @@ spr_status spr_dense_recompute_baseline(
     a.gk = dk_acc; a.gv = dv_acc;
     a.dk_s = dk_s; a.dv_s = dv_s;
     a.n_prefix_q_tiles = have_dop ? tiles(dims->prefix_len, block_q(dims->dtype)) : 0;
+    a.kv_rsplit = dense_bwd_kv_splits(dims, max_len);
+    if (a.kv_rsplit > 1) {
+      a.part_dk = at<float>(ws, w.part_dk);
+      a.part_dv = at<float>(ws, w.part_dv);
+    }
     SPR_TRY(launch_bwd(dims, a, 1, stream), "dense backward");
   }
   SPR_TRY(launch_convert(dims->dtype, dq_acc_p, scale, nullptr, dq_p, P * hq * hd, stream), "convert");

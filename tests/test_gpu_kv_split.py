@@ -1,0 +1,124 @@
+"""Key-outer row shares.  When a backward launch has few key tiles (few kv
+heads and a short prefix, e.g. one GPU's share of a kv-head-sharded group),
+each key tile's row sweep is cut into contiguous shares whose fp32 partial
+dK/dV a combine kernel sums in share order before the epilogue (cache add,
+cache injection, or store).  At such shapes: the schedule and the dense
+baseline against the fp64 oracle, bitwise reproducibility, the Phase C
+halves against the whole call, and the padded layout against the packed one.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import dense_group_reference, max_abs_rel, three_phase_reference
+from synthetic import GroupShape, make_group
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-2
+SCHED_KEYS = ["o_p", "lse_p", "o_s", "lse_s", "dq_p", "dk_p", "dv_p", "dq_s", "dk_s", "dv_s",
+              "g_k", "g_v"]
+DENSE_KEYS = SCHED_KEYS[:10]
+
+# (name, shape, microbatches); the shares each launch takes follow from the
+# sizes (one kv head: 2 to 5 in Phase B, 8 in Phase C; two kv heads, d = 64, one
+# microbatch of three ragged suffixes: 4 in Phase B, 6 in Phase C)
+CASES = [
+    ("hkv1_gqa4_p2048", GroupShape(4, 1, 128, 2048, (700, 333), "bf16"), None),
+    ("hkv1_gqa8_p1024", GroupShape(8, 1, 128, 1024, (300,), "bf16"), None),
+    ("hkv2_d64_p1536_one_mb", GroupShape(4, 2, 64, 1536, (400, 97, 250), "bf16"), [(0, 3)]),
+]
+
+
+def _announce(msg):
+    sys.stderr.write(f"\n[gpu-case] {msg}\n")
+    sys.stderr.flush()
+
+
+def _check(got, ref, keys, what):
+    errs = {}
+    for k in keys:
+        r = ref[k].T if k.startswith("lse") else ref[k]
+        errs[k] = max_abs_rel(got[k], r, floor=1e-3)
+    bad = {k: v for k, v in errs.items() if not v <= TOL}
+    assert not bad, f"{what}: {bad} (all: {errs})"
+
+
+@pytest.mark.parametrize("name,shape,mbs", CASES, ids=[c[0] for c in CASES])
+def test_row_shares_match_oracle(gpu, name, shape, mbs):
+    import torch
+    from paper_2606_01143_amd import binding as B
+    from paper_2606_01143_amd.group import DeviceGroup
+    _announce(f"row shares {name} {shape}")
+    inp = make_group(shape, seed=11)
+    grp = DeviceGroup(inp, dense=True, microbatch_splits=[mbs] if mbs else None)
+    B.profile_reset()
+    B.profile_enable(True)
+    try:
+        grp.run_schedule(mbs, overlap=False)
+        torch.cuda.synchronize()
+        _, n_sched = B.profile_query("bwd_kv_combine")
+        grp.run_dense()
+        torch.cuda.synchronize()
+        _, n_all = B.profile_query("bwd_kv_combine")
+    finally:
+        B.profile_enable(False)
+    n_bwd = len(mbs) if mbs else shape.n
+    # every suffix backward, Phase C, and every dense trajectory split its rows
+    assert n_sched == n_bwd + 1 and n_all - n_sched == shape.n, (n_sched, n_all)
+    _check(grp.fetch("schedule"), three_phase_reference(inp), SCHED_KEYS, "schedule")
+    _check(grp.fetch("dense"), dense_group_reference(inp), DENSE_KEYS, "dense")
+
+
+@pytest.mark.parametrize("name,shape,mbs", CASES[:2], ids=[c[0] for c in CASES[:2]])
+def test_row_shares_bitwise_reproducible(gpu, name, shape, mbs):
+    from paper_2606_01143_amd.group import DeviceGroup
+    _announce(f"row shares reruns {name}")
+    inp = make_group(shape, seed=12)
+    grp = DeviceGroup(inp, dense=False)
+    grp.run_schedule()
+    a = grp.fetch("schedule")
+    grp.run_schedule()
+    b = grp.fetch("schedule")
+    for k in SCHED_KEYS:
+        assert np.array_equal(a[k], b[k]), k
+
+
+def test_row_shares_prefix_backward_halves_equal_whole(gpu):
+    import torch
+    from paper_2606_01143_amd import binding as B
+    from paper_2606_01143_amd.group import DeviceGroup
+    shape = CASES[0][1]
+    _announce(f"row shares split Phase C {shape}")
+    inp = make_group(shape, seed=13)
+    grp = DeviceGroup(inp, dense=False)
+    grp.run_schedule(overlap=False)
+    o, d = grp.out, grp.dims
+    ws2 = torch.empty_like(grp.ws)
+    B.prefix_bwd(d, grp.q_p, grp.k_p, grp.v_p, o["o_p"], o["lse_p"], grp.g_y, grp.gk, grp.gv,
+                 o["dq_p"], o["dk_p"], o["dv_p"], grp.ws)
+    ref = {k: o[k].clone() for k in ("dq_p", "dk_p", "dv_p")}
+    dq, dk, dv = (torch.full_like(ref[k], 3) for k in ("dq_p", "dk_p", "dv_p"))
+    B.prefix_bwd_dq(d, grp.q_p, grp.k_p, grp.v_p, o["o_p"], o["lse_p"], grp.g_y, dq, ws2)
+    B.prefix_bwd_dkv(d, grp.q_p, grp.k_p, grp.v_p, o["o_p"], o["lse_p"], grp.g_y, grp.gk, grp.gv,
+                     dk, dv, grp.ws)
+    torch.cuda.synchronize()
+    assert torch.equal(dq, ref["dq_p"]) and torch.equal(dk, ref["dk_p"]) and torch.equal(dv, ref["dv_p"])
+
+
+def test_row_shares_padded_equals_packed(gpu):
+    import torch
+    from paper_2606_01143_amd.group import DeviceGroup
+    name, shape, mbs = CASES[2]
+    _announce(f"row shares padded vs packed {name}")
+    inp = make_group(shape, seed=14)
+    packed = DeviceGroup(inp, dense=False, microbatch_splits=[mbs])
+    padded = DeviceGroup(inp, dense=False, microbatch_splits=[mbs], layout="padded")
+    packed.run_schedule(mbs)
+    padded.run_schedule(mbs)
+    padded.gather_padded_outputs()
+    torch.cuda.synchronize()
+    for k in packed.out:
+        assert torch.equal(packed.out[k], padded.out[k]), k
+    assert torch.equal(packed.gk, padded.gk) and torch.equal(packed.gv, padded.gv)

@@ -140,6 +140,50 @@ def _stream(stream):
     return stream.cuda_stream
 
 
+class _Sizes:
+    """Required sizes of one call's tensors, from the dims and the row counts.
+
+    The C ABI takes plain pointers and cannot see a buffer's size; a tensor
+    that is too small, or of another element type than the dims say, would
+    be read or written past its end on the GPU.  Every attention wrapper
+    therefore checks its tensors here first (None is a NULL pointer and is
+    left to the library's own checks)."""
+
+    def __init__(self, dims, rows_s: int = 0):
+        self.P, self.hq, self.hkv, self.d = (int(dims.prefix_len), int(dims.num_q_heads),
+                                             int(dims.num_kv_heads), int(dims.head_dim))
+        self.eb = 4 if dims.dtype == SPR_F32 else 2
+        self.T = int(rows_s)
+
+    def _need(self, name, x, elems, esize):
+        if x is None or isinstance(x, int):
+            return
+        if x.element_size() != esize:
+            raise ValueError(f"{name}: elements of {x.element_size()} bytes, the call needs {esize}")
+        if x.numel() < elems:
+            raise ValueError(f"{name}: {x.numel()} elements, the call needs {elems}")
+
+    def q(self, rows, **kw):   # [rows, Hq, d] storage dtype
+        for k, v in kw.items():
+            self._need(k, v, rows * self.hq * self.d, self.eb)
+
+    def kv(self, rows, **kw):  # [rows, Hkv, d] storage dtype
+        for k, v in kw.items():
+            self._need(k, v, rows * self.hkv * self.d, self.eb)
+
+    def lse(self, rows, **kw):  # [rows, Hq] fp32
+        for k, v in kw.items():
+            self._need(k, v, rows * self.hq, 4)
+
+    def cache(self, **kw):     # [P, Hkv, d] fp32
+        for k, v in kw.items():
+            self._need(k, v, self.P * self.hkv * self.d, 4)
+
+    def i32(self, n, **kw):
+        for k, v in kw.items():
+            self._need(k, v, n, 4)
+
+
 def _check(status: int) -> None:
     if status != 0:
         raise SprError(status, lib().spr_last_error().decode())
@@ -151,12 +195,22 @@ def _nbytes(ws) -> int:
 
 # ------------------------------------------------------------ entry points
 def prefix_fwd(dims, q_p, k_p, v_p, o_p, lse_p, stream=None):
+    z = _Sizes(dims)
+    z.q(z.P, q_p=q_p, o_p=o_p)
+    z.kv(z.P, k_p=k_p, v_p=v_p)
+    z.lse(z.P, lse_p=lse_p)
     _check(lib().spr_prefix_fwd(byref(dims), _ptr(q_p), _ptr(k_p), _ptr(v_p), _ptr(o_p),
                                 _ptr(lse_p), _stream(stream)))
 
 
 def suffix_attn_fwd(dims, k_p, v_p, q_s, k_s, v_s, cu_seqlens, n_mb, max_len, total_len, o_s,
                     lse_s, ws=None, stream=None):
+    z = _Sizes(dims, total_len)
+    z.kv(z.P, k_p=k_p, v_p=v_p)
+    z.q(z.T, q_s=q_s, o_s=o_s)
+    z.kv(z.T, k_s=k_s, v_s=v_s)
+    z.lse(z.T, lse_s=lse_s)
+    z.i32(int(n_mb) + 1, cu_seqlens=cu_seqlens)
     _check(lib().spr_suffix_attn_fwd(byref(dims), _ptr(k_p), _ptr(v_p), _ptr(q_s), _ptr(k_s),
                                      _ptr(v_s), _ptr(cu_seqlens), n_mb, max_len, total_len,
                                      _ptr(o_s), _ptr(lse_s), _ptr(ws), _nbytes(ws),
@@ -166,6 +220,13 @@ def suffix_attn_fwd(dims, k_p, v_p, q_s, k_s, v_s, cu_seqlens, n_mb, max_len, to
 def suffix_attn_bwd_accum(dims, k_p, v_p, q_s, k_s, v_s, o_s, lse_s, do_s, cu_seqlens, n_mb,
                           max_len, total_len, dq_s, dk_s, dv_s, gk_cache, gv_cache, ws=None,
                           stream=None):
+    z = _Sizes(dims, total_len)
+    z.kv(z.P, k_p=k_p, v_p=v_p)
+    z.q(z.T, q_s=q_s, o_s=o_s, do_s=do_s, dq_s=dq_s)
+    z.kv(z.T, k_s=k_s, v_s=v_s, dk_s=dk_s, dv_s=dv_s)
+    z.lse(z.T, lse_s=lse_s)
+    z.cache(gk_cache=gk_cache, gv_cache=gv_cache)
+    z.i32(int(n_mb) + 1, cu_seqlens=cu_seqlens)
     _check(lib().spr_suffix_attn_bwd_accum(
         byref(dims), _ptr(k_p), _ptr(v_p), _ptr(q_s), _ptr(k_s), _ptr(v_s), _ptr(o_s),
         _ptr(lse_s), _ptr(do_s), _ptr(cu_seqlens), n_mb, max_len, total_len, _ptr(dq_s),
@@ -175,6 +236,11 @@ def suffix_attn_bwd_accum(dims, k_p, v_p, q_s, k_s, v_s, o_s, lse_s, do_s, cu_se
 
 def prefix_bwd(dims, q_p, k_p, v_p, o_p, lse_p, do_p, gk_cache, gv_cache, dq_p, dk_p, dv_p,
                ws=None, stream=None):
+    z = _Sizes(dims)
+    z.q(z.P, q_p=q_p, o_p=o_p, do_p=do_p, dq_p=dq_p)
+    z.kv(z.P, k_p=k_p, v_p=v_p, dk_p=dk_p, dv_p=dv_p)
+    z.lse(z.P, lse_p=lse_p)
+    z.cache(gk_cache=gk_cache, gv_cache=gv_cache)
     _check(lib().spr_prefix_bwd(byref(dims), _ptr(q_p), _ptr(k_p), _ptr(v_p), _ptr(o_p),
                                 _ptr(lse_p), _ptr(do_p), _ptr(gk_cache), _ptr(gv_cache),
                                 _ptr(dq_p), _ptr(dk_p), _ptr(dv_p), _ptr(ws), _nbytes(ws),
@@ -183,6 +249,12 @@ def prefix_bwd(dims, q_p, k_p, v_p, o_p, lse_p, do_p, gk_cache, gv_cache, dq_p, 
 
 def suffix_attn_fwd_padded(dims, k_p, v_p, q_s, k_s, v_s, seq_lens, n, s_max, o_s, lse_s, ws=None,
                            stream=None):
+    z = _Sizes(dims, int(n) * int(s_max))
+    z.kv(z.P, k_p=k_p, v_p=v_p)
+    z.q(z.T, q_s=q_s, o_s=o_s)
+    z.kv(z.T, k_s=k_s, v_s=v_s)
+    z.lse(z.T, lse_s=lse_s)
+    z.i32(int(n), seq_lens=seq_lens)
     _check(lib().spr_suffix_attn_fwd_padded(byref(dims), _ptr(k_p), _ptr(v_p), _ptr(q_s), _ptr(k_s),
                                             _ptr(v_s), _ptr(seq_lens), n, s_max, _ptr(o_s), _ptr(lse_s),
                                             _ptr(ws), _nbytes(ws), _stream(stream)))
@@ -190,6 +262,13 @@ def suffix_attn_fwd_padded(dims, k_p, v_p, q_s, k_s, v_s, seq_lens, n, s_max, o_
 
 def suffix_attn_bwd_accum_padded(dims, k_p, v_p, q_s, k_s, v_s, o_s, lse_s, do_s, seq_lens, n, s_max,
                                  dq_s, dk_s, dv_s, gk_cache, gv_cache, ws=None, stream=None):
+    z = _Sizes(dims, int(n) * int(s_max))
+    z.kv(z.P, k_p=k_p, v_p=v_p)
+    z.q(z.T, q_s=q_s, o_s=o_s, do_s=do_s, dq_s=dq_s)
+    z.kv(z.T, k_s=k_s, v_s=v_s, dk_s=dk_s, dv_s=dv_s)
+    z.lse(z.T, lse_s=lse_s)
+    z.cache(gk_cache=gk_cache, gv_cache=gv_cache)
+    z.i32(int(n), seq_lens=seq_lens)
     _check(lib().spr_suffix_attn_bwd_accum_padded(
         byref(dims), _ptr(k_p), _ptr(v_p), _ptr(q_s), _ptr(k_s), _ptr(v_s), _ptr(o_s), _ptr(lse_s),
         _ptr(do_s), _ptr(seq_lens), n, s_max, _ptr(dq_s), _ptr(dk_s), _ptr(dv_s), _ptr(gk_cache),
@@ -197,6 +276,10 @@ def suffix_attn_bwd_accum_padded(dims, k_p, v_p, q_s, k_s, v_s, o_s, lse_s, do_s
 
 
 def prefix_bwd_dq(dims, q_p, k_p, v_p, o_p, lse_p, do_p, dq_p, ws=None, stream=None):
+    z = _Sizes(dims)
+    z.q(z.P, q_p=q_p, o_p=o_p, do_p=do_p, dq_p=dq_p)
+    z.kv(z.P, k_p=k_p, v_p=v_p)
+    z.lse(z.P, lse_p=lse_p)
     _check(lib().spr_prefix_bwd_dq(byref(dims), _ptr(q_p), _ptr(k_p), _ptr(v_p), _ptr(o_p),
                                    _ptr(lse_p), _ptr(do_p), _ptr(dq_p), _ptr(ws), _nbytes(ws),
                                    _stream(stream)))
@@ -204,6 +287,11 @@ def prefix_bwd_dq(dims, q_p, k_p, v_p, o_p, lse_p, do_p, dq_p, ws=None, stream=N
 
 def prefix_bwd_dkv(dims, q_p, k_p, v_p, o_p, lse_p, do_p, gk_cache, gv_cache, dk_p, dv_p,
                    ws=None, stream=None):
+    z = _Sizes(dims)
+    z.q(z.P, q_p=q_p, o_p=o_p, do_p=do_p)
+    z.kv(z.P, k_p=k_p, v_p=v_p, dk_p=dk_p, dv_p=dv_p)
+    z.lse(z.P, lse_p=lse_p)
+    z.cache(gk_cache=gk_cache, gv_cache=gv_cache)
     _check(lib().spr_prefix_bwd_dkv(byref(dims), _ptr(q_p), _ptr(k_p), _ptr(v_p), _ptr(o_p),
                                     _ptr(lse_p), _ptr(do_p), _ptr(gk_cache), _ptr(gv_cache),
                                     _ptr(dk_p), _ptr(dv_p), _ptr(ws), _nbytes(ws),
@@ -213,6 +301,15 @@ def prefix_bwd_dkv(dims, q_p, k_p, v_p, o_p, lse_p, do_p, gk_cache, gv_cache, dk
 def dense_recompute_baseline(dims, q_p, k_p, v_p, do_p_seq, q_s, k_s, v_s, do_s, cu_seqlens, n,
                              max_len, total_len, o_p, lse_p, o_s, lse_s, dq_s, dk_s, dv_s, dq_p,
                              dk_p, dv_p, ws=None, stream=None):
+    z = _Sizes(dims, total_len)
+    z.q(z.P, q_p=q_p, o_p=o_p, dq_p=dq_p)
+    z.q(int(n) * z.P, do_p_seq=do_p_seq)
+    z.kv(z.P, k_p=k_p, v_p=v_p, dk_p=dk_p, dv_p=dv_p)
+    z.lse(z.P, lse_p=lse_p)
+    z.q(z.T, q_s=q_s, o_s=o_s, do_s=do_s, dq_s=dq_s)
+    z.kv(z.T, k_s=k_s, v_s=v_s, dk_s=dk_s, dv_s=dv_s)
+    z.lse(z.T, lse_s=lse_s)
+    z.i32(int(n) + 1, cu_seqlens=cu_seqlens)
     _check(lib().spr_dense_recompute_baseline(
         byref(dims), _ptr(q_p), _ptr(k_p), _ptr(v_p), _ptr(do_p_seq), _ptr(q_s), _ptr(k_s),
         _ptr(v_s), _ptr(do_s), _ptr(cu_seqlens), n, max_len, total_len, _ptr(o_p), _ptr(lse_p),
@@ -294,10 +391,12 @@ def workspace_size(op, dims, n_mb=0, max_len=0, total_len=0) -> int:
 
 
 def gkv_cache_zero(dims, gk_cache, gv_cache, stream=None):
+    _Sizes(dims).cache(gk_cache=gk_cache, gv_cache=gv_cache)
     _check(lib().spr_gkv_cache_zero(byref(dims), _ptr(gk_cache), _ptr(gv_cache), _stream(stream)))
 
 
 def gkv_accumulate(dims, gk_cache, gv_cache, dgk, dgv, stream=None):
+    _Sizes(dims).cache(gk_cache=gk_cache, gv_cache=gv_cache, dgk=dgk, dgv=dgv)
     _check(lib().spr_gkv_accumulate(byref(dims), _ptr(gk_cache), _ptr(gv_cache), _ptr(dgk),
                                     _ptr(dgv), _stream(stream)))
 

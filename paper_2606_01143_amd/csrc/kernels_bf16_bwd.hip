@@ -763,13 +763,14 @@ int bwd_bf16_kvsplit(long kv_tiles, long max_tiles) {
   // kv_tiles: the key-outer role's (32-row tile, q head) steps over all its
   // blocks; max_tiles: the longest block's.  The query-outer role adds about
   // 3/4 of that work (three products per visible block instead of four),
-  // spread over two slots per CU on 256 CUs.  A block longer than 1.5x that
-  // average per slot would end the launch alone: then every key tile's
+  // spread over two slots per CU on 256 CUs.  A block clearly longer than
+  // that average per slot (by over 10%: the shares' partials and combine
+  // cost about that much) would end the launch alone: then every key tile's
   // sweep is cut into R contiguous shares, about the average each, at most
   // 8 and at least 16 steps each.
   if (kv_tiles <= 0 || max_tiles <= 0) return 1;
   const double per_slot = 1.75 * (double)kv_tiles / 512.0;
-  if ((double)max_tiles <= 1.5 * per_slot) return 1;
+  if ((double)max_tiles <= 1.1 * per_slot) return 1;
   long r = (long)std::ceil((double)max_tiles / per_slot);
   r = std::min(r, max_tiles / 16);
   return (int)std::max(1L, std::min(r, 8L));

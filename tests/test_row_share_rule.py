@@ -1,0 +1,118 @@
+"""The key-outer row-share rule, pinned on the CPU through the workspace
+sizes the library reports: a backward launch that splits its key tiles'
+row sweeps into R shares reserves R * (P + T) * Hkv * d fp32 partials for
+dK and for dV.  The rule is restated here from its description (work in
+(32-row tile, q head) steps of 64-key tiles; the query-outer role adds 3/4;
+two slots per CU on 256 CUs; split when the longest sweep exceeds the
+average per slot by over 10%, R = ceil(longest / average), 1 <= R <= 8,
+each share >= 16 steps) and compared with the library's choice."""
+import math
+
+import pytest
+
+from paper_2606_01143_amd import binding as B
+
+
+def _tiles(n, b):
+    return 0 if n <= 0 else (n + b - 1) // b
+
+
+def _causal(length, g):
+    return sum(g * ((length - k0 + 31) // 32) for k0 in range(0, length, 64))
+
+
+def _rule(kv_steps, max_steps):
+    if kv_steps <= 0 or max_steps <= 0:
+        return 1
+    per_slot = 1.75 * kv_steps / 512.0
+    if max_steps <= 1.1 * per_slot:
+        return 1
+    return max(1, min(math.ceil(max_steps / per_slot), max_steps // 16, 8))
+
+
+def _suffix_r(hq, hkv, P, n, ml):
+    g, rows = hq // hkv, n * ml
+    kv = _tiles(P, 64) * g * ((rows + 31) // 32) + n * _causal(ml, g)
+    crit = g * ((rows + 31) // 32) if P > 0 else g * ((ml + 31) // 32)
+    return _rule(kv * hkv, crit)
+
+
+def _prefix_r(hq, hkv, P):
+    g = hq // hkv
+    return _rule(_causal(P, g) * hkv, g * ((P + 31) // 32))
+
+
+def _qsplit(hq, P, n, ml):
+    """key splits of the query-outer role (fill two slots per CU, at least
+    16 key tiles per split, at most 8 splits)"""
+    nrb = _tiles(ml, 128) * hq * n
+    if nrb <= 0 or nrb >= 512:
+        return 1
+    nkt = _tiles(P, 64) + _tiles(ml, 64)
+    return max(1, min(nkt // 16, (512 + nrb - 1) // nrb, 8))
+
+
+def _align(x):
+    return (x + 255) // 256 * 256
+
+
+def _suffix_ws(hq, hkv, d, P, n, ml, T):
+    off = _align(hq * T * 4) + _align(hq * T * 4)  # row statistic, log2 LSE
+    ns = _qsplit(hq, P, n, ml)
+    if ns > 1:
+        off += _align(ns * T * hq * d * 4)
+    r = _suffix_r(hq, hkv, P, n, ml)
+    if r > 1:
+        off += 2 * _align(r * (P + T) * hkv * d * 4)
+    return off, r
+
+
+def _prefix_ws(hq, hkv, d, P):
+    off = _align(hq * P * 4) * 2
+    r = _prefix_r(hq, hkv, P)
+    if r > 1:
+        off += 2 * _align(r * P * hkv * d * 4)
+    return off, r
+
+
+CASES = [
+    # (Hq, Hkv, d, P, n_mb, max_len, total)
+    (32, 8, 128, 4096, 1, 512, 512),     # bench workload, one suffix: no split in Phase B
+    (32, 8, 128, 2048, 1, 1024, 1024),   # Qwen3-8B sweep, P = 2048
+    (4, 1, 128, 2048, 1, 700, 700),      # one kv head: 5 shares
+    (4, 1, 128, 2048, 1, 333, 333),      # 2 shares
+    (8, 1, 128, 1024, 1, 300, 300),
+    (4, 2, 64, 1536, 3, 400, 747),       # ragged microbatch of three
+    (4, 1, 128, 16384, 1, 1024, 1024),
+    (4, 1, 128, 131072, 2, 1000, 1037),
+]
+
+
+@pytest.mark.parametrize("hq,hkv,d,P,n,ml,T", CASES)
+def test_suffix_backward_workspace_follows_the_rule(hq, hkv, d, P, n, ml, T):
+    dims = B.make_dims(hq, hkv, d, P, "bf16")
+    want, r = _suffix_ws(hq, hkv, d, P, n, ml, T)
+    assert B.workspace_size(B.OP_SUFFIX_BWD, dims, n, ml, T) == want, r
+
+
+@pytest.mark.parametrize("hq,hkv,d,P", sorted({(c[0], c[1], c[2], c[3]) for c in CASES}))
+def test_prefix_backward_workspace_follows_the_rule(hq, hkv, d, P):
+    dims = B.make_dims(hq, hkv, d, P, "bf16")
+    want, r = _prefix_ws(hq, hkv, d, P)
+    assert B.workspace_size(B.OP_PREFIX_BWD, dims) == want, r
+
+
+def test_rule_decisions_at_named_shapes():
+    # the bench workload: Phase B whole, Phase C in two shares
+    assert _suffix_r(32, 8, 4096, 1, 512) == 1 and _prefix_r(32, 8, 4096) == 2
+    # one kv head, short prefix: the sweeps are cut
+    assert _suffix_r(4, 1, 2048, 1, 700) == 5 and _prefix_r(4, 1, 2048) == 8
+    # long prefixes fill the GPU without shares
+    assert _prefix_r(32, 8, 16384) == 1 and _suffix_r(4, 1, 131072, 2, 1000) == 1
+
+
+def test_fp32_storage_never_splits():
+    dims = B.make_dims(4, 1, 128, 2048, "f32")
+    base = B.workspace_size(B.OP_SUFFIX_BWD, dims, 1, 700, 700)
+    # fp32: row statistic, log2 LSE and the fp32 dQ accumulator only
+    assert base == _align(4 * 700 * 4) * 2 + _align(700 * 4 * 128 * 4)

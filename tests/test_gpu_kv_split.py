@@ -122,3 +122,20 @@ def test_row_shares_padded_equals_packed(gpu):
     for k in packed.out:
         assert torch.equal(packed.out[k], padded.out[k]), k
     assert torch.equal(packed.gk, padded.gk) and torch.equal(packed.gv, padded.gv)
+
+
+@pytest.mark.parametrize("name,shape", [
+    ("whole_sweeps", GroupShape(4, 2, 128, 96, (40, 77), "bf16")),
+    ("row_shares", CASES[0][1]),
+], ids=["whole_sweeps", "row_shares"])
+def test_dense_baseline_without_prefix_adjoint(gpu, name, shape):
+    """do_p_seq = NULL: every trajectory's prefix rows get a zero upstream
+    adjoint; the dense baseline then equals the oracle's dense definition
+    with dO_P = 0."""
+    from paper_2606_01143_amd.group import DeviceGroup
+    _announce(f"dense without prefix adjoint {name} {shape}")
+    inp = make_group(shape, seed=15)
+    grp = DeviceGroup(inp, dense=True)
+    grp.run_dense(use_dop=False)
+    ref = dense_group_reference(inp, do_p=np.zeros_like(inp["do_p"]))
+    _check(grp.fetch("dense"), ref, DENSE_KEYS, f"dense, no prefix adjoint, {name}")

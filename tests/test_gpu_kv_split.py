@@ -139,3 +139,28 @@ def test_dense_baseline_without_prefix_adjoint(gpu, name, shape):
     grp.run_dense(use_dop=False)
     ref = dense_group_reference(inp, do_p=np.zeros_like(inp["do_p"]))
     _check(grp.fetch("dense"), ref, DENSE_KEYS, f"dense, no prefix adjoint, {name}")
+
+
+def test_row_shares_without_prefix(gpu):
+    """P = 0 with long suffixes and one kv head: only suffix key tiles exist
+    and split their rows; the combine stores dK_S/dV_S.  Schedule and dense
+    baseline against the oracle."""
+    import torch
+    from paper_2606_01143_amd import binding as B
+    from paper_2606_01143_amd.group import DeviceGroup
+    shape = GroupShape(4, 1, 128, 0, (1500, 700), "bf16")
+    _announce(f"row shares, no prefix {shape}")
+    inp = make_group(shape, seed=16)
+    grp = DeviceGroup(inp, dense=True)
+    B.profile_reset()
+    B.profile_enable(True)
+    try:
+        grp.run_schedule(overlap=False)
+        grp.run_dense()
+        torch.cuda.synchronize()
+        _, n = B.profile_query("bwd_kv_combine")
+    finally:
+        B.profile_enable(False)
+    assert n == 2 * shape.n, n  # every suffix backward and every dense trajectory split
+    _check(grp.fetch("schedule"), three_phase_reference(inp), SCHED_KEYS, "schedule, P = 0")
+    _check(grp.fetch("dense"), dense_group_reference(inp), DENSE_KEYS, "dense, P = 0")

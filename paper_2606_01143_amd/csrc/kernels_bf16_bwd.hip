@@ -76,7 +76,7 @@ struct KvLds {
   bf16 o[kKvBufs][TE];
   float l[kKvBufs][64];  // log2-domain LSE of the tile's rows (32 used)
   float e[kKvBufs][64];  // rowsum(dO * O) of the tile's rows (32 used)
-  float4 p[2][2][4][64];  // P exchange [tile parity][key block][quarter][lane]
+  bf16x8 p[2][2][2][64];  // P exchange (bf16) [tile parity][key block][k-step v][lane]
 };
 
 template <int D>
@@ -270,7 +270,7 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
   auto compute = [&](int tc, const RowTile& rt, const int b) {
     const bf16* Qc = L.q[b];
     const bf16* Oc = L.o[b];
-    float4* px = &L.p[tc & 1][kb][0][lane];  // quarter q at px[64 q]
+    bf16x8* px = &L.p[tc & 1][kb][0][lane];  // k-step v at px[64 v]
     f32x16 c = product(pw ? Qc : Oc);
     bf16x8 ops[2];
     if (pw) {
@@ -292,21 +292,22 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
       }
       ops[0] = c_kfrag(c, 0);
       ops[1] = c_kfrag(c, 1);
-      // P in fp32 for the dS-wave (no unpacking on its side)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) px[64 * q] = make_float4(c[4 * q], c[4 * q + 1], c[4 * q + 2], c[4 * q + 3]);
+      // the bf16 operands of dV^T += dO^T P also go to the dS-wave
+      px[0] = ops[0];
+      px[64] = ops[1];
     } else {
       // P of this tile was written by the P-wave one barrier ago
       const float* Ec = L.e[b];
       f32x16 ds;
+      const bf16x8 pv[2] = {px[0], px[64]};  // C elements 8 v .. 8 v + 7
 #pragma unroll
       for (int g4 = 0; g4 < 4; ++g4) {
         const float4 e4 = *(const float4*)(Ec + 8 * g4 + 4 * h);
-        const float4 p4 = px[64 * g4];
-        ds[4 * g4 + 0] = p4.x * (c[4 * g4 + 0] - e4.x);
-        ds[4 * g4 + 1] = p4.y * (c[4 * g4 + 1] - e4.y);
-        ds[4 * g4 + 2] = p4.z * (c[4 * g4 + 2] - e4.z);
-        ds[4 * g4 + 3] = p4.w * (c[4 * g4 + 3] - e4.w);
+        const int v = g4 >> 1, j0 = 4 * (g4 & 1);
+        ds[4 * g4 + 0] = (float)pv[v][j0 + 0] * (c[4 * g4 + 0] - e4.x);
+        ds[4 * g4 + 1] = (float)pv[v][j0 + 1] * (c[4 * g4 + 1] - e4.y);
+        ds[4 * g4 + 2] = (float)pv[v][j0 + 2] * (c[4 * g4 + 2] - e4.z);
+        ds[4 * g4 + 3] = (float)pv[v][j0 + 3] * (c[4 * g4 + 3] - e4.w);
       }
       ops[0] = c_kfrag(ds, 0);
       ops[1] = c_kfrag(ds, 1);

@@ -22,7 +22,10 @@ around each of its launches over the same steps run again in serial order
 the last timed step, where it shares the GPU with the suffix forwards.
 ``roofline.traffic`` is taken from the committed FETCH_SIZE /
 WRITE_SIZE counter summary of the dominant kernel when that summary was made
-from the kernel sources in the tree (else null).
+from the kernel sources in the tree (else null); ``roofline.mfma_util`` is
+the matrix-core utilisation (busy cycles over elapsed cycles of all SIMDs)
+of its Phase B and Phase C launches, from the committed counter summary,
+under the same condition and on the headline workload only.
 
 Prints ONE JSON line.  ``--sweep c3|c4|c5attn|all`` instead prints one JSON
 line per configuration of the speedup surface (schedule vs dense, no CPU
@@ -58,6 +61,10 @@ KERNEL_FLOP_PER_PAIR_PER_D = {"fwd_bf16": 4, "bwd_bf16": 10}
 # committed counter summary of the dominant kernel's HBM traffic, and the
 # sources whose hash it records
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "bwd_bf16_traffic_llama3_8b_p4096_n8_s512.md")
+# the headline workload (Llama3-8B attention group, P = 4096, N = 8 x 512)
+DEFAULT_WORKLOAD = "llama3_8b_p4096_n8_s512"
+# committed counter summary of the matrix-core utilisation (same workload)
+MFMA_SUMMARY = os.path.join(ROOT, "profiles", "mfma_util_llama3_8b_p4096_n8_s512.md")
 BWD_SOURCES = ["kernels_bf16_bwd.hip", "tile.hpp", "common.hpp"]
 SWEEPS = {
     "c3": [f"qwen3_8b_p{p}_n{n}" for p in (2048, 8192, 16384) for n in (4, 8, 16)],
@@ -114,6 +121,21 @@ def committed_traffic():
     if m_hash.group(1) != bwd_source_hash():
         return None, "kernel changed since the counters were taken"
     return float(m_val.group(1)), os.path.relpath(TRAFFIC_SUMMARY, ROOT)
+
+
+def committed_mfma_util():
+    """{"phase_b": %, "phase_c": %, "source": path} from the counter summary
+    of the dominant kernel's matrix-core utilisation, or None."""
+    if not os.path.exists(MFMA_SUMMARY):
+        return None
+    text = open(MFMA_SUMMARY).read()
+    m_hash = re.search(r"kernel source hash: `([0-9a-f]+)`", text)
+    m_val = re.search(r"MfmaUtil % per launch: Phase B `([0-9.]+)`, Phase C `([0-9.]+)`", text)
+    if not m_hash or not m_val or m_hash.group(1) != bwd_source_hash():
+        return None
+    return {"phase_b_pct": float(m_val.group(1)), "phase_c_pct": float(m_val.group(2)),
+            "counter": "SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE x 1024 SIMDs)",
+            "source": os.path.relpath(MFMA_SUMMARY, ROOT)}
 
 
 def phase_times(grp, mbs):
@@ -207,7 +229,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="llama3_8b_p4096_n8_s512")
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--policy", choices=["per_suffix", "packed"], default="per_suffix")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-dense", action="store_true")
@@ -355,6 +377,8 @@ def main():
                        "frac": round(iso_achieved / BF16_PEAK_TFLOPS, 4), "traffic": traffic,
                        "traffic_unit": "HBM bytes per launch", "traffic_source": traffic_src,
                        "kernel": dominant,
+                       "mfma_util": (committed_mfma_util() if dominant == "bwd_bf16"
+                                     and args.workload == DEFAULT_WORKLOAD else None),
                        "flop_per_pair": f"{KERNEL_FLOP_PER_PAIR_PER_D[dominant]}d",
                        "launches_per_step": iso_count // max(args.steps, 1),
                        "avg_launch_ms": round(iso_ms / max(iso_count, 1), 4),

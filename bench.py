@@ -10,9 +10,16 @@ from one extra step in serial order.  The dense-recompute baseline (full causal 
 every [P||S(i)], one sequence at a time) is timed the same way on the same
 GPU for the speedup.
 
+The default workload is the long-context Llama3-8B attention group (GQA
+32/8, d = 128, P = 28672, N = 8 suffixes of 128 tokens): the largest group
+of the configurations that one GPU holds.  ``--workload`` selects another.
+
 value = useful TFLOP/s = 14 d FLOP per visible (query row, key) pair per q
 head that the schedule computes (4d forward + 10d backward), divided by the
-step time.  The dense baseline's extra work is never counted.
+mean step time; the median and minimum of the per-step times are reported
+beside it.  The dense baseline's extra work is never counted.  The other
+batching policy (all suffixes packed into one microbatch) is timed on the
+same inputs and reported beside the headline's.
 
 Also reported: per-phase times of one step, the standalone gK/gV cache
 accumulate (G += g, HBM-bound) against 8 TB/s, and the 12d (no S recompute)
@@ -51,20 +58,30 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "prefix-shared attn fwd+bwd TFLOP/s (% MFMA peak) + speedup vs dense recompute"
-BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+# MI355X dense bf16 MFMA peak, the published 2.5 PFLOP/s at its clock:
+# 256 CUs x 4096 flop per CU per clock x 2.4 GHz
+BF16_PEAK_TFLOPS = 256 * 4096 * 2.4e9 / 1e12
 HBM_PEAK_GBS = 8000.0
 # algorithmic FLOP per visible (row, key) pair per q head of each matrix-core
 # kernel: forward QK^T + PV (4d); backward S recompute, dP, dV, dK, dQ (10d,
 # the usual flash-attention count: the backward kernel's second S/dP pass
 # for dQ is implementation overhead and is not counted)
 KERNEL_FLOP_PER_PAIR_PER_D = {"fwd_bf16": 4, "bwd_bf16": 10}
-# committed counter summary of the dominant kernel's HBM traffic, and the
-# sources whose hash it records
-TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "bwd_bf16_traffic_llama3_8b_p4096_n8_s512.md")
-# the headline workload (Llama3-8B attention group, P = 4096, N = 8 x 512)
-DEFAULT_WORKLOAD = "llama3_8b_p4096_n8_s512"
-# committed counter summary of the matrix-core utilisation (same workload)
-MFMA_SUMMARY = os.path.join(ROOT, "profiles", "mfma_util_llama3_8b_p4096_n8_s512.md")
+# the headline workload: the long-context Llama3-8B attention group (GQA
+# 32/8, d = 128, P = 28672, N = 8 suffixes of 128), the largest group that
+# the configurations put on one GPU
+DEFAULT_WORKLOAD = "llama3_8b_p28672_n8_s128"
+
+
+def traffic_summary(workload: str) -> str:
+    """Committed counter summary of the dominant kernel's HBM traffic."""
+    return os.path.join(ROOT, "profiles", f"bwd_bf16_traffic_{workload}.md")
+
+
+def mfma_summary(workload: str) -> str:
+    """Committed counter summary of the matrix-core utilisation."""
+    return os.path.join(ROOT, "profiles", f"mfma_util_{workload}.md")
+
 BWD_SOURCES = ["kernels_bf16_bwd.hip", "tile.hpp", "common.hpp"]
 SWEEPS = {
     "c3": [f"qwen3_8b_p{p}_n{n}" for p in (2048, 8192, 16384) for n in (4, 8, 16)],
@@ -109,33 +126,35 @@ def bwd_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def committed_traffic():
+def committed_traffic(workload: str):
     """(bytes per launch, note) from the counter summary, or (None, why)."""
-    if not os.path.exists(TRAFFIC_SUMMARY):
-        return None, "no counter summary"
-    text = open(TRAFFIC_SUMMARY).read()
+    path = traffic_summary(workload)
+    if not os.path.exists(path):
+        return None, "no counter summary for this workload"
+    text = open(path).read()
     m_hash = re.search(r"kernel source hash: `([0-9a-f]+)`", text)
     m_val = re.search(r"HBM bytes per launch \(calibrated\): `([0-9.eE+]+)`", text)
     if not m_hash or not m_val:
         return None, "summary unreadable"
     if m_hash.group(1) != bwd_source_hash():
         return None, "kernel changed since the counters were taken"
-    return float(m_val.group(1)), os.path.relpath(TRAFFIC_SUMMARY, ROOT)
+    return float(m_val.group(1)), os.path.relpath(path, ROOT)
 
 
-def committed_mfma_util():
+def committed_mfma_util(workload: str):
     """{"phase_b": %, "phase_c": %, "source": path} from the counter summary
     of the dominant kernel's matrix-core utilisation, or None."""
-    if not os.path.exists(MFMA_SUMMARY):
+    path = mfma_summary(workload)
+    if not os.path.exists(path):
         return None
-    text = open(MFMA_SUMMARY).read()
+    text = open(path).read()
     m_hash = re.search(r"kernel source hash: `([0-9a-f]+)`", text)
     m_val = re.search(r"MfmaUtil % per launch: Phase B `([0-9.]+)`, Phase C `([0-9.]+)`", text)
     if not m_hash or not m_val or m_hash.group(1) != bwd_source_hash():
         return None
     return {"phase_b_pct": float(m_val.group(1)), "phase_c_pct": float(m_val.group(2)),
             "counter": "SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE x 1024 SIMDs)",
-            "source": os.path.relpath(MFMA_SUMMARY, ROOT)}
+            "source": os.path.relpath(path, ROOT)}
 
 
 def phase_times(grp, mbs):
@@ -173,55 +192,104 @@ def gkv_accumulate_rate(grp, reps: int = 20):
             "bytes_per_call": nbytes, "ms_per_call": round(ms, 4)}
 
 
-def time_steps(fn, steps: int, warmup: int):
+def time_steps_stats(fn, steps: int, warmup: int):
+    """Mean, median and minimum milliseconds per step: one event between
+    consecutive steps on the current stream (the mean is the whole span over
+    the steps)."""
+    import statistics
     import torch
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    start.record()
-    for _ in range(steps):
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    ev[0].record()
+    for i in range(steps):
         fn()
-    end.record()
+        ev[i + 1].record()
     torch.cuda.synchronize()
-    return start.elapsed_time(end) / steps
+    per = [ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]
+    return {"mean": ev[0].elapsed_time(ev[-1]) / steps, "median": statistics.median(per),
+            "min": min(per)}
+
+
+def time_steps(fn, steps: int, warmup: int):
+    return time_steps_stats(fn, steps, warmup)["mean"]
+
+
+def host_facts():
+    """Host cores the process may use, BLAS vendor and thread pool, CPU model."""
+    facts = {"cores": len(os.sched_getaffinity(0)), "blas": "unknown", "blas_threads": None,
+             "cpu_model": "unknown"}
+    try:
+        from threadpoolctl import threadpool_info
+        blas = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        if blas:
+            facts["blas"] = f"{blas[0].get('internal_api')} {blas[0].get('version')}"
+            facts["blas_threads"] = int(blas[0].get("num_threads", 1))
+    except Exception:  # pragma: no cover
+        pass
+    try:
+        import subprocess
+        txt = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in txt.splitlines():
+            if line.strip().startswith("Model name"):
+                facts["cpu_model"] = line.split(":", 1)[1].strip()
+                return facts
+    except Exception:  # pragma: no cover
+        pass
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    facts["cpu_model"] = line.split(":", 1)[1].strip()
+                    break
+    except OSError:  # pragma: no cover
+        pass
+    return facts
 
 
 def cpu_baseline(inp, shape, budget_s: float):
-    """The fp64 oracle's three-phase reference on a bounded sample: the G query
-    heads of one kv head (heads are independent), repeated while time allows."""
-    import numpy as np
+    """The fp64 oracle's three-phase reference on a bounded sample of the same
+    group: one q head at a time with its kv head (heads are independent, so
+    each is the same schedule on a one-head group), until the time budget is
+    spent; the BLAS pool uses every core the process may run on."""
     from oracle import three_phase_reference
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
-    except Exception:  # pragma: no cover
-        threads = os.cpu_count() or 1
     from synthetic import GroupShape
+    facts = host_facts()
+    try:
+        from threadpoolctl import threadpool_limits
+        limiter = threadpool_limits(limits=facts["cores"], user_api="blas")
+        facts["blas_threads"] = facts["cores"]
+    except Exception:  # pragma: no cover
+        limiter = None
     g = shape.group
-    done, t0, flops = 0, time.perf_counter(), 0.0
     pre, suf, _ = pair_counts(shape)
-    per_group_flops = 14 * shape.head_dim * g * (pre + sum(suf))
+    per_head_flops = 14 * shape.head_dim * (pre + sum(suf))
+    done, t0 = 0, time.perf_counter()
     while True:
-        kv = done % shape.num_kv_heads
-        qh = slice(kv * g, (kv + 1) * g)
+        h = done % shape.num_q_heads
+        kv = h // g
         sub = dict(inp)
         for k in ("q_p", "q_s", "do_s", "g_y"):
-            sub[k] = inp[k][:, qh]
+            sub[k] = inp[k][:, h:h + 1]
+        sub["do_p"] = inp["do_p"][:, :, h:h + 1]
         for k in ("k_p", "v_p", "k_s", "v_s"):
             sub[k] = inp[k][:, kv:kv + 1]
-        sub["shape"] = GroupShape(g, 1, shape.head_dim, shape.prefix_len, shape.suffix_lens,
+        sub["shape"] = GroupShape(1, 1, shape.head_dim, shape.prefix_len, shape.suffix_lens,
                                   shape.dtype)
         three_phase_reference(sub)
         done += 1
-        flops += per_group_flops
         el = time.perf_counter() - t0
-        if el >= budget_s or done >= shape.num_kv_heads:
+        if el >= budget_s or done >= shape.num_q_heads:
             break
-    return {"value": round(flops / el / 1e12, 6), "unit": "TFLOP/s", "cores": int(threads),
-            "kind": "oracle",
-            "sample": f"fp64 three-phase oracle on {done} of {shape.num_kv_heads} kv-head groups "
-                      f"({g} q heads each) of the same group, {el:.1f} s wall"}
+    if limiter is not None:
+        limiter.restore_original_limits()
+    return {"value": round(done * per_head_flops / el / 1e12, 6), "unit": "TFLOP/s",
+            "cores": int(facts["blas_threads"] or facts["cores"]), "kind": "oracle",
+            "sample": f"fp64 three-phase oracle (NumPy) on {done} of {shape.num_q_heads} q heads of "
+                      f"the same group, each with its kv head, {el:.1f} s wall; "
+                      f"value = those heads' 14d FLOP per visible pair / wall time",
+            "host_cores": facts["cores"], "cpu_model": facts["cpu_model"], "blas": facts["blas"]}
 
 
 def main():
@@ -233,7 +301,8 @@ def main():
     ap.add_argument("--policy", choices=["per_suffix", "packed"], default="per_suffix")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-dense", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--cpu-seconds", type=float, default=20.0,
+                    help="time budget of the CPU oracle baseline (0: skip it)")
     ap.add_argument("--sweep", choices=["c3", "c4", "c5attn", "all"], default=None)
     ap.add_argument("--layout", choices=["packed", "padded"], default="packed",
                     help="suffix layout of Phase B (padded: batch-plus-padding calls)")
@@ -279,9 +348,11 @@ def main():
     inp = workload(args.workload, args.seed)
     shape = inp["shape"]
     n = shape.n
-    mbs = [(i, i + 1) for i in range(n)] if args.policy == "per_suffix" else [(0, n)]
-    grp = DeviceGroup(inp, device="cuda:0", dense=not args.no_dense, microbatch_splits=[mbs],
-                      layout=args.layout)
+    per_suffix = [(i, i + 1) for i in range(n)]
+    packed = [(0, n)]
+    mbs = per_suffix if args.policy == "per_suffix" else packed
+    grp = DeviceGroup(inp, device="cuda:0", dense=not args.no_dense,
+                      microbatch_splits=[per_suffix, packed], layout=args.layout)
     grp.prepare(mbs)
     torch.cuda.synchronize()
 
@@ -289,6 +360,7 @@ def main():
     hq, d = shape.num_q_heads, shape.head_dim
     sched_flops = 14 * d * hq * (pre + sum(suf))
     dense_flops = 14 * d * hq * sum(dense_pairs)
+    tf = lambda flop, ms: flop / (ms * 1e-3) / 1e12
 
     log("schedule warmup")
     for _ in range(args.warmup):
@@ -318,7 +390,8 @@ def main():
         grp.run_schedule(mbs)
 
     B.profile_reset()
-    ms_step = time_steps(step, args.steps, 0)
+    st = time_steps_stats(step, args.steps, 0)
+    ms_step = st["mean"]
     B.profile_enable(False)
     dom_ms, dom_count = B.profile_query(dominant)
     # algorithmic FLOP of all launches of the dominant kernel in one step:
@@ -327,9 +400,10 @@ def main():
     dom_flops_per_step = KERNEL_FLOP_PER_PAIR_PER_D[dominant] * d * hq * (pre + sum(suf))
     dom_avg_ms = dom_ms / max(dom_count, 1)
     dom_achieved = dom_flops_per_step / (dom_ms * 1e-3) / 1e12 if dom_ms > 0 else 0.0
-    value = sched_flops / (ms_step * 1e-3) / 1e12
-    log(f"schedule {ms_step:.3f} ms/step, {value:.1f} TFLOP/s; {dominant} "
-        f"{dom_count} launches avg {dom_avg_ms:.3f} ms -> {dom_achieved:.1f} TFLOP/s")
+    value = tf(sched_flops, ms_step)
+    log(f"schedule {ms_step:.3f} ms/step (median {st['median']:.3f}, min {st['min']:.3f}), "
+        f"{value:.1f} TFLOP/s; {dominant} {dom_count} launches avg {dom_avg_ms:.3f} ms "
+        f"-> {dom_achieved:.1f} TFLOP/s")
 
     # the same steps in serial order, events around every launch of the
     # dominant kernel: its own rate, alone on the GPU (the roofline)
@@ -341,10 +415,19 @@ def main():
     iso_ms, iso_count = B.profile_query(dominant)
     iso_achieved = dom_flops_per_step * args.steps / (iso_ms * 1e-3) / 1e12 if iso_ms > 0 else 0.0
     phases = phase_times(grp, mbs)
+    # per-phase rates of the serial step: algorithmic FLOP of each phase over
+    # its time (forward 4d, backward 10d per visible pair)
+    sp = sum(suf)
+    phase_flops = {"A": 4 * d * hq * pre, "B_fwd": 4 * d * hq * sp, "B_bwd": 10 * d * hq * sp,
+                   "C": 10 * d * hq * pre}
+    phase_rates = {k: {"tflops": round(tf(f, phases[k]), 1),
+                       "pct_peak": round(100 * tf(f, phases[k]) / BF16_PEAK_TFLOPS, 2)}
+                   for k, f in phase_flops.items() if phases.get(k, 0) > 0}
     gkv = gkv_accumulate_rate(grp)
     out = {
         "metric": METRIC, "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+        "ms_per_step_median": round(st["median"], 4), "ms_per_step_min": round(st["min"], 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": args.workload, "num_q_heads": hq,
@@ -354,31 +437,52 @@ def main():
                    else shape.suffix_lens[0],
                    "microbatching": args.policy, "layout": args.layout},
         "pct_mfma_peak": round(100 * value / BF16_PEAK_TFLOPS, 2),
+        "value_at_median": round(tf(sched_flops, st["median"]), 3),
         "schedule_tflop_per_step": round(sched_flops / 1e12, 4),
         "kernel_ms_one_step": per_kernel,
         "phases_ms": phases,
+        "phase_rates": phase_rates,
         "ms_per_step_serial_order": round(ms_serial, 4),
         "value_12d_tflops": round(value * 12 / 14, 3),
         "gkv_accumulate": gkv,
     }
 
+    # the other batching policy on the same inputs: all suffixes packed into
+    # one microbatch (policy (ii)) when the headline runs one per microbatch,
+    # and the reverse
+    other = packed if mbs is per_suffix else per_suffix
+    other_name = "packed" if mbs is per_suffix else "per_suffix"
+    grp.prepare(other)
+    st_o = time_steps_stats(lambda: grp.run_schedule(other), args.steps, 1)
+    out["policy_" + other_name] = {"ms_per_step": round(st_o["mean"], 4),
+                                   "ms_per_step_median": round(st_o["median"], 4),
+                                   "ms_per_step_min": round(st_o["min"], 4),
+                                   "value": round(tf(sched_flops, st_o["mean"]), 3)}
+    log(f"schedule, {other_name} microbatches: {st_o['mean']:.3f} ms/step")
+
     if not args.no_dense:
         log("dense baseline warmup + timed steps")
-        ms_dense = time_steps(lambda: grp.run_dense(), max(3, args.steps // 2), 1)
+        st_d = time_steps_stats(lambda: grp.run_dense(), max(3, args.steps // 2), 1)
+        ms_dense = st_d["mean"]
         out["dense_ms_per_step"] = round(ms_dense, 4)
+        out["dense_ms_per_step_median"] = round(st_d["median"], 4)
+        out["dense_ms_per_step_min"] = round(st_d["min"], 4)
         out["speedup_vs_dense"] = round(ms_dense / ms_step, 3)
-        out["dense_equiv_tflops"] = round(dense_flops / (ms_dense * 1e-3) / 1e12, 3)
+        out["dense_equiv_tflops"] = round(tf(dense_flops, ms_dense), 3)
         out["flop_ratio_dense_over_schedule"] = round(dense_flops / sched_flops, 3)
+        out["policy_" + other_name]["speedup_vs_dense"] = round(ms_dense / st_o["mean"], 3)
+        out["dense_policy"] = "one trajectory per launch pair (the dense trainer's per-sequence order)"
         log(f"dense {ms_dense:.3f} ms/step, speedup {ms_dense / ms_step:.2f}x")
 
-    traffic, traffic_src = committed_traffic() if dominant == "bwd_bf16" else (None, "n/a")
+    traffic, traffic_src = (committed_traffic(args.workload) if dominant == "bwd_bf16"
+                            else (None, "n/a"))
     out["roofline"] = {"bound": "mfma", "achieved": round(iso_achieved, 2),
-                       "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                       "peak": round(BF16_PEAK_TFLOPS, 1), "unit": "TFLOP/s",
                        "frac": round(iso_achieved / BF16_PEAK_TFLOPS, 4), "traffic": traffic,
                        "traffic_unit": "HBM bytes per launch", "traffic_source": traffic_src,
                        "kernel": dominant,
-                       "mfma_util": (committed_mfma_util() if dominant == "bwd_bf16"
-                                     and args.workload == DEFAULT_WORKLOAD else None),
+                       "mfma_util": (committed_mfma_util(args.workload)
+                                     if dominant == "bwd_bf16" else None),
                        "flop_per_pair": f"{KERNEL_FLOP_PER_PAIR_PER_D[dominant]}d",
                        "launches_per_step": iso_count // max(args.steps, 1),
                        "avg_launch_ms": round(iso_ms / max(iso_count, 1), 4),
@@ -389,8 +493,11 @@ def main():
                                    "frac": round(dom_achieved / BF16_PEAK_TFLOPS, 4),
                                    "avg_launch_ms": round(dom_avg_ms, 4),
                                    "measured": "HIP events around each launch of the last timed step"}}
-    log("cpu baseline (oracle)")
-    out["cpu_baseline"] = cpu_baseline(inp, shape, args.cpu_seconds)
+    del grp
+    torch.cuda.empty_cache()
+    if args.cpu_seconds > 0:
+        log("cpu baseline (oracle)")
+        out["cpu_baseline"] = cpu_baseline(inp, shape, args.cpu_seconds)
     print(json.dumps(out), flush=True)
 
 

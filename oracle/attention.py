@@ -136,6 +136,111 @@ def sampled_rows_reference(inp: Dict[str, np.ndarray], prefix_rows, suffix_rows,
     return out
 
 
+def causal_forward_rows(q, k, v, scale, *, first_query_pos=0):
+    """The forward half of ``causal_attention``: O and the row LSE of query
+    rows at positions first_query_pos .. first_query_pos + Lq - 1 of one
+    sequence whose keys/values sit at positions 0 .. Lk - 1 (key j visible
+    to position r iff j <= r).  Rows are taken in chunks and each chunk only
+    against the keys its last row sees (memory only).  Returns o [Lq, Hq, d]
+    and lse [Hq, Lq]."""
+    q, k, v = _f64(q), _f64(k), _f64(v)
+    lq, hq, d = q.shape
+    g = hq // k.shape[1]
+    o = np.zeros_like(q)
+    lse = np.zeros((hq, lq))
+    for r0 in range(0, lq, _CHUNK):
+        r1 = min(lq, r0 + _CHUNK)
+        pos = first_query_pos + np.arange(r0, r1)
+        nk = min(k.shape[0], int(pos[-1]) + 1)
+        hidden = np.arange(nk)[None, :] > pos[:, None]
+        for h in range(hq):
+            s = scale * (q[r0:r1, h, :] @ k[:nk, h // g, :].T)
+            s[hidden] = -np.inf
+            p, lse[h, r0:r1] = _softmax_rows(s)
+            o[r0:r1, h, :] = p @ v[:nk, h // g, :]
+    return o, lse
+
+
+def sampled_keys_reference(inp: Dict[str, np.ndarray], prefix_keys, suffix_keys,
+                           scale: Optional[float] = None) -> Dict[str, Dict]:
+    """dK and dV of a few keys of a group, and for prefix keys the cache
+    values gK, gV, each from its own sequences' definition (Sec. 2.1).
+
+    prefix_keys: prefix positions j.  Key j is seen by the prefix rows
+    r >= j of every trajectory (with that trajectory's dO_P(i)) and by every
+    suffix row of every trajectory; its gradient is the sum over all those
+    uses.  gK(j) and gV(j) are the suffix rows' part of it (App. A.3: the
+    suffix-row x prefix-key block, summed over i).
+    suffix_keys: pairs (i, t), key t of suffix i, seen by the rows u >= t of
+    suffix i only.
+    Every row's probabilities come from its own LSE and O (computed by
+    ``causal_forward_rows`` over the row's visible keys), then per key
+    P = exp(s - LSE), dP = dO . v, D = dO . O, dS = P (dP - D),
+    dK = scale sum dS q, dV = sum P dO, summed over the G query heads of
+    the key's kv head.  For groups too large for the full oracle: the cost
+    is one forward over the rows that see a sampled key, plus one column of
+    scores per sampled key."""
+    shp = inp["shape"]
+    sc = _default_scale(shp.head_dim, scale)
+    P, n, cu = shp.prefix_len, shp.n, np.asarray(inp["cu_seqlens"], np.int64)
+    hq, hkv = shp.num_q_heads, shp.num_kv_heads
+    g = hq // hkv
+    q_p, k_p, v_p = _f64(inp["q_p"]), _f64(inp["k_p"]), _f64(inp["v_p"])
+    out = {"prefix": {}, "suffix": {}}
+    prefix_keys = sorted(set(int(j) for j in prefix_keys))
+    need_sfx = set(i for i, _ in suffix_keys) | (set(range(n)) if prefix_keys else set())
+    # forward statistics of every row that sees a sampled key
+    sfx = {}
+    for i in sorted(need_sfx):
+        a, b = int(cu[i]), int(cu[i + 1])
+        kk = np.concatenate([k_p, _f64(inp["k_s"][a:b])], axis=0)
+        vv = np.concatenate([v_p, _f64(inp["v_s"][a:b])], axis=0)
+        q_i, do_i = _f64(inp["q_s"][a:b]), _f64(inp["do_s"][a:b])
+        o_i, lse_i = causal_forward_rows(q_i, kk, vv, sc, first_query_pos=P)
+        sfx[i] = (q_i, do_i, lse_i, np.einsum("thd,thd->ht", do_i, o_i))
+    if prefix_keys:
+        r_min = prefix_keys[0]
+        o_p, lse_p = causal_forward_rows(q_p[r_min:], k_p, v_p, sc, first_query_pos=r_min)
+        do_p = _f64(inp["do_p"][:, r_min:])                      # [N, P - r_min, Hq, d]
+        d_p = np.einsum("nrhd,rhd->nhr", do_p, o_p)             # D of each trajectory's prefix rows
+        qp = q_p[r_min:]
+    for j in prefix_keys:
+        dk, dv = np.zeros((hkv, shp.head_dim)), np.zeros((hkv, shp.head_dim))
+        gk, gv = np.zeros_like(dk), np.zeros_like(dv)
+        for h in range(hq):
+            kv = h // g
+            kj, vj = k_p[j, kv], v_p[j, kv]
+            # prefix rows r >= j, the same probabilities in every trajectory
+            rows = slice(j - r_min, P - r_min)
+            p = np.exp(sc * (qp[rows, h] @ kj) - lse_p[h, rows])
+            for i in range(n):
+                doi = do_p[i, rows, h]
+                ds = p * (doi @ vj - d_p[i, h, rows])
+                dk[kv] += sc * (ds @ qp[rows, h])
+                dv[kv] += p @ doi
+            # every suffix row of every trajectory
+            for i in range(n):
+                q_i, do_i, lse_i, d_i = sfx[i]
+                p = np.exp(sc * (q_i[:, h] @ kj) - lse_i[h])
+                ds = p * (do_i[:, h] @ vj - d_i[h])
+                gk[kv] += sc * (ds @ q_i[:, h])
+                gv[kv] += p @ do_i[:, h]
+        out["prefix"][j] = {"dk": dk + gk, "dv": dv + gv, "g_k": gk, "g_v": gv}
+    for i, t in suffix_keys:
+        a = int(cu[i])
+        q_i, do_i, lse_i, d_i = sfx[i]
+        dk, dv = np.zeros((hkv, shp.head_dim)), np.zeros((hkv, shp.head_dim))
+        for h in range(hq):
+            kv = h // g
+            kj, vj = _f64(inp["k_s"][a + t, kv]), _f64(inp["v_s"][a + t, kv])
+            p = np.exp(sc * (q_i[t:, h] @ kj) - lse_i[h, t:])
+            ds = p * (do_i[t:, h] @ vj - d_i[h, t:])
+            dk[kv] += sc * (ds @ q_i[t:, h])
+            dv[kv] += p @ do_i[t:, h]
+        out["suffix"][(i, t)] = {"dk": dk, "dv": dv}
+    return out
+
+
 def _default_scale(d: int, scale: Optional[float]) -> float:
     return 1.0 / np.sqrt(d) if not scale else float(scale)
 

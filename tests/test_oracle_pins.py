@@ -339,3 +339,43 @@ def test_sampled_rows_equal_full_oracle_rows():
         assert np.abs(v["o"] - ref["o_s"][row]).max() < 1e-12
         assert np.abs(v["dq"] - ref["dq_s"][row]).max() < 1e-12
         assert np.abs(v["lse"] - ref["lse_s"][:, row]).max() < 1e-12
+
+
+@pytest.mark.parametrize("shape,ragged", [
+    (GroupShape(4, 2, 16, 20, (5, 9), "f32"), None),
+    (GroupShape(8, 2, 8, 70, (3, 1, 40), "bf16"), None),
+    (GroupShape(4, 1, 8, 33, (0,) * 3, "bf16"), (1, 9)),
+])
+def test_sampled_keys_equal_full_oracle_keys(shape, ragged):
+    """The per-key reference used at full size equals the full oracle's
+    dK/dV rows and cache rows, at prefix keys including the first and last
+    and at the first, middle and last key of each suffix."""
+    from oracle.attention import sampled_keys_reference
+    inp = make_group(shape, seed=5, ragged=ragged)
+    shp = inp["shape"]
+    ref = dense_group_reference(inp)
+    P, lens = shp.prefix_len, shp.suffix_lens
+    pk = sorted({0, 1, P // 2, P - 2, P - 1})
+    sk = sorted({(i, t) for i in range(shp.n) for t in (0, lens[i] // 2, lens[i] - 1)})
+    smp = sampled_keys_reference(inp, pk, sk)
+    for j, v in smp["prefix"].items():
+        for f, rk in (("dk", "dk_p"), ("dv", "dv_p"), ("g_k", "g_k"), ("g_v", "g_v")):
+            assert np.abs(v[f] - ref[rk][j]).max() < 1e-11, (j, f)
+    cu = inp["cu_seqlens"]
+    for (i, t), v in smp["suffix"].items():
+        assert np.abs(v["dk"] - ref["dk_s"][cu[i] + t]).max() < 1e-11, (i, t)
+        assert np.abs(v["dv"] - ref["dv_s"][cu[i] + t]).max() < 1e-11, (i, t)
+
+
+def test_causal_forward_rows_equals_full_oracle_forward():
+    """The forward-only row function equals the full oracle's O and LSE, also
+    for a row range that starts inside the sequence."""
+    from oracle.attention import causal_forward_rows, causal_attention
+    rng = np.random.default_rng(3)
+    q, k, v, do = (rng.standard_normal((2500, 4, 8)), rng.standard_normal((2500, 2, 8)),
+                   rng.standard_normal((2500, 2, 8)), rng.standard_normal((2500, 4, 8)))
+    o, lse, *_ = causal_attention(q, k, v, do, 0.3)
+    o2, lse2 = causal_forward_rows(q, k, v, 0.3)
+    assert np.abs(o - o2).max() < 1e-12 and np.abs(lse - lse2).max() < 1e-12
+    o3, lse3 = causal_forward_rows(q[1700:], k, v, 0.3, first_query_pos=1700)
+    assert np.abs(o[1700:] - o3).max() < 1e-12 and np.abs(lse[:, 1700:] - lse3).max() < 1e-12

@@ -34,8 +34,12 @@
  *          cu_seqlens is a DEVICE int32 array of n+1 entries with
  *          cu_seqlens[0] = 0, strictly increasing (every suffix has >= 1
  *          token), cu_seqlens[n] = total_len; max_len (host) is the longest
- *          suffix.  The library trusts these values (it does not read device
- *          memory on the host); inconsistent values give undefined results.
+ *          suffix.  The library does not read device memory on the host:
+ *          callers that hold a host copy validate it with
+ *          spr_check_cu_seqlens (the Python binding always does).  The
+ *          kernels clamp every offset into [0, total_len] and every segment
+ *          to a non-negative length, so inconsistent device values give
+ *          wrong rows but no access outside the caller's buffers.
  * Mask     Causal, inclusive of the diagonal.  A prefix row r sees prefix
  *          keys 0..r.  A suffix row at local position t sees every prefix key
  *          and keys 0..t of its own suffix, never another suffix (paper
@@ -137,6 +141,18 @@ spr_status spr_suffix_attn_fwd(const spr_dims* dims, const void* k_p, const void
                                const int32_t* cu_seqlens, int32_t n_mb, int32_t max_len,
                                int32_t total_len, void* o_s, float* lse_s, void* ws,
                                size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Host-side check of a packed microbatch's suffix offsets, for callers that
+ * hold a host copy of the cu_seqlens they upload (the library never reads
+ * device memory on the host).  SPR_OK iff cu_host[0] == 0, every suffix
+ * length cu_host[s+1] - cu_host[s] is in [1, max_len], the longest equals
+ * max_len and cu_host[n_mb] == total_len; otherwise SPR_ERR_INVALID_ARG
+ * naming the first violation (a zero-length suffix included).  Launches
+ * nothing.
+ */
+spr_status spr_check_cu_seqlens(const int32_t* cu_host, int32_t n_mb, int32_t max_len,
+                                int32_t total_len);
 
 /*
  * Phase B backward with gradient-cache accumulation (paper App. A.2-A.3):

@@ -50,6 +50,7 @@ _SIGNATURES = {
                                       c_int32, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
                                       c_size_t, _P], c_int32),
     "spr_workspace_size": ([c_int32, _P, c_int32, c_int32, c_int32, POINTER(c_size_t)], c_int32),
+    "spr_check_cu_seqlens": ([POINTER(c_int32), c_int32, c_int32, c_int32], c_int32),
     "spr_gkv_cache_zero": ([_P, _P, _P, _P], c_int32),
     "spr_gkv_accumulate": ([_P, _P, _P, _P, _P, _P], c_int32),
     "spr_rmsnorm_fwd": ([c_int32, c_int32, c_float, _P, _P, _P, _P], c_int32),
@@ -189,6 +190,17 @@ def _check(status: int) -> None:
         raise SprError(status, lib().spr_last_error().decode())
 
 
+def check_cu_seqlens(cu_host, n_mb, max_len, total_len) -> None:
+    """Host-side check of a microbatch's suffix offsets (the values uploaded
+    as cu_seqlens): raises SprError(SPR_ERR_INVALID_ARG) on a zero-length
+    suffix or offsets inconsistent with n_mb / max_len / total_len."""
+    vals = [int(x) for x in cu_host]
+    if len(vals) != int(n_mb) + 1:
+        raise SprError(1, f"cu_seqlens has {len(vals)} entries, n_mb + 1 = {int(n_mb) + 1} expected")
+    arr = (c_int32 * len(vals))(*vals)
+    _check(lib().spr_check_cu_seqlens(arr, n_mb, max_len, total_len))
+
+
 def _nbytes(ws) -> int:
     return 0 if ws is None else ws.numel() * ws.element_size()
 
@@ -204,7 +216,10 @@ def prefix_fwd(dims, q_p, k_p, v_p, o_p, lse_p, stream=None):
 
 
 def suffix_attn_fwd(dims, k_p, v_p, q_s, k_s, v_s, cu_seqlens, n_mb, max_len, total_len, o_s,
-                    lse_s, ws=None, stream=None):
+                    lse_s, ws=None, stream=None, cu_host=None):
+    """``cu_host``: the host copy of cu_seqlens, checked first when given."""
+    if cu_host is not None:
+        check_cu_seqlens(cu_host, n_mb, max_len, total_len)
     z = _Sizes(dims, total_len)
     z.kv(z.P, k_p=k_p, v_p=v_p)
     z.q(z.T, q_s=q_s, o_s=o_s)
@@ -219,7 +234,10 @@ def suffix_attn_fwd(dims, k_p, v_p, q_s, k_s, v_s, cu_seqlens, n_mb, max_len, to
 
 def suffix_attn_bwd_accum(dims, k_p, v_p, q_s, k_s, v_s, o_s, lse_s, do_s, cu_seqlens, n_mb,
                           max_len, total_len, dq_s, dk_s, dv_s, gk_cache, gv_cache, ws=None,
-                          stream=None):
+                          stream=None, cu_host=None):
+    """``cu_host``: the host copy of cu_seqlens, checked first when given."""
+    if cu_host is not None:
+        check_cu_seqlens(cu_host, n_mb, max_len, total_len)
     z = _Sizes(dims, total_len)
     z.kv(z.P, k_p=k_p, v_p=v_p)
     z.q(z.T, q_s=q_s, o_s=o_s, do_s=do_s, dq_s=dq_s)
@@ -300,7 +318,10 @@ def prefix_bwd_dkv(dims, q_p, k_p, v_p, o_p, lse_p, do_p, gk_cache, gv_cache, dk
 
 def dense_recompute_baseline(dims, q_p, k_p, v_p, do_p_seq, q_s, k_s, v_s, do_s, cu_seqlens, n,
                              max_len, total_len, o_p, lse_p, o_s, lse_s, dq_s, dk_s, dv_s, dq_p,
-                             dk_p, dv_p, ws=None, stream=None):
+                             dk_p, dv_p, ws=None, stream=None, cu_host=None):
+    """``cu_host``: the host copy of cu_seqlens, checked first when given."""
+    if cu_host is not None:
+        check_cu_seqlens(cu_host, n, max_len, total_len)
     z = _Sizes(dims, total_len)
     z.q(z.P, q_p=q_p, o_p=o_p, dq_p=dq_p)
     z.q(int(n) * z.P, do_p_seq=do_p_seq)
@@ -317,33 +338,55 @@ def dense_recompute_baseline(dims, q_p, k_p, v_p, do_p_seq, q_s, k_s, v_s, do_s,
         _ptr(dv_p), _ptr(ws), _nbytes(ws), _stream(stream)))
 
 
+def _need_all(elems, esize, **tensors):
+    """Every named tensor holds at least `elems` elements of `esize` bytes
+    (None: a NULL pointer, left to the library)."""
+    for name, x in tensors.items():
+        if x is None:
+            continue
+        if x.element_size() != esize:
+            raise ValueError(f"{name}: elements of {x.element_size()} bytes, the call needs {esize}")
+        if x.numel() < elems:
+            raise ValueError(f"{name}: {x.numel()} elements, the call needs {elems}")
+
+
 def rmsnorm_fwd(x, y, rstd, eps=1e-5, stream=None):
     rows, width = int(x.shape[0]), int(x.shape[-1])
+    _need_all(rows * width, 2, x=x, y=y)
+    _need_all(rows, 4, rstd=rstd)
     _check(lib().spr_rmsnorm_fwd(rows, width, eps, _ptr(x), _ptr(y), _ptr(rstd), _stream(stream)))
 
 
 def rmsnorm_bwd(x, rstd, dy, dx, add=None, stream=None):
     rows, width = int(x.shape[0]), int(x.shape[-1])
+    _need_all(rows * width, 2, x=x, dy=dy, dx=dx, add=add)
+    _need_all(rows, 4, rstd=rstd)
     _check(lib().spr_rmsnorm_bwd(rows, width, _ptr(x), _ptr(rstd), _ptr(dy), _ptr(add), _ptr(dx),
                                  _stream(stream)))
 
 
 def rope_fwd(x, y, pos0, theta, stream=None):
     t, h, d = (int(v) for v in x.shape)
+    _need_all(t * h * d, 2, x=x, y=y)
     _check(lib().spr_rope_fwd(t, h, d, pos0, float(theta), _ptr(x), _ptr(y), _stream(stream)))
 
 
 def rope_bwd(dy, dx, pos0, theta, stream=None):
     t, h, d = (int(v) for v in dy.shape)
+    _need_all(t * h * d, 2, dy=dy, dx=dx)
     _check(lib().spr_rope_bwd(t, h, d, pos0, float(theta), _ptr(dy), _ptr(dx), _stream(stream)))
 
 
 def swiglu_fwd(g, u, m, stream=None):
-    _check(lib().spr_swiglu_fwd(int(g.numel()), _ptr(g), _ptr(u), _ptr(m), _stream(stream)))
+    n = int(g.numel())
+    _need_all(n, 2, g=g, u=u, m=m)
+    _check(lib().spr_swiglu_fwd(n, _ptr(g), _ptr(u), _ptr(m), _stream(stream)))
 
 
 def swiglu_bwd(g, u, dm, dg, du, stream=None):
-    _check(lib().spr_swiglu_bwd(int(g.numel()), _ptr(g), _ptr(u), _ptr(dm), _ptr(dg), _ptr(du),
+    n = int(g.numel())
+    _need_all(n, 2, g=g, u=u, dm=dm, dg=dg, du=du)
+    _check(lib().spr_swiglu_bwd(n, _ptr(g), _ptr(u), _ptr(dm), _ptr(dg), _ptr(du),
                                 _stream(stream)))
 
 

@@ -124,4 +124,23 @@ __device__ __forceinline__ bf16 from_f32<bf16>(float x) { return (bf16)x; }
 
 __device__ __forceinline__ int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
+// First row and row count of packed suffix s: cu[s] .. cu[s+1]-1, clamped
+// into [0, total_len] with a non-negative count.  Offsets that break the
+// documented contract then give wrong rows but never an access outside the
+// caller's buffers.
+struct SegRows {
+  int base, len;
+};
+__device__ __forceinline__ SegRows suffix_rows(const int32_t* cu, int s, int total_len) {
+  const int lo = min(max(cu[s], 0), total_len);
+  const int hi = min(max(cu[s + 1], lo), total_len);
+  return {lo, hi - lo};
+}
+// The rows of suffixes s0 .. s1-1 together, clamped the same way.
+__device__ __forceinline__ SegRows suffix_span(const int32_t* cu, int s0, int s1, int total_len) {
+  const int lo = min(max(cu[s0], 0), total_len);
+  const int hi = min(max(cu[s1], lo), total_len);
+  return {lo, hi - lo};
+}
+
 }  // namespace spr

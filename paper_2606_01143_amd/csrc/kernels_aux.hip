@@ -26,12 +26,14 @@ int aux_blocks(size_t n_vec) {
 
 // LPR lanes per (row, head), each loading 16 consecutive bytes of dO and of
 // O, then a shuffle reduction over those lanes.  With cu != nullptr the rows
-// are those of suffix `seq` only: cu[seq] .. cu[seq+1]-1, and `rows` is an
-// upper bound on their count.  Also converts the row's LSE to the log2
+// are those of suffix `seq` only: cu[seq] .. cu[seq+1]-1 (clamped into the
+// total_rows rows of the buffers), and `rows` is an upper bound on their
+// count.  Also converts the row's LSE to the log2
 // domain the backward kernels use: lse2 = lse * log2(e).
 template <typename T, int D>
 __global__ __launch_bounds__(kAuxThreads) void row_dot_kernel(const T* __restrict__ dO,
                                                             const T* __restrict__ O, int rows,
+                                                            int total_rows,
                                                             const int32_t* __restrict__ cu,
                                                             int seq, int hq,
                                                             float* __restrict__ dd,
@@ -44,8 +46,9 @@ __global__ __launch_bounds__(kAuxThreads) void row_dot_kernel(const T* __restric
   const int sub = (int)(tid % LPR);
   int row0 = 0, nrows = rows;
   if (cu != nullptr) {
-    row0 = cu[seq];
-    nrows = cu[seq + 1] - row0;
+    const SegRows sg = suffix_rows(cu, seq, total_rows);
+    row0 = sg.base;
+    nrows = min(sg.len, rows);
   }
   // items past the end still take part in the shuffles (a group of LPR
   // lanes never straddles the end), but load and store nothing
@@ -111,9 +114,9 @@ __global__ __launch_bounds__(kAuxThreads) void convert_kernel(const float4* __re
   }
 }
 
-hipError_t launch_row_dot(int dtype, const void* dO, const void* O, int rows, const int32_t* cu,
-                          int seq, int hq, int head_dim, float* dd, const float* lse, float* lse2,
-                          hipStream_t st) {
+hipError_t launch_row_dot(int dtype, const void* dO, const void* O, int rows, int total_rows,
+                          const int32_t* cu, int seq, int hq, int head_dim, float* dd,
+                          const float* lse, float* lse2, hipStream_t st) {
   if (rows <= 0) return hipSuccess;
   const size_t lpr = (size_t)head_dim * (dtype == 0 ? 4 : 2) / 16;  // lanes per (row, head)
   const size_t threads = (size_t)rows * hq * lpr;
@@ -122,17 +125,17 @@ hipError_t launch_row_dot(int dtype, const void* dO, const void* O, int rows, co
   if (dtype == 0) {
     if (head_dim == 64)
       hipLaunchKernelGGL((row_dot_kernel<float, 64>), blocks, kAuxThreads, 0, st,
-                         (const float*)dO, (const float*)O, rows, cu, seq, hq, dd, lse, lse2);
+                         (const float*)dO, (const float*)O, rows, total_rows, cu, seq, hq, dd, lse, lse2);
     else
       hipLaunchKernelGGL((row_dot_kernel<float, 128>), blocks, kAuxThreads, 0, st,
-                         (const float*)dO, (const float*)O, rows, cu, seq, hq, dd, lse, lse2);
+                         (const float*)dO, (const float*)O, rows, total_rows, cu, seq, hq, dd, lse, lse2);
   } else {
     if (head_dim == 64)
       hipLaunchKernelGGL((row_dot_kernel<bf16, 64>), blocks, kAuxThreads, 0, st,
-                         (const bf16*)dO, (const bf16*)O, rows, cu, seq, hq, dd, lse, lse2);
+                         (const bf16*)dO, (const bf16*)O, rows, total_rows, cu, seq, hq, dd, lse, lse2);
     else
       hipLaunchKernelGGL((row_dot_kernel<bf16, 128>), blocks, kAuxThreads, 0, st,
-                         (const bf16*)dO, (const bf16*)O, rows, cu, seq, hq, dd, lse, lse2);
+                         (const bf16*)dO, (const bf16*)O, rows, total_rows, cu, seq, hq, dd, lse, lse2);
   }
   return hipGetLastError();
 }

@@ -111,8 +111,9 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
     const int y = sfx_first ? x : x - a.n_prefix_k_tiles;
     const int s = a.seq_base + y / a.n_suffix_k_tiles;
     k0 = (y % a.n_suffix_k_tiles) * kKvBK;
-    kbase = a.cu[s];
-    kseg = a.cu[s + 1] - kbase;
+    const SegRows sg = suffix_rows(a.cu, s, a.total_len);
+    kbase = sg.base;
+    kseg = sg.len;
     kpre = false;
   }
   if (k0 >= kseg) return;
@@ -143,8 +144,9 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
   if (kpre) {
     if (a.prefix_rows) n_pr = (a.P - k0 + BQ - 1) / BQ;
     if (a.suffix_rows) {
-      sr0 = a.cu[a.seq_base];
-      sr1 = a.cu[a.seq_base + a.n_seq];
+      const SegRows sp = suffix_span(a.cu, a.seq_base, a.seq_base + a.n_seq, a.total_len);
+      sr0 = sp.base;
+      sr1 = sp.base + sp.len;
       n_sr = (sr1 - sr0 + BQ - 1) / BQ;
     }
   } else {
@@ -451,8 +453,9 @@ __device__ __forceinline__ void bwd_q_body(const AttnArgs& a, const int bid, bf1
   } else {
     prefix_rows = false;
     lp0 = (blk.tile - a.n_prefix_q_tiles) * kQBQ;
-    row_base = a.cu[seq];
-    seg_len = a.cu[seq + 1] - row_base;
+    const SegRows sg = suffix_rows(a.cu, seq, a.total_len);
+    row_base = sg.base;
+    seg_len = sg.len;
   }
   if (lp0 >= seg_len) return;
   const int hq = blk.hq, hk = hq / (a.hq / a.hkv);
@@ -674,7 +677,8 @@ __global__ __launch_bounds__(256) void bwd_kv_combine_kernel(AttnArgs a, int n_p
   if (pre) {
     key = kh / a.hkv;
   } else {
-    const int r0 = a.cu[a.seq_base], r1 = a.cu[a.seq_base + a.n_seq];
+    const SegRows sp = suffix_span(a.cu, a.seq_base, a.seq_base + a.n_seq, a.total_len);
+    const int r0 = sp.base, r1 = sp.base + sp.len;
     key = r0 + (kh - n_pre_kh) / a.hkv;
     if (key >= r1) return;
   }

@@ -81,8 +81,9 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(AttnArgs a) {
   } else {
     prefix_rows = false;
     lp0 = (blk.tile - a.n_prefix_q_tiles) * kFwdBQ;
-    row_base = a.cu[seq];
-    seg_len = a.cu[seq + 1] - row_base;
+    const SegRows sg = suffix_rows(a.cu, seq, a.total_len);
+    row_base = sg.base;
+    seg_len = sg.len;
   }
   if (lp0 >= seg_len) return;
   const int hq = blk.hq, hk = hq / (a.hq / a.hkv);

@@ -37,8 +37,9 @@ __device__ __forceinline__ bool decode_qtile(const AttnArgs& a, int bq, QTile& t
   } else {
     t.prefix = false;
     t.lp0 = (tile - a.n_prefix_q_tiles) * bq;
-    t.row_base = a.cu[t.seq];
-    t.seg_len = a.cu[t.seq + 1] - t.row_base;
+    const SegRows sg = suffix_rows(a.cu, t.seq, a.total_len);
+    t.row_base = sg.base;
+    t.seg_len = sg.len;
   }
   return t.lp0 < t.seg_len;
 }
@@ -146,8 +147,9 @@ __global__ __launch_bounds__(kF32Threads) void bwd_kv_f32_kernel(AttnArgs a) {
     const int y = x - a.n_prefix_k_tiles;
     s = a.seq_base + y / a.n_suffix_k_tiles;
     k0 = (y % a.n_suffix_k_tiles) * BK;
-    kbase = a.cu[s];
-    kseg = a.cu[s + 1] - kbase;
+    const SegRows sg = suffix_rows(a.cu, s, a.total_len);
+    kbase = sg.base;
+    kseg = sg.len;
     kpre = false;
   }
   if (k0 >= kseg) return;
@@ -209,7 +211,8 @@ __global__ __launch_bounds__(kF32Threads) void bwd_kv_f32_kernel(AttnArgs a) {
     if (kpre) {
       if (a.prefix_rows) run_rows(hh, true, 0, k0, a.P, true);
       if (a.suffix_rows) {
-        const int r0 = a.cu[a.seq_base], r1 = a.cu[a.seq_base + a.n_seq];
+        const SegRows sp = suffix_span(a.cu, a.seq_base, a.seq_base + a.n_seq, a.total_len);
+        const int r0 = sp.base, r1 = sp.base + sp.len;
         run_rows(hh, false, r0, 0, r1 - r0, false);
       }
     } else {

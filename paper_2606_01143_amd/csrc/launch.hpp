@@ -68,10 +68,11 @@ int f32_block_k();
 // dd[row * hq + h] = sum_d dO[row,h,d] * O[row,h,d] and
 // lse2[row * hq + h] = lse[row * hq + h] * log2(e) for rows [0, rows), or,
 // when cu != nullptr, for the rows cu[seq] .. cu[seq+1]-1 of one packed
-// suffix (rows then bounds their count); dO == nullptr gives dd = 0.
-hipError_t launch_row_dot(int dtype, const void* dO, const void* O, int rows, const int32_t* cu,
-                          int seq, int hq, int head_dim, float* dd, const float* lse, float* lse2,
-                          hipStream_t st);
+// suffix (rows then bounds their count, total_rows is the buffers' row
+// count the offsets are clamped to); dO == nullptr gives dd = 0.
+hipError_t launch_row_dot(int dtype, const void* dO, const void* O, int rows, int total_rows,
+                          const int32_t* cu, int seq, int hq, int head_dim, float* dd,
+                          const float* lse, float* lse2, hipStream_t st);
 hipError_t launch_fill_zero(float* p, size_t n, hipStream_t st);
 // out = acc * scale (+ add when add != nullptr), converted to `dtype`
 hipError_t launch_convert(int dtype, const float* acc, float scale, const float* add,

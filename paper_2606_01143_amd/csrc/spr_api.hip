@@ -478,6 +478,28 @@ spr_status spr_suffix_attn_fwd(const spr_dims* dims, const void* k_p, const void
   return ok();
 }
 
+spr_status spr_check_cu_seqlens(const int32_t* cu_host, int32_t n_mb, int32_t max_len,
+                                int32_t total_len) {
+  if (cu_host == nullptr) return fail(SPR_ERR_INVALID_ARG, "cu_seqlens (host copy) is null");
+  spr_status st = check_suffix_sizes(n_mb, max_len, total_len);
+  if (st != SPR_OK) return st;
+  if (cu_host[0] != 0) return fail(SPR_ERR_INVALID_ARG, "cu_seqlens[0] must be 0");
+  int32_t longest = 0;
+  for (int32_t s = 0; s < n_mb; ++s) {
+    const int64_t len = (int64_t)cu_host[s + 1] - cu_host[s];
+    if (len < 1)
+      return fail(SPR_ERR_INVALID_ARG, "suffix " + std::to_string(s) + " has length " +
+                                           std::to_string(len) + " (every suffix needs >= 1 token)");
+    if (len > max_len)
+      return fail(SPR_ERR_INVALID_ARG, "suffix " + std::to_string(s) + " is longer than max_len");
+    longest = std::max(longest, (int32_t)len);
+  }
+  if (cu_host[n_mb] != total_len)
+    return fail(SPR_ERR_INVALID_ARG, "cu_seqlens[n_mb] must equal total_len");
+  if (longest != max_len) return fail(SPR_ERR_INVALID_ARG, "max_len is not the longest suffix");
+  return ok();
+}
+
 spr_status spr_suffix_attn_bwd_accum(const spr_dims* dims, const void* k_p, const void* v_p,
                                      const void* q_s, const void* k_s, const void* v_s,
                                      const void* o_s, const float* lse_s, const void* do_s,
@@ -515,7 +537,7 @@ spr_status spr_suffix_attn_bwd_accum(const spr_dims* dims, const void* k_p, cons
   float* dd_s = at<float>(ws, w.dd_s);
   float* lse2_s = at<float>(ws, w.lse2_s);
   float* dq_acc = f32 ? at<float>(ws, w.dq_acc_s) : nullptr;
-  if ((st = hip_check(launch_row_dot(dims->dtype, do_s, o_s, total_len, nullptr, 0, (int)hq,
+  if ((st = hip_check(launch_row_dot(dims->dtype, do_s, o_s, total_len, total_len, nullptr, 0, (int)hq,
                                      (int)hd, dd_s, lse_s, lse2_s, stream), "row statistic")) != SPR_OK)
     return st;
   if (f32 && (st = hip_check(launch_fill_zero(dq_acc, T * hq * hd, stream), "dq clear")) != SPR_OK)
@@ -704,7 +726,7 @@ spr_status prefix_bwd_parts(const spr_dims* dims, const void* q_p, const void* k
   float* dd_p = at<float>(ws, w.dd_p);
   float* lse2_p = at<float>(ws, w.lse2_p);
   float* dq_acc = f32 && want_dq ? at<float>(ws, w.dq_acc_p) : nullptr;
-  if ((st = hip_check(launch_row_dot(dims->dtype, do_p, o_p, (int)P, nullptr, 0, (int)hq, (int)hd,
+  if ((st = hip_check(launch_row_dot(dims->dtype, do_p, o_p, (int)P, (int)P, nullptr, 0, (int)hq, (int)hd,
                                      dd_p, lse_p, lse2_p, stream), "row statistic")) != SPR_OK)
     return st;
   if (dq_acc && (st = hip_check(launch_fill_zero(dq_acc, P * hq * hd, stream), "dq clear")) != SPR_OK)
@@ -828,9 +850,9 @@ spr_status spr_dense_recompute_baseline(
     SPR_TRY(launch_fwd(dims, a, 1, stream), "dense forward");
     const void* dop_i = have_dop ? (const char*)do_p_seq + (size_t)i * P * hq * hd * eb : nullptr;
     if (have_dop && P > 0)
-      SPR_TRY(launch_row_dot(dims->dtype, dop_i, o_p, (int)P, nullptr, 0, (int)hq, (int)hd, dd_p,
+      SPR_TRY(launch_row_dot(dims->dtype, dop_i, o_p, (int)P, (int)P, nullptr, 0, (int)hq, (int)hd, dd_p,
                              lse_p, lse2_p, stream), "row statistic");
-    SPR_TRY(launch_row_dot(dims->dtype, do_s, o_s, max_len, cu_seqlens, i, (int)hq, (int)hd, dd_s,
+    SPR_TRY(launch_row_dot(dims->dtype, do_s, o_s, max_len, total_len, cu_seqlens, i, (int)hq, (int)hd, dd_s,
                            lse_s, lse2_s, stream), "row statistic");
     a.do_p = dop_i; a.dd_p = dd_p; a.lse2_p = lse2_p; a.dq_acc_p = dq_acc_p;
     a.do_s = do_s; a.dd_s = dd_s; a.lse2_s = lse2_s; a.dq_acc_s = dq_acc_s;

@@ -161,8 +161,10 @@ class DeviceGroup:
         key = (a, b)
         if key not in self._cu_cache:
             base = self.cu_host[a]
-            self._cu_cache[key] = torch.tensor([x - base for x in self.cu_host[a:b + 1]],
-                                               dtype=torch.int32, device=self.device)
+            host = [x - base for x in self.cu_host[a:b + 1]]
+            nmb, mx, tot = self._mb_sizes(a, b)
+            B.check_cu_seqlens(host, nmb, mx, tot)  # once per microbatch, before any launch
+            self._cu_cache[key] = torch.tensor(host, dtype=torch.int32, device=self.device)
         return self._cu_cache[key]
 
     def prepare(self, microbatches: Sequence[Tuple[int, int]]) -> None:
@@ -306,6 +308,9 @@ class DeviceGroup:
         """Dense recompute baseline; results land in ``self.dense_out``."""
         o = self.dense_out
         shp = self.shape
+        if not getattr(self, "_cu_checked", False):
+            B.check_cu_seqlens(self.cu_host, shp.n, max(self.lens), shp.total_suffix)
+            self._cu_checked = True
         B.dense_recompute_baseline(
             self.dims, self.q_p, self.k_p, self.v_p, self.do_p if use_dop else None, self.q_s,
             self.k_s, self.v_s, self.do_s, self.cu, shp.n, max(self.lens), shp.total_suffix,

@@ -135,6 +135,7 @@ class StackedGroup:
         self.pool = PinnedPool(int(self.dormant_bytes * pool_factor)) if offload else None
         self.host: List[Dict[str, torch.Tensor]] = [dict() for _ in range(L)]
         self.ready: List[Optional[torch.cuda.Event]] = [None] * L
+        self.packed: List[Optional[torch.cuda.Event]] = [None] * L
         self.stats = {"prefetched": 0, "demand_loaded": 0, "pool_fallbacks": 0}
         self.suffix_grads: List[Dict[str, torch.Tensor]] = []
 
@@ -164,6 +165,11 @@ class StackedGroup:
                 self.host[l][k] = h
                 x.record_stream(cs)
                 t[k] = None
+            # the host copies are complete once this event has passed: a
+            # restore on another stream waits for it
+            packed = torch.cuda.Event()
+            packed.record(cs)
+            self.packed[l] = packed
         self.stats["pool_fallbacks"] = self.pool.fallbacks
 
     def _restore(self, l: int, prefetch: bool) -> None:
@@ -171,6 +177,10 @@ class StackedGroup:
         (prefetch) or on the compute stream right before use (demand load)."""
         t = self.layers[l]
         stream = self.copy_stream if prefetch else torch.cuda.current_stream(self.dev)
+        # the pack of this layer ran on the copy stream: a demand load on
+        # the compute stream must not read the pinned slices before it ends
+        if not prefetch and self.packed[l] is not None:
+            stream.wait_event(self.packed[l])
         with torch.cuda.stream(stream):
             for k in _DORMANT:
                 h = self.host[l][k]
@@ -210,6 +220,7 @@ class StackedGroup:
         if self.offload:
             self.pool.reset()
             self.ready = [None] * L
+            self.packed = [None] * L
         # Phase A: prefix forward layer by layer; each layer's dormant set
         # leaves for the host as soon as the layer is done
         for l in range(L):

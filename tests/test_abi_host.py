@@ -210,3 +210,34 @@ def test_padded_workspace_holds_packed_copies_and_inner_workspace(lib):
     rows = n * s
     assert fwd >= B.workspace_size(B.OP_SUFFIX_FWD, dims, n, s, rows) + rows * (2 * 32 + 2 * 8) * 128 * 2
     assert bwd >= B.workspace_size(B.OP_SUFFIX_BWD, dims, n, s, rows) + rows * (4 * 32 + 4 * 8) * 128 * 2
+
+
+@pytest.mark.parametrize("cu,n,mx,tot,ok", [
+    ([0, 3, 5], 2, 3, 5, True),
+    ([0, 3, 3, 5], 3, 3, 5, False),     # a zero-length suffix
+    ([0, 3, 2, 5], 3, 3, 5, False),     # decreasing offsets
+    ([1, 3, 5], 2, 2, 5, False),        # cu[0] != 0
+    ([0, 3, 6], 2, 3, 5, False),        # cu[n] != total_len
+    ([0, 4, 5], 2, 3, 5, False),        # a suffix longer than max_len
+    ([0, 2, 4], 2, 3, 4, False),        # max_len is not the longest suffix
+    ([0, 1], 1, 1, 1, True),
+])
+def test_check_cu_seqlens(lib, cu, n, mx, tot, ok):
+    """The host-side offset check: a zero-length suffix and offsets that
+    disagree with n / max_len / total_len are INVALID_ARG, nothing else."""
+    if ok:
+        B.check_cu_seqlens(cu, n, mx, tot)
+    else:
+        with pytest.raises(B.SprError) as e:
+            B.check_cu_seqlens(cu, n, mx, tot)
+        assert e.value.status_name == "SPR_ERR_INVALID_ARG"
+
+
+def test_suffix_calls_check_host_offsets_before_launching(lib):
+    """With the host offsets given, a zero-length suffix is rejected before
+    the binding reaches the library's launch path (fake pointers)."""
+    with pytest.raises(B.SprError) as e:
+        B.suffix_attn_fwd(_dims(), _addr(1), _addr(2), _addr(3), _addr(4), _addr(5), _addr(6),
+                          2, 4, 4, _addr(7), _addr(8), cu_host=[0, 4, 4])
+    assert e.value.status_name == "SPR_ERR_INVALID_ARG"
+    assert "length 0" in str(e.value)

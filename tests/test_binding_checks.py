@@ -66,3 +66,26 @@ def test_suffix_backward_cache_and_offsets_are_checked():
         call(dq_s=bf(T - 1, 4, 64))
     with pytest.raises(ValueError, match="GPU tensors only"):
         call()
+
+
+@pytest.mark.parametrize("call,args,bad", [
+    ("rmsnorm_fwd", lambda: (torch.zeros(4, 16, dtype=torch.bfloat16), torch.zeros(3, 16, dtype=torch.bfloat16),
+                             torch.zeros(4)), "y: 48 elements"),
+    ("rmsnorm_fwd", lambda: (torch.zeros(4, 16, dtype=torch.bfloat16), torch.zeros(4, 16, dtype=torch.bfloat16),
+                             torch.zeros(3)), "rstd: 3 elements"),
+    ("rmsnorm_bwd", lambda: (torch.zeros(4, 16, dtype=torch.bfloat16), torch.zeros(4),
+                             torch.zeros(4, 16, dtype=torch.bfloat16), torch.zeros(4, 16)), "dx: elements of 4 bytes"),
+    ("rope_fwd", lambda: (torch.zeros(5, 2, 8, dtype=torch.bfloat16), torch.zeros(5, 2, 7, dtype=torch.bfloat16),
+                          0, 1e4), "y: 70 elements"),
+    ("rope_bwd", lambda: (torch.zeros(5, 2, 8, dtype=torch.bfloat16), torch.zeros(5, 2, 8),
+                          0, 1e4), "dx: elements of 4 bytes"),
+    ("swiglu_fwd", lambda: (torch.zeros(16, dtype=torch.bfloat16), torch.zeros(16, dtype=torch.bfloat16),
+                            torch.zeros(8, dtype=torch.bfloat16)), "m: 8 elements"),
+    ("swiglu_bwd", lambda: (torch.zeros(16, dtype=torch.bfloat16), torch.zeros(16, dtype=torch.bfloat16),
+                            torch.zeros(16, dtype=torch.bfloat16), torch.zeros(16, dtype=torch.bfloat16),
+                            torch.zeros(15, dtype=torch.bfloat16)), "du: 15 elements"),
+])
+def test_layer_op_wrappers_refuse_short_or_mistyped_tensors(call, args, bad):
+    """The decoder-layer op wrappers check element size and count too."""
+    with pytest.raises(ValueError, match=bad):
+        getattr(B, call)(*args())

@@ -1,14 +1,29 @@
 """Full-length groups of the sweep and the long-context shape on one kv
-group (4 q heads), where the full oracle is too slow: sampled rows against
-the oracle's per-row definition (O, LSE, dQ of prefix and suffix rows),
-and every key's dK/dV through identities that hold at any size:
-  sum over all keys of dK = 0 (softmax-backward rows sum to zero), and
-  sum over all keys of dV = sum over all rows and group heads of dO, with
-  G_Y for the prefix rows (probability rows sum to one)."""
+group, where the whole fp64 oracle is too slow, checked element by element
+on sampled rows and sampled keys, both computed by the oracle from each
+row's own sequence:
+
+* rows (``sampled_rows_reference``): O, LSE and dQ of prefix rows (first,
+  tile edges, middle, last, random) and suffix rows (first, last and both
+  sides of row-tile edges of three suffixes).  Every row's O and dQ sum over
+  all its key tiles, so they also cover every key-split range of the split
+  suffix forward and backward launches and their combine kernels.
+* keys (``sampled_keys_reference``): dK and dV of prefix keys (first, both
+  sides of 64-key tile edges, the middle, the last, random) with the cache
+  values G_K, G_V, and of suffix keys (first, tile edges, middle, last of
+  three suffixes).  Every sampled prefix key is swept by all rows that see
+  it, so its dK/dV/G_K/G_V check the cache accumulation over every suffix
+  microbatch and the row shares of the key-outer role.
+
+The longest-prefix case samples prefix keys in its last 2048 positions
+only (each sampled prefix key costs a forward over the rows that see it).
+Identities that hold at any size are checked on every key as well:
+sum over all keys of dK = 0, and sum over all keys of dV = sum over all
+rows and group heads of dO (G_Y for the prefix rows)."""
 import numpy as np
 import pytest
 
-from oracle.attention import sampled_rows_reference
+from oracle.attention import sampled_keys_reference, sampled_rows_reference
 from synthetic import GroupShape, make_group
 
 TOL = 2e-2
@@ -27,9 +42,37 @@ CASES = [
 ]
 
 
+def _rel(got, ref):
+    g, r = np.stack(got), np.stack(ref)
+    return float(np.max(np.abs(g - r)) / max(np.max(np.abs(r)), 1e-30))
+
+
+def sample_rows(P, lens, rng):
+    n = len(lens)
+    prefix = sorted({0, 1, 63, 64, 127, 128, 255, 256, P // 2, P - 2, P - 1,
+                     *rng.integers(0, P, 5).tolist()})
+    suffix = sorted({(i, t) for i in (0, n // 2, n - 1)
+                     for t in (0, 31, 32, 127, 128, lens[i] // 2, lens[i] - 1) if t < lens[i]})
+    return prefix, suffix
+
+
+def sample_keys(P, lens, rng):
+    n = len(lens)
+    if P > 32768:
+        lo = P - 2048
+        prefix = sorted({lo, lo + 63, lo + 64, P - 1025, P - 1024, P - 65, P - 64, P - 2, P - 1,
+                         *rng.integers(lo, P, 3).tolist()})
+    else:
+        prefix = sorted({0, 1, 63, 64, 127, 128, P // 2 - 1, P // 2, P - 65, P - 64, P - 2, P - 1,
+                         *rng.integers(0, P, 4).tolist()})
+    suffix = sorted({(i, t) for i in (0, n // 2, n - 1)
+                     for t in (0, 1, 63, 64, lens[i] // 2, lens[i] - 1) if t < lens[i]})
+    return prefix, suffix
+
+
 @pytest.mark.gpu
 @pytest.mark.parametrize("name,shape,ragged", CASES, ids=[c[0] for c in CASES])
-def test_full_length_sampled_rows_and_identities(gpu, name, shape, ragged):
+def test_full_length_sampled_rows_keys_and_identities(gpu, name, shape, ragged):
     import torch
     from paper_2606_01143_amd.group import DeviceGroup
     _announce(name)
@@ -39,25 +82,33 @@ def test_full_length_sampled_rows_and_identities(gpu, name, shape, ragged):
     grp.run_schedule()
     torch.cuda.synchronize()
     got = grp.fetch("schedule")
+    del grp
     P, n, lens = shp.prefix_len, shp.n, [int(x) for x in inp["suffix_lens"]]
-    rng = np.random.default_rng(0)
-    prefix_rows = sorted({0, 1, 63, 64, P // 2, P - 2, P - 1, *rng.integers(0, P, 5).tolist()})
-    suffix_rows = [(0, 0), (0, lens[0] - 1), (n - 1, lens[-1] - 1), (n // 2, lens[n // 2] // 2)]
-    ref = sampled_rows_reference(inp, prefix_rows, suffix_rows)
     cu = inp["cu_seqlens"]
+    rng = np.random.default_rng(0)
     errs = {}
-    for key, rows, gk in (("prefix", prefix_rows, "_p"), ("suffix", suffix_rows, "_s")):
+    # ---- rows
+    prefix_rows, suffix_rows = sample_rows(P, lens, rng)
+    ref = sampled_rows_reference(inp, prefix_rows, suffix_rows)
+    for key, rows, sfx in (("prefix", prefix_rows, "_p"), ("suffix", suffix_rows, "_s")):
         for f in ("o", "dq", "lse"):
             g, r = [], []
             for row in rows:
                 idx = row if key == "prefix" else int(cu[row[0]]) + row[1]
-                g.append(got[f + gk][idx])
+                g.append(got[f + sfx][idx])
                 r.append(ref[key][row][f])
-            g, r = np.stack(g), np.stack(r)
-            errs[f"{f}{gk}"] = float(np.max(np.abs(g - r)) / max(np.max(np.abs(r)), 1e-30))
+            errs[f"{f}{sfx}"] = _rel(g, r)
+    # ---- keys
+    prefix_keys, suffix_keys = sample_keys(P, lens, rng)
+    kref = sampled_keys_reference(inp, prefix_keys, suffix_keys)
+    for f, gk in (("dk", "dk_p"), ("dv", "dv_p"), ("g_k", "g_k"), ("g_v", "g_v")):
+        errs[gk + "@keys"] = _rel([got[gk][j] for j in prefix_keys], [kref["prefix"][j][f] for j in prefix_keys])
+    for f in ("dk", "dv"):
+        errs[f + "_s@keys"] = _rel([got[f + "_s"][int(cu[i]) + t] for i, t in suffix_keys],
+                                   [kref["suffix"][(i, t)][f] for i, t in suffix_keys])
     bad = {k: v for k, v in errs.items() if not v <= TOL}
     assert not bad, (bad, errs)
-    # identities over every key
+    # ---- identities over every key
     dk = np.concatenate([got["dk_p"], got["dk_s"]]).sum(axis=0)
     dk_scale = np.abs(np.concatenate([got["dk_p"], got["dk_s"]])).sum(axis=0).max()
     assert np.abs(dk).max() <= 1e-3 * dk_scale, np.abs(dk).max() / dk_scale

@@ -1,11 +1,31 @@
 """Batch-plus-padding suffix layout (paper Sec. 2.1, Sec. 4.2): the padded
 calls must give bitwise the packed calls' results on the valid rows, zero on
-the padding rows, and the same gK/gV cache.  The padding rows of every
+the padding rows, and the same gK/gV cache; and their valid rows and cache
+must match the fp64 oracle's three-phase reference on the same inputs (the
+max-abs-relative gate: 1e-4 fp32, 2e-2 bf16).  The padding rows of every
 input hold NaN, so any read of them would show."""
 import numpy as np
 import pytest
 
+from oracle import max_abs_rel, three_phase_reference
 from synthetic import GroupShape, make_group
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+
+def _against_oracle(inp, rows, gk, gv, what, microbatches=None):
+    """rows: packed [T, ...] valid-row outputs o, lse, dq, dk, dv (torch);
+    gk, gv: the cache after Phase B.  Compared with the oracle's Phase B
+    outputs and cache."""
+    ref = three_phase_reference(inp, microbatches=microbatches)
+    f64 = lambda x: x.float().cpu().numpy().astype(np.float64)
+    errs = {k: max_abs_rel(f64(rows[k]), ref[k + "_s"].T if k == "lse" else ref[k + "_s"])
+            for k in ("o", "lse", "dq", "dk", "dv")}
+    errs["g_k"] = max_abs_rel(f64(gk), ref["g_k"])
+    errs["g_v"] = max_abs_rel(f64(gv), ref["g_v"])
+    tol = TOL[inp["shape"].dtype]
+    bad = {k: v for k, v in errs.items() if not v <= tol}
+    assert not bad, (what, bad, errs)
 
 
 def _announce(what):
@@ -67,6 +87,9 @@ def _run_packed_and_padded(shape, seed, ragged=None):
             assert torch.equal(got, packed[key][cu_h[i]:cu_h[i + 1]]), (key, i)
             assert not padded[key][i, lens[i]:].float().abs().sum().item(), (key, i, "padding not zero")
     assert torch.equal(gk, gk2) and torch.equal(gv, gv2)
+    # the padded call's own valid rows and cache against the oracle
+    valid = {k: torch.cat([padded[k][i, :lens[i]] for i in range(n)]) for k in padded}
+    _against_oracle(inp, valid, gk2, gv2, f"padded {shape}")
 
 
 CASES = [
@@ -115,3 +138,11 @@ def test_padded_schedule_equals_packed_schedule(gpu, budget):
     for k in packed.out:
         assert torch.equal(packed.out[k], padded.out[k]), k
     assert torch.equal(packed.gk, padded.gk) and torch.equal(packed.gv, padded.gv)
+    # the padded schedule's outputs against the oracle's schedule on the same waves
+    ref = three_phase_reference(inp, microbatches=[list(range(a, b)) for a, b in waves])
+    got = padded.fetch("schedule")
+    errs = {k: max_abs_rel(got[k], ref[k].T if k.startswith("lse") else ref[k])
+            for k in ("o_p", "lse_p", "o_s", "lse_s", "dq_p", "dk_p", "dv_p", "dq_s", "dk_s", "dv_s",
+                      "g_k", "g_v")}
+    bad = {k: v for k, v in errs.items() if not v <= 2e-2}
+    assert not bad, (bad, errs)

@@ -269,3 +269,21 @@ def test_qwen3_moe_ragged_full_size_on_one_kv_group(gpu):
     sel.update({k: got[k][:, qh] for k in ("lse_p", "lse_s")})
     sel.update({k: got[k][:, kv:kv + 1] for k in kv_keys})
     _assert_close(sel, ref, SCHED_KEYS, TOL["bf16"], f"qwen3-moe full kv={kv}")
+
+
+def test_gkv_accumulate_equals_host_sum(gpu):
+    """spr_gkv_accumulate (G += g over [P, Hkv, d] fp32, App. A.8's
+    element-wise accumulation): bitwise the fp32 sum done on the host, also
+    for a size that leaves the last thread block partly idle."""
+    import torch
+    from paper_2606_01143_amd import binding as B
+    for P, hkv, d in ((4096, 8, 128), (37, 3, 64)):
+        _announce(f"gkv_accumulate P={P} Hkv={hkv} d={d}")
+        dims = B.make_dims(hkv, hkv, d, P, "bf16")
+        g = torch.Generator().manual_seed(P)
+        host = [torch.randn(P, hkv, d, generator=g, dtype=torch.float32) for _ in range(4)]
+        gk, gv, dgk, dgv = (x.to("cuda:0") for x in host)
+        B.gkv_accumulate(dims, gk, gv, dgk, dgv)
+        torch.cuda.synchronize()
+        assert torch.equal(gk.cpu(), host[0] + host[2])
+        assert torch.equal(gv.cpu(), host[1] + host[3])

@@ -143,6 +143,28 @@ spr_status spr_suffix_attn_fwd(const spr_dims* dims, const void* k_p, const void
                                size_t ws_bytes, hipStream_t stream);
 
 /*
+ * spr_suffix_attn_fwd without a workspace argument and without any device
+ * allocation, for callers that cannot allocate: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  Same
+ * arguments, semantics and outputs as spr_suffix_attn_fwd (bitwise: the
+ * same kernels with the same launch shapes).  Its workspace is a static
+ * device array of 64 MiB (67108864 bytes) that every GPU the library runs
+ * on holds until the process ends; its address is looked
+ * up on the first call on each device, which must be the calling thread's
+ * current device.  Sizes whose workspace (spr_workspace_size of
+ * SPR_OP_SUFFIX_FWD) exceeds the scratch are rejected with
+ * SPR_ERR_WORKSPACE and nothing is launched.  All calls on one GPU share
+ * that GPU's scratch: two calls that overlap in time on one GPU (different
+ * streams, or host threads) race and give undefined results; calls ordered
+ * on one stream are safe.
+ */
+spr_status spr_suffix_attn_fwd_noalloc(const spr_dims* dims, const void* k_p, const void* v_p,
+                                       const void* q_s, const void* k_s, const void* v_s,
+                                       const int32_t* cu_seqlens, int32_t n_mb, int32_t max_len,
+                                       int32_t total_len, void* o_s, float* lse_s,
+                                       hipStream_t stream);
+
+/*
  * Host-side check of a packed microbatch's suffix offsets, for callers that
  * hold a host copy of the cu_seqlens they upload (the library never reads
  * device memory on the host).  SPR_OK iff cu_host[0] == 0, every suffix

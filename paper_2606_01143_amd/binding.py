@@ -37,6 +37,8 @@ _SIGNATURES = {
     "spr_prefix_fwd": ([_P, _P, _P, _P, _P, _P, _P], c_int32),
     "spr_suffix_attn_fwd": ([_P, _P, _P, _P, _P, _P, _P, c_int32, c_int32, c_int32, _P, _P, _P,
                              c_size_t, _P], c_int32),
+    "spr_suffix_attn_fwd_noalloc": ([_P, _P, _P, _P, _P, _P, _P, c_int32, c_int32, c_int32, _P, _P,
+                                     _P], c_int32),
     "spr_suffix_attn_bwd_accum": ([_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, c_int32, c_int32, c_int32,
                                    _P, _P, _P, _P, _P, _P, c_size_t, _P], c_int32),
     "spr_prefix_bwd": ([_P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, c_size_t, _P], c_int32),
@@ -230,6 +232,28 @@ def suffix_attn_fwd(dims, k_p, v_p, q_s, k_s, v_s, cu_seqlens, n_mb, max_len, to
                                      _ptr(v_s), _ptr(cu_seqlens), n_mb, max_len, total_len,
                                      _ptr(o_s), _ptr(lse_s), _ptr(ws), _nbytes(ws),
                                      _stream(stream)))
+
+
+# bytes of the static device scratch behind suffix_attn_fwd_noalloc
+STATIC_SCRATCH_BYTES = 64 << 20
+
+
+def suffix_attn_fwd_noalloc(dims, k_p, v_p, q_s, k_s, v_s, cu_seqlens, n_mb, max_len, total_len,
+                            o_s, lse_s, stream=None, cu_host=None):
+    """suffix_attn_fwd with the library's static scratch as its workspace:
+    no device allocation anywhere (callers under graph capture, serving
+    loops).  Calls that overlap on one GPU race on the scratch."""
+    if cu_host is not None:
+        check_cu_seqlens(cu_host, n_mb, max_len, total_len)
+    z = _Sizes(dims, total_len)
+    z.kv(z.P, k_p=k_p, v_p=v_p)
+    z.q(z.T, q_s=q_s, o_s=o_s)
+    z.kv(z.T, k_s=k_s, v_s=v_s)
+    z.lse(z.T, lse_s=lse_s)
+    z.i32(int(n_mb) + 1, cu_seqlens=cu_seqlens)
+    _check(lib().spr_suffix_attn_fwd_noalloc(byref(dims), _ptr(k_p), _ptr(v_p), _ptr(q_s), _ptr(k_s),
+                                             _ptr(v_s), _ptr(cu_seqlens), n_mb, max_len, total_len,
+                                             _ptr(o_s), _ptr(lse_s), _stream(stream)))
 
 
 def suffix_attn_bwd_accum(dims, k_p, v_p, q_s, k_s, v_s, o_s, lse_s, do_s, cu_seqlens, n_mb,

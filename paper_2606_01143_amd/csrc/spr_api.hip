@@ -478,6 +478,63 @@ spr_status spr_suffix_attn_fwd(const spr_dims* dims, const void* k_p, const void
   return ok();
 }
 
+// ------------------------------------------ static scratch, no allocation
+// For callers that cannot allocate device memory (code under graph capture,
+// tight serving loops): a file-scope device array serves as the workspace
+// of spr_suffix_attn_fwd_noalloc.  Each GPU the library runs on holds its
+// own copy for the life of the process.  In host code the array's name is
+// not a device address: the address is looked up once per device with
+// hipGetSymbolAddress and only that pointer is passed to kernels.
+namespace {
+constexpr size_t kStaticScratchBytes = size_t(64) << 20;
+constexpr int kMaxDevices = 64;
+}  // namespace
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+namespace {
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// the current device's scratch address, looked up on the device's first use
+spr_status scratch_of_current_device(void** ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(SPR_ERR_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(SPR_ERR_UNSUPPORTED, "device index beyond the static scratch table");
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || p == nullptr)
+      return fail(SPR_ERR_HIP, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return SPR_OK;
+}
+}  // namespace
+
+spr_status spr_suffix_attn_fwd_noalloc(const spr_dims* dims, const void* k_p, const void* v_p,
+                                       const void* q_s, const void* k_s, const void* v_s,
+                                       const int32_t* cu_seqlens, int32_t n_mb, int32_t max_len,
+                                       int32_t total_len, void* o_s, float* lse_s,
+                                       hipStream_t stream) {
+  spr_status st = check_dims(dims);
+  if (st != SPR_OK) return st;
+  if ((st = check_suffix_sizes(n_mb, max_len, total_len)) != SPR_OK) return st;
+  const size_t need = ws_layout(SPR_OP_SUFFIX_FWD, dims, n_mb, max_len, total_len).total;
+  if (need > kStaticScratchBytes)
+    return fail(SPR_ERR_WORKSPACE, "these sizes need " + std::to_string(need) +
+                                       " bytes of scratch; the static scratch holds " +
+                                       std::to_string(kStaticScratchBytes));
+  void* ws = nullptr;
+  if ((st = scratch_of_current_device(&ws)) != SPR_OK) return st;
+  // every scratch byte the forward reads it first writes in the same call
+  return spr_suffix_attn_fwd(dims, k_p, v_p, q_s, k_s, v_s, cu_seqlens, n_mb, max_len, total_len,
+                             o_s, lse_s, ws, kStaticScratchBytes, stream);
+}
+
 spr_status spr_check_cu_seqlens(const int32_t* cu_host, int32_t n_mb, int32_t max_len,
                                 int32_t total_len) {
   if (cu_host == nullptr) return fail(SPR_ERR_INVALID_ARG, "cu_seqlens (host copy) is null");

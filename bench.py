@@ -301,6 +301,8 @@ def main():
     ap.add_argument("--policy", choices=["per_suffix", "packed"], default="per_suffix")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--atomic-dq", action="store_true",
+                    help="SPR_ATOMIC_DQ: dQ added by the key-outer blocks with fp32 atomics")
     ap.add_argument("--cpu-seconds", type=float, default=20.0,
                     help="time budget of the CPU oracle baseline (0: skip it)")
     ap.add_argument("--sweep", choices=["c3", "c4", "c5attn", "all"], default=None)
@@ -352,7 +354,8 @@ def main():
     packed = [(0, n)]
     mbs = per_suffix if args.policy == "per_suffix" else packed
     grp = DeviceGroup(inp, device="cuda:0", dense=not args.no_dense,
-                      microbatch_splits=[per_suffix, packed], layout=args.layout)
+                      microbatch_splits=[per_suffix, packed], layout=args.layout,
+                      atomic_dq=args.atomic_dq)
     grp.prepare(mbs)
     torch.cuda.synchronize()
 
@@ -435,7 +438,8 @@ def main():
                    "prefix_len": shape.prefix_len, "n_suffixes": n,
                    "suffix_lens": list(shape.suffix_lens) if len(set(shape.suffix_lens)) > 1
                    else shape.suffix_lens[0],
-                   "microbatching": args.policy, "layout": args.layout},
+                   "microbatching": args.policy, "layout": args.layout,
+                   "dq": "atomic" if args.atomic_dq else "query_outer"},
         "pct_mfma_peak": round(100 * value / BF16_PEAK_TFLOPS, 2),
         "value_at_median": round(tf(sched_flops, st["median"]), 3),
         "schedule_tflop_per_step": round(sched_flops / 1e12, 4),

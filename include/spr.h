@@ -83,10 +83,17 @@ typedef enum spr_dtype { SPR_F32 = 0, SPR_BF16 = 1 } spr_dtype;
 
 /* flags */
 enum {
-  /* dQ of the bf16 backward is accumulated without floating-point atomics,
-   * so every output is bitwise reproducible run to run (G_K/G_V and dK/dV
-   * always are). */
-  SPR_DETERMINISTIC = 1u << 0
+  /* Every output bitwise reproducible run to run: dQ of the bf16 backward
+   * from a query-outer role with no floating-point atomics.  This is the
+   * default; the bit is accepted for callers that state it. */
+  SPR_DETERMINISTIC = 1u << 0,
+  /* bf16 backward: the key-outer blocks add dQ = dS K / sqrt(d) into an fp32
+   * accumulator with fp32 atomics (5 matrix products per visible pair
+   * instead of 7, no query-outer role); dQ is then reproducible only to
+   * rounding, dK/dV/G_K/G_V stay bitwise.  Measured about 3x slower on
+   * MI355X (the atomic traffic, P/64 adds of every dQ element, exceeds what
+   * the L2 sustains), so it is opt-in.  Not with SPR_DETERMINISTIC. */
+  SPR_ATOMIC_DQ = 1u << 1
 };
 
 typedef struct spr_dims {
@@ -96,7 +103,7 @@ typedef struct spr_dims {
   int32_t prefix_len;   /* P >= 0; P == 0 makes the prefix calls no-ops */
   float softmax_scale;  /* 0 => 1/sqrt(d) */
   int32_t dtype;        /* spr_dtype */
-  uint32_t flags;       /* SPR_DETERMINISTIC or 0 */
+  uint32_t flags;       /* 0, SPR_DETERMINISTIC or SPR_ATOMIC_DQ */
 } spr_dims;
 
 typedef enum spr_status {

@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "lib", "libs
 SPR_F32 = 0
 SPR_BF16 = 1
 SPR_DETERMINISTIC = 1
+SPR_ATOMIC_DQ = 2
 
 OP_PREFIX_FWD = 0
 OP_SUFFIX_FWD = 1
@@ -116,10 +117,10 @@ def lib() -> ctypes.CDLL:
 
 def make_dims(num_q_heads: int, num_kv_heads: int, head_dim: int, prefix_len: int,
               dtype: str = "bf16", softmax_scale: float = 0.0,
-              deterministic: bool = False) -> SprDims:
+              deterministic: bool = False, atomic_dq: bool = False) -> SprDims:
     code = {"f32": SPR_F32, "bf16": SPR_BF16}[dtype]
-    return SprDims(num_q_heads, num_kv_heads, head_dim, prefix_len, softmax_scale, code,
-                   SPR_DETERMINISTIC if deterministic else 0)
+    flags = (SPR_DETERMINISTIC if deterministic else 0) | (SPR_ATOMIC_DQ if atomic_dq else 0)
+    return SprDims(num_q_heads, num_kv_heads, head_dim, prefix_len, softmax_scale, code, flags)
 
 
 def _ptr(x):

@@ -55,6 +55,11 @@ struct AttnArgs {
   void* dq_p;
   void* dq_s;
   int32_t dq_p_accumulate;
+  // bf16 backward, atomic dQ: the key-outer blocks add the unscaled dS K of
+  // their keys into dq_acc_p (prefix rows) / dq_acc_s (suffix rows), fp32
+  // accumulators the caller zeroes first and converts afterwards; the launch
+  // then has no query-outer role
+  int32_t dq_atomic;
   const int32_t* cu;   // device cu_seqlens
   int32_t P;
   int32_t total_len;

@@ -69,7 +69,9 @@ constexpr int kKvBQ = 32;  // rows per key-outer tile
 constexpr int kKvBufs = 3;
 }  // namespace
 
-template <int D>
+typedef __attribute__((address_space(1))) float gfloat;  // global memory
+
+template <int D, bool AQ>
 struct KvLds {
   static constexpr int TE = kKvBQ * D;  // bf16 elements of one 32-row tile
   bf16 q[kKvBufs][TE];
@@ -78,9 +80,22 @@ struct KvLds {
   float e[kKvBufs][64];  // rowsum(dO * O) of the tile's rows (32 used)
   bf16x8 p[2][2][2][64];  // P exchange (bf16) [tile parity][key block][k-step v][lane]
 };
-
 template <int D>
-__device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, KvLds<D>& L) {
+struct KvLds<D, true> : KvLds<D, false> {
+  // dS^T of a tile for the dQ product: 64 keys x 32 rows bf16, [tile parity]
+  bf16 ds[2][64 * kKvBQ];
+};
+
+// dS^T exchange tile (64 keys x 32 rows, row-major by key): 16-byte chunk c
+// of key row k sits at chunk c ^ ((k >> 2) & 3).  A dS-wave's 8-byte writes
+// (32 keys at one column) then spread over all banks, and the transposed
+// reads (4 consecutive keys x 32 bytes per 16 lanes) stay conflict-free.
+__device__ __forceinline__ int dst_off(int key, int col) {
+  return key * kKvBQ + ((((col >> 3) ^ ((key >> 2) & 3))) << 3) + (col & 7);
+}
+
+template <int D, bool AQ>
+__device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, KvLds<D, AQ>& L) {
   constexpr int NS = D / 16;
   constexpr int NDB = D / 32;
   constexpr int BQ = kKvBQ;
@@ -135,6 +150,16 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
   f32x16 acc[NDB];  // dV^T (P-wave) or dK^T (dS-wave)
 #pragma unroll
   for (int db = 0; db < NDB; ++db) acc[db] = zero16();
+  // the block's last key tile of its segment may be partial: keys past the
+  // end recompute the last key and their P must be zero wherever dQ sums
+  // over keys
+  const bool kpartial = k0 + kKvBK > kseg;
+  const bool key_ok = wave_k0 + r < kseg;
+  // atomic dQ: wave w < NDB owns dQ columns 32 w .. 32 w + 31 of every row
+  // tile; its B operands K[16 v + k][32 w + r] for the 4 k-steps over the
+  // block's 64 keys stay in registers for the whole sweep
+  const bool dq_on = AQ && a.dq_atomic;
+  bf16x8 kq[4];
 
   // ---- the 32-row tiles this key tile sees, per q head of the group:
   // prefix key tile: prefix rows from k0 on (causal) and/or every suffix row
@@ -229,7 +254,7 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
   // [q_lo, nr) get P = 0): the diagonal tile or a ragged end.
   auto hidden = [&](const RowTile& rt) { return rt.causal && rt.lp_first + BQ - 1 < wave_k0; };
   auto masked = [&](const RowTile& rt) {
-    return rt.nr < BQ || (rt.causal && rt.lp_first < wave_k0 + 31);
+    return rt.nr < BQ || (rt.causal && rt.lp_first < wave_k0 + 31) || kpartial;
   };
   // S or dP of the tile: A = Q or dO tile rows, B = kvf
   auto product = [&](const bf16* T) {
@@ -286,9 +311,10 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
         c[4 * g4 + 3] = fast_exp2(fmaf(c[4 * g4 + 3], a.scale_log2, -l4.w));
       }
       if (masked(rt)) {
-        // row lp_first + q sees my_key iff q >= q_lo
+        // row lp_first + q sees my_key iff q >= q_lo; keys past the segment
+        // see no row
         const int q_lo = rt.causal ? my_key - rt.lp_first : 0;
-        const int lo = q_lo - 4 * h, hi = rt.nr - 4 * h;
+        const int lo = q_lo - 4 * h, hi = key_ok ? rt.nr - 4 * h : -1;
 #pragma unroll
         for (int i = 0; i < 16; ++i) c[i] = (c_row0(i) >= lo && c_row0(i) < hi) ? c[i] : 0.f;
       }
@@ -313,20 +339,112 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
       }
       ops[0] = c_kfrag(ds, 0);
       ops[1] = c_kfrag(ds, 1);
+      if constexpr (AQ) {
+        if (dq_on) {
+          // dS^T rows 32 kb + r (keys), columns 8 g + 4 h .. + 3 (rows)
+          bf16* dsx = L.ds[tc & 1];
+#pragma unroll
+          for (int g4 = 0; g4 < 4; ++g4) {
+            const bf16x8& o8 = ops[g4 >> 1];
+            const int j0 = 4 * (g4 & 1);
+            *(bf16x4*)(dsx + dst_off(32 * kb + r, 8 * g4 + 4 * h)) =
+                bf16x4{o8[j0], o8[j0 + 1], o8[j0 + 2], o8[j0 + 3]};
+          }
+        }
+      }
     }
     accumulate(pw ? Oc : Qc, ops);
   };
+
+  // dQ of tile tq (atomic variant): dQ[row][32 w + r] += sum over the
+  // block's 64 keys of dS[row][key] K[key][32 w + r], A = dS^T read
+  // transposed from the exchange tile, B = kq; then one fp32 atomic add per
+  // element into the row's accumulator (unscaled; the caller converts).
+  // Key blocks whose pair skipped the tile (rows all above its keys) are
+  // skipped here too: their exchange tile was not written.
+  int trlo = 0, trhi = 0;
+  if (dq_on) {
+    const int i16 = lane & 15;
+    const int col = (lane & 16) + 4 * (i16 & 3);
+    trlo = dst_off(4 * h + (i16 >> 2), col);
+    trhi = dst_off(8 + 4 * h + (i16 >> 2), col);
+  }
+  float *dqa_p = nullptr, *dqa_s = nullptr;
+  if (dq_on) {
+    dqa_p = in_sgpr(a.dq_acc_p);
+    dqa_s = in_sgpr(a.dq_acc_s);
+  }
+  auto dq_step = [&](int tq, const RowTile& rt) {
+    if constexpr (AQ) {
+      const bool skip0 = rt.causal && rt.lp_first + BQ - 1 < k0;
+      const bool skip1 = rt.causal && rt.lp_first + BQ - 1 < k0 + 32;
+      if (skip0 || w >= NDB) return;
+      const bf16* dsx = L.ds[tq & 1];
+      auto ds_frag = [&](int v) {
+        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(dsx + 16 * v * kKvBQ + trlo));
+        const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(dsx + 16 * v * kKvBQ + trhi));
+        return bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+      };
+      f32x16 c = zero16();
+      c = mfma32(ds_frag(0), kq[0], c);
+      c = mfma32(ds_frag(1), kq[1], c);
+      if (!skip1) {
+        c = mfma32(ds_frag(2), kq[2], c);
+        c = mfma32(ds_frag(3), kq[3], c);
+      }
+      gfloat* base = (gfloat*)pick(rt.prefix, dqa_p, dqa_s) + ((size_t)rt.row0 * a.hq + rt.hh) * D + 32 * w + r;
+      const size_t rs = (size_t)a.hq * D;  // row stride
+      if (rt.nr >= BQ) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          __builtin_amdgcn_global_atomic_fadd_f32(base + (size_t)(c_row0(i) + 4 * h) * rs, c[i]);
+      } else {
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          if (c_row0(i) + 4 * h < rt.nr)
+            __builtin_amdgcn_global_atomic_fadd_f32(base + (size_t)(c_row0(i) + 4 * h) * rs, c[i]);
+      }
+    }
+  };
+
 
   // iteration t: the P-wave takes tile t, the dS-wave tile t - 1; tile t + 1
   // loads meanwhile
   Cursor cl = {t_lo / G, t_lo % G, 0};  // next tile to load
   Cursor cc = cl;                        // next tile this wave computes
+  Cursor cq = cl;                        // next tile whose dQ this wave adds
   if (ntiles > 0) {
     issue(cl);
     advance(cl);
   }
+  if (dq_on) {
+    // the block's 64 keys, staged once through Q/dO buffers 1-2 (free until
+    // the first iteration loads tile 1), then read as the dQ product's B
+    // operands; keys past the segment repeat the last one
+    const bf16* kb_ = (const bf16*)(kpre ? a.k_p : a.k_s);
+    load_tile<D, 4, kKvBK>(&L.q[1][0], kb_, kbase + k0, kseg - k0, a.hkv, hk, w, lane);
+  }
   tile_barrier();
-  for (int t = 0; t <= ntiles; ++t) {
+  if (dq_on) {
+    if (w < NDB) {
+      // K[16 v + k][32 w + r]: the transposed read of tr_frag at column
+      // block w (a wave-uniform index, so the offsets are formed here)
+      const int i16 = lane & 15, col = 32 * w + (lane & 16) + 4 * (i16 & 3);
+      const int olo = toff<D>(4 * h + (i16 >> 2), col), ohi = toff<D>(8 + 4 * h + (i16 >> 2), col);
+      const bf16* kt = &L.q[1][0];
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const bf16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(kt + 16 * v * D + olo));
+        const bf16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)(kt + 16 * v * D + ohi));
+        kq[v] = bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+      }
+#pragma unroll
+      for (int v = 0; v < 4; ++v) settle(kq[v]);
+    }
+    __syncthreads();  // every wave holds its operands before buffer 1 reloads
+  }
+  const int t_end = dq_on ? ntiles + 1 : ntiles;
+  for (int t = 0; t <= t_end; ++t) {
     if (t + 1 < ntiles) {
       issue(cl);
       advance(cl);
@@ -337,6 +455,14 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
       const RowTile rt = tile_info(cc);
       if (!hidden(rt)) compute(tc, rt, cc.buf);
       advance(cc);
+    }
+    if (dq_on) {
+      // the dS-waves published tile t - 2 one barrier ago
+      const int tq = t - 2;
+      if (tq >= 0 && tq < ntiles) {
+        dq_step(tq, tile_info(cq));
+        advance(cq);
+      }
     }
     tile_barrier();
   }
@@ -613,24 +739,31 @@ __device__ __forceinline__ void bwd_q_body(const AttnArgs& a, const int bid, bf1
 // one role, the rest the other, so that the key-outer and query-outer work
 // of a microbatch share the GPU (a suffix microbatch alone fills neither).
 // The heavier role goes first; both segments start on a multiple of 8 blocks
-// so the XCD mapping of each role holds.
-template <int D>
+// so the XCD mapping of each role holds.  The atomic-dQ variant (AQ) has the
+// key-outer role only: its blocks also add dQ into fp32 accumulators.
+template <int D, bool AQ>
 __global__ __launch_bounds__(kThreads, 2) void bwd_bf16_kernel(AttnArgs a, int n_first, int n_kv,
                                                                int n_q, int kv_first) {
   constexpr int TE = Tile<D>::ELEMS;
   // one LDS block shared by the two roles: the query-outer role's four
   // 64-key tiles, or the key-outer role's KvLds
-  constexpr int kBytes = sizeof(KvLds<D>) > 4 * TE * 2 ? sizeof(KvLds<D>) : 4 * TE * 2;
+  constexpr int kQBytes = AQ ? 0 : 4 * TE * 2;
+  constexpr int kBytes = sizeof(KvLds<D, AQ>) > kQBytes ? sizeof(KvLds<D, AQ>) : kQBytes;
   __shared__ __attribute__((aligned(1024))) unsigned char lds[kBytes];
   const int b = blockIdx.x;
-  const bool first = b < n_first;
-  const int bid = first ? b : b - n_first;
-  // the first segment is padded to a multiple of 8 blocks: padding exits
-  if (first == (kv_first != 0)) {
-    if (bid < n_kv) bwd_kv_body<D>(a, bid, *(KvLds<D>*)lds);
+  if constexpr (AQ) {
+    if (b < n_kv) bwd_kv_body<D, true>(a, b, *(KvLds<D, true>*)lds);
+    return;
   } else {
-    bf16(*tiles)[TE] = (bf16(*)[TE])lds;
-    if (bid < n_q) bwd_q_body<D>(a, bid, tiles, tiles + 2);
+    const bool first = b < n_first;
+    const int bid = first ? b : b - n_first;
+    // the first segment is padded to a multiple of 8 blocks: padding exits
+    if (first == (kv_first != 0)) {
+      if (bid < n_kv) bwd_kv_body<D, false>(a, bid, *(KvLds<D, false>*)lds);
+    } else {
+      bf16(*tiles)[TE] = (bf16(*)[TE])lds;
+      if (bid < n_q) bwd_q_body<D>(a, bid, tiles, tiles + 2);
+    }
   }
 }
 
@@ -715,10 +848,16 @@ __global__ __launch_bounds__(256) void bwd_kv_combine_kernel(AttnArgs a, int n_p
 
 hipError_t launch_bwd_bf16(const AttnArgs& a, int head_dim, int n_qz, bool deterministic,
                            hipStream_t st) {
-  (void)deterministic;  // both roles are deterministic: no atomics anywhere
   if (a.n_split > 1 && (a.prefix_rows || a.part_dq == nullptr)) return hipErrorInvalidValue;
   const int R = a.kv_rsplit > 1 ? a.kv_rsplit : 1;
   if (R > 1 && (a.part_dk == nullptr || a.part_dv == nullptr)) return hipErrorInvalidValue;
+  // the atomic-dQ launch has no query-outer role, and needs an accumulator
+  // for every kind of row its key tiles sweep
+  (void)deterministic;  // the default path has no atomics; the atomic one is asked for explicitly
+  const bool aq = a.dq_atomic != 0;
+  if (aq && (a.n_prefix_q_tiles || a.n_suffix_q_tiles || a.n_split > 1 ||
+             (a.prefix_rows && a.dq_acc_p == nullptr) || (a.n_seq > 0 && a.dq_acc_s == nullptr)))
+    return hipErrorInvalidValue;
   const long n_kt = (long)a.n_prefix_k_tiles + (long)a.n_seq * a.n_suffix_k_tiles;
   const long n_kv = n_kt * a.hkv * R;
   const long n_q = (long)(a.n_prefix_q_tiles + a.n_suffix_q_tiles) * a.hq * n_qz * a.n_split;
@@ -726,17 +865,25 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, int head_dim, int n_qz, bool deter
   // Phase C / dense prefix: the causal key tiles near the start of the prefix
   // carry the most rows.  Phase B suffix: every query tile sweeps the prefix,
   // so the query-outer role goes first unless its keys are split.
-  const int kv_first = (a.prefix_rows || a.n_split > 1) ? 1 : 0;
+  const int kv_first = (aq || a.prefix_rows || a.n_split > 1) ? 1 : 0;
   const long first = kv_first ? n_kv : n_q;
-  const long n_first = (first + 7) / 8 * 8;
+  const long n_first = aq ? n_kv : (first + 7) / 8 * 8;
   const long nb = n_first + (kv_first ? n_q : n_kv);
   ProfileScope ps("bwd_bf16", st);
-  if (head_dim == 64)
-    hipLaunchKernelGGL(bwd_bf16_kernel<64>, dim3((unsigned)nb), dim3(kThreads), 0, st, a, (int)n_first,
-                       (int)n_kv, (int)n_q, kv_first);
-  else
-    hipLaunchKernelGGL(bwd_bf16_kernel<128>, dim3((unsigned)nb), dim3(kThreads), 0, st, a, (int)n_first,
-                       (int)n_kv, (int)n_q, kv_first);
+  if (aq) {
+    if (head_dim == 64)
+      hipLaunchKernelGGL((bwd_bf16_kernel<64, true>), dim3((unsigned)nb), dim3(kThreads), 0, st, a,
+                         (int)n_first, (int)n_kv, 0, 1);
+    else
+      hipLaunchKernelGGL((bwd_bf16_kernel<128, true>), dim3((unsigned)nb), dim3(kThreads), 0, st, a,
+                         (int)n_first, (int)n_kv, 0, 1);
+  } else if (head_dim == 64) {
+    hipLaunchKernelGGL((bwd_bf16_kernel<64, false>), dim3((unsigned)nb), dim3(kThreads), 0, st, a,
+                       (int)n_first, (int)n_kv, (int)n_q, kv_first);
+  } else {
+    hipLaunchKernelGGL((bwd_bf16_kernel<128, false>), dim3((unsigned)nb), dim3(kThreads), 0, st, a,
+                       (int)n_first, (int)n_kv, (int)n_q, kv_first);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (R > 1 && n_kt > 0) {
@@ -764,17 +911,18 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, int head_dim, int n_qz, bool deter
 
 int bwd_bf16_block_q() { return kQBQ; }
 
-int bwd_bf16_kvsplit(long kv_tiles, long max_tiles) {
+int bwd_bf16_kvsplit(long kv_tiles, long max_tiles, bool atomic_dq) {
   // kv_tiles: the key-outer role's (32-row tile, q head) steps over all its
   // blocks; max_tiles: the longest block's.  The query-outer role adds about
   // 3/4 of that work (three products per visible block instead of four),
-  // spread over two slots per CU on 256 CUs.  A block clearly longer than
-  // that average per slot (by over 10%: the shares' partials and combine
-  // cost about that much) would end the launch alone: then every key tile's
-  // sweep is cut into R contiguous shares, about the average each, at most
-  // 8 and at least 16 steps each.
+  // spread over two slots per CU on 256 CUs; with atomic dQ there is no
+  // query-outer role and the dQ product lengthens every step alike.  A
+  // block clearly longer than that average per slot (by over 10%: the
+  // shares' partials and combine cost about that much) would end the launch
+  // alone: then every key tile's sweep is cut into R contiguous shares,
+  // about the average each, at most 8 and at least 16 steps each.
   if (kv_tiles <= 0 || max_tiles <= 0) return 1;
-  const double per_slot = 1.75 * (double)kv_tiles / 512.0;
+  const double per_slot = (atomic_dq ? 1.0 : 1.75) * (double)kv_tiles / 512.0;
   if ((double)max_tiles <= 1.1 * per_slot) return 1;
   long r = (long)std::ceil((double)max_tiles / per_slot);
   r = std::min(r, max_tiles / 16);

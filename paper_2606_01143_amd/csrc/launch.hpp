@@ -59,7 +59,7 @@ int bwd_bf16_block_k();
 // n_row_blocks (row tile, q head, suffix) blocks that each sweep
 // n_key_tiles key tiles
 int bwd_bf16_qsplit(int n_row_blocks, int n_key_tiles);
-int bwd_bf16_kvsplit(long kv_tiles, long max_tiles);
+int bwd_bf16_kvsplit(long kv_tiles, long max_tiles, bool atomic_dq);
 int bwd_bf16_block_q();
 int f32_block_q();
 int f32_block_k();

@@ -52,8 +52,10 @@ spr_status check_dims(const spr_dims* d) {
     return fail(SPR_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
   if (d->dtype != SPR_F32 && d->dtype != SPR_BF16)
     return fail(SPR_ERR_UNSUPPORTED, "dtype must be SPR_F32 or SPR_BF16");
-  if ((d->flags & ~(uint32_t)SPR_DETERMINISTIC) != 0)
+  if ((d->flags & ~(uint32_t)(SPR_DETERMINISTIC | SPR_ATOMIC_DQ)) != 0)
     return fail(SPR_ERR_UNSUPPORTED, "unknown flag bits");
+  if ((d->flags & SPR_DETERMINISTIC) && (d->flags & SPR_ATOMIC_DQ))
+    return fail(SPR_ERR_INVALID_ARG, "SPR_ATOMIC_DQ contradicts SPR_DETERMINISTIC");
   if (!(d->softmax_scale >= 0.f) || isinf(d->softmax_scale))
     return fail(SPR_ERR_INVALID_ARG, "softmax_scale must be finite and >= 0");
   return SPR_OK;
@@ -146,10 +148,12 @@ int suffix_fwd_splits(const spr_dims* d, int32_t n_mb, int32_t max_len) {
   return fwd_bf16_split(nrb, d->prefix_len);
 }
 
+bool atomic_dq(const spr_dims* d);
+
 // key splits of the suffix backward's query-outer role (bf16 path only),
 // see bwd_bf16_qsplit
 int suffix_bwd_splits(const spr_dims* d, int32_t n_mb, int32_t max_len) {
-  if (d->dtype != SPR_BF16) return 1;
+  if (d->dtype != SPR_BF16 || atomic_dq(d)) return 1;
   const int nrb = tiles(max_len, bwd_bf16_block_q()) * d->num_q_heads * n_mb;
   const int nkt = tiles(d->prefix_len, bwd_bf16_block_k()) + tiles(max_len, bwd_bf16_block_k());
   return bwd_bf16_qsplit(nrb, nkt);
@@ -165,9 +169,17 @@ long causal_steps(long len, long g) {
   for (long k0 = 0; k0 < len; k0 += 64) s += g * ((len - k0 + 31) / 32);
   return s;
 }
+// dQ of the bf16 backward: by default a query-outer role recomputes S and
+// dP for it (7 products per visible pair, no atomics, bitwise
+// reproducible); with SPR_ATOMIC_DQ the key-outer blocks add it with fp32
+// atomics (5 products per pair, one launch role).
+bool atomic_dq(const spr_dims* d) {
+  return d->dtype == SPR_BF16 && (d->flags & SPR_ATOMIC_DQ) != 0;
+}
+
 int bwd_kv_splits(const spr_dims* d, long kv_steps, long max_steps) {
   if (d->dtype != SPR_BF16) return 1;
-  return bwd_bf16_kvsplit(kv_steps * d->num_kv_heads, max_steps);
+  return bwd_bf16_kvsplit(kv_steps * d->num_kv_heads, max_steps, atomic_dq(d));
 }
 // Phase B: prefix key tiles see every suffix row (at most n_mb * max_len),
 // suffix key tiles their own causal rows
@@ -244,7 +256,7 @@ WsLayout ws_layout(int op, const spr_dims* d, int32_t n_mb, int32_t max_len, int
     case SPR_OP_SUFFIX_BWD: {
       w.dd_s = take(hq * T * 4);
       w.lse2_s = take(hq * T * 4);
-      if (f32) w.dq_acc_s = take(T * hq * hd * 4);
+      if (f32 || atomic_dq(d)) w.dq_acc_s = take(T * hq * hd * 4);
       const size_t ns = suffix_bwd_splits(d, n_mb, max_len);
       if (ns > 1) w.part_dq = take(ns * T * hq * hd * 4);
       const size_t rs = suffix_bwd_kv_splits(d, n_mb, max_len);
@@ -257,7 +269,7 @@ WsLayout ws_layout(int op, const spr_dims* d, int32_t n_mb, int32_t max_len, int
     case SPR_OP_PREFIX_BWD: {
       w.dd_p = take(hq * P * 4);
       w.lse2_p = take(hq * P * 4);
-      if (f32) w.dq_acc_p = take(P * hq * hd * 4);
+      if (f32 || atomic_dq(d)) w.dq_acc_p = take(P * hq * hd * 4);
       const size_t rs = prefix_bwd_kv_splits(d);
       if (rs > 1) {
         w.part_dk = take(rs * P * hkv * hd * 4);
@@ -294,7 +306,7 @@ WsLayout ws_layout(int op, const spr_dims* d, int32_t n_mb, int32_t max_len, int
       w.dq_acc_p = take(P * hq * hd * 4);
       w.dd_s = take(hq * T * 4);
       w.lse2_s = take(hq * T * 4);
-      if (f32) w.dq_acc_s = take(T * hq * hd * 4);
+      if (f32 || atomic_dq(d)) w.dq_acc_s = take(T * hq * hd * 4);
       w.dk_acc_p = take(P * hkv * hd * 4);
       w.dv_acc_p = take(P * hkv * hd * 4);
       {
@@ -591,13 +603,14 @@ spr_status spr_suffix_attn_bwd_accum(const spr_dims* dims, const void* k_p, cons
   if ((st = check_aliasing({bufs[12], bufs[13]}, all)) != SPR_OK) return st;
 
   const bool f32 = dims->dtype == SPR_F32;
+  const bool aq = atomic_dq(dims);
   float* dd_s = at<float>(ws, w.dd_s);
   float* lse2_s = at<float>(ws, w.lse2_s);
-  float* dq_acc = f32 ? at<float>(ws, w.dq_acc_s) : nullptr;
+  float* dq_acc = (f32 || aq) ? at<float>(ws, w.dq_acc_s) : nullptr;
   if ((st = hip_check(launch_row_dot(dims->dtype, do_s, o_s, total_len, total_len, nullptr, 0, (int)hq,
                                      (int)hd, dd_s, lse_s, lse2_s, stream), "row statistic")) != SPR_OK)
     return st;
-  if (f32 && (st = hip_check(launch_fill_zero(dq_acc, T * hq * hd, stream), "dq clear")) != SPR_OK)
+  if (dq_acc && (st = hip_check(launch_fill_zero(dq_acc, T * hq * hd, stream), "dq clear")) != SPR_OK)
     return st;
   AttnArgs a = base_args(dims);
   a.dq_s = dq_s;
@@ -616,17 +629,21 @@ spr_status spr_suffix_attn_bwd_accum(const spr_dims* dims, const void* k_p, cons
   a.pk_mode = kPkAccumulate;
   a.gk = gk_cache; a.gv = gv_cache;
   a.dk_s = dk_s; a.dv_s = dv_s;
-  a.n_suffix_q_tiles = tiles(max_len, block_q(dims->dtype));
-  a.n_split = suffix_bwd_splits(dims, n_mb, max_len);
-  if (a.n_split > 1) a.part_dq = at<float>(ws, w.part_dq);
+  if (aq) {
+    a.dq_atomic = 1;  // the key-outer blocks add dQ; no query-outer role
+  } else {
+    a.n_suffix_q_tiles = tiles(max_len, block_q(dims->dtype));
+    a.n_split = suffix_bwd_splits(dims, n_mb, max_len);
+    if (a.n_split > 1) a.part_dq = at<float>(ws, w.part_dq);
+  }
   a.kv_rsplit = suffix_bwd_kv_splits(dims, n_mb, max_len);
   if (a.kv_rsplit > 1) {
     a.part_dk = at<float>(ws, w.part_dk);
     a.part_dv = at<float>(ws, w.part_dv);
   }
   if ((st = hip_check(launch_bwd(dims, a, n_mb, stream), "suffix backward")) != SPR_OK) return st;
-  if (f32 && (st = hip_check(launch_convert(dims->dtype, dq_acc, a.scale, nullptr, dq_s,
-                                            T * hq * hd, stream), "dq convert")) != SPR_OK)
+  if (dq_acc && (st = hip_check(launch_convert(dims->dtype, dq_acc, a.scale, nullptr, dq_s,
+                                               T * hq * hd, stream), "dq convert")) != SPR_OK)
     return st;
   return ok();
 }
@@ -780,9 +797,12 @@ spr_status prefix_bwd_parts(const spr_dims* dims, const void* q_p, const void* k
     return ok();
   }
   const bool f32 = dims->dtype == SPR_F32;
+  // the whole Phase C adds dQ atomically from the key-outer blocks; the dQ
+  // half alone keeps its query-outer role (fewer products without dK/dV)
+  const bool aq = atomic_dq(dims) && want_dq && want_dkv;
   float* dd_p = at<float>(ws, w.dd_p);
   float* lse2_p = at<float>(ws, w.lse2_p);
-  float* dq_acc = f32 && want_dq ? at<float>(ws, w.dq_acc_p) : nullptr;
+  float* dq_acc = (f32 || aq) && want_dq ? at<float>(ws, w.dq_acc_p) : nullptr;
   if ((st = hip_check(launch_row_dot(dims->dtype, do_p, o_p, (int)P, (int)P, nullptr, 0, (int)hq, (int)hd,
                                      dd_p, lse_p, lse2_p, stream), "row statistic")) != SPR_OK)
     return st;
@@ -797,7 +817,10 @@ spr_status prefix_bwd_parts(const spr_dims* dims, const void* q_p, const void* k
   if (want_dq) {
     a.dq_p = dq_p;
     a.dq_acc_p = dq_acc;
-    a.n_prefix_q_tiles = tiles(dims->prefix_len, block_q(dims->dtype));
+    if (aq)
+      a.dq_atomic = 1;
+    else
+      a.n_prefix_q_tiles = tiles(dims->prefix_len, block_q(dims->dtype));
   }
   if (want_dkv) {
     a.pk_mode = kPkInject;
@@ -882,7 +905,8 @@ spr_status spr_dense_recompute_baseline(
   float* dd_s = at<float>(ws, w.dd_s);
   float* lse2_p = at<float>(ws, w.lse2_p);
   float* lse2_s = at<float>(ws, w.lse2_s);
-  float* dq_acc_s = f32 ? at<float>(ws, w.dq_acc_s) : nullptr;
+  const bool aq = atomic_dq(dims);
+  float* dq_acc_s = (f32 || aq) ? at<float>(ws, w.dq_acc_s) : nullptr;
   float* dk_acc = at<float>(ws, w.dk_acc_p);
   float* dv_acc = at<float>(ws, w.dv_acc_p);
   const float scale = eff_scale(dims);
@@ -890,7 +914,7 @@ spr_status spr_dense_recompute_baseline(
 #define SPR_TRY(expr, what) \
   if ((st = hip_check((expr), (what))) != SPR_OK) return st
   SPR_TRY(launch_fill_zero(dq_acc_p, P * hq * hd, stream), "clear");
-  if (f32) SPR_TRY(launch_fill_zero(dq_acc_s, T * hq * hd, stream), "clear");
+  if (dq_acc_s) SPR_TRY(launch_fill_zero(dq_acc_s, T * hq * hd, stream), "clear");
   SPR_TRY(launch_fill_zero(dk_acc, P * hkv * hd, stream), "clear");
   SPR_TRY(launch_fill_zero(dv_acc, P * hkv * hd, stream), "clear");
   // one trajectory at a time, as a dense trainer runs them
@@ -923,6 +947,13 @@ spr_status spr_dense_recompute_baseline(
     a.gk = dk_acc; a.gv = dv_acc;
     a.dk_s = dk_s; a.dv_s = dv_s;
     a.n_prefix_q_tiles = have_dop ? tiles(dims->prefix_len, block_q(dims->dtype)) : 0;
+    if (aq) {
+      // dQ of the prefix rows sums over the trajectories in dq_acc_p and of
+      // the suffix rows in dq_acc_s, both by the key-outer blocks' atomics
+      a.dq_atomic = 1;
+      a.n_prefix_q_tiles = 0;
+      a.n_suffix_q_tiles = 0;
+    }
     a.kv_rsplit = dense_bwd_kv_splits(dims, max_len);
     if (a.kv_rsplit > 1) {
       a.part_dk = at<float>(ws, w.part_dk);
@@ -933,7 +964,7 @@ spr_status spr_dense_recompute_baseline(
   SPR_TRY(launch_convert(dims->dtype, dq_acc_p, scale, nullptr, dq_p, P * hq * hd, stream), "convert");
   SPR_TRY(launch_convert(dims->dtype, dk_acc, 1.f, nullptr, dk_p, P * hkv * hd, stream), "convert");
   SPR_TRY(launch_convert(dims->dtype, dv_acc, 1.f, nullptr, dv_p, P * hkv * hd, stream), "convert");
-  if (f32) SPR_TRY(launch_convert(dims->dtype, dq_acc_s, scale, nullptr, dq_s, T * hq * hd, stream), "convert");
+  if (dq_acc_s) SPR_TRY(launch_convert(dims->dtype, dq_acc_s, scale, nullptr, dq_s, T * hq * hd, stream), "convert");
 #undef SPR_TRY
   return ok();
 }

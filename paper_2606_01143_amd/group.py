@@ -75,7 +75,7 @@ class DeviceGroup:
     """
 
     def __init__(self, inp: Dict, device="cuda:0", softmax_scale: float = 0.0,
-                 deterministic: bool = False, dense: bool = True,
+                 deterministic: bool = False, dense: bool = True, atomic_dq: bool = False,
                  microbatch_splits: Optional[Sequence[Sequence[Tuple[int, int]]]] = None,
                  layout: str = "packed"):
         if layout not in ("packed", "padded"):
@@ -89,7 +89,7 @@ class DeviceGroup:
         self.dtype = dt
         hq, hkv, d, p = shp.num_q_heads, shp.num_kv_heads, shp.head_dim, shp.prefix_len
         t = shp.total_suffix
-        self.dims = B.make_dims(hq, hkv, d, p, shp.dtype, softmax_scale, deterministic)
+        self.dims = B.make_dims(hq, hkv, d, p, shp.dtype, softmax_scale, deterministic, atomic_dq)
         self.lens = [int(x) for x in inp["suffix_lens"]]
         self.cu_host = [int(x) for x in inp["cu_seqlens"]]
 

@@ -17,7 +17,8 @@ them are outside the hot path), each with seeded synthetic inputs generated
 on the device.  Phase B takes one suffix per microbatch: the microbatch's
 tensors for every layer are made at its start and released after its
 backward, as a trainer's activations are.  Every launch is the same in both
-modes, so outputs and caches are bitwise identical with and without offload.
+modes, so outputs and caches are bitwise identical with and without offload
+(with ``atomic_dq=True`` dQ agrees to rounding only).
 """
 from __future__ import annotations
 
@@ -99,7 +100,7 @@ _DORMANT = ("q_p", "o_p", "lse_p", "g_y")
 class StackedGroup:
     def __init__(self, shape: StackShape, seed: int = 0, device="cuda:0", offload: bool = False,
                  pool_factor: float = 1.5, budget: Optional[HbmBudget] = None,
-                 keep_suffix_grads: bool = False):
+                 keep_suffix_grads: bool = False, atomic_dq: bool = False):
         self.shape = shape
         self.dev = torch.device(device)
         self.seed = seed
@@ -107,7 +108,7 @@ class StackedGroup:
         self.budget = budget or HbmBudget()
         self.keep_suffix_grads = keep_suffix_grads
         L, hq, hkv, d, P = shape.layers, shape.num_q_heads, shape.num_kv_heads, shape.head_dim, shape.prefix_len
-        self.dims = B.make_dims(hq, hkv, d, P, "bf16")
+        self.dims = B.make_dims(hq, hkv, d, P, "bf16", atomic_dq=atomic_dq)
         bf = torch.bfloat16
         # hot set and prefix outputs stay resident; dormant set may move
         self.layers: List[Dict[str, torch.Tensor]] = []

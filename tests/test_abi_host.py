@@ -241,3 +241,16 @@ def test_suffix_calls_check_host_offsets_before_launching(lib):
                           2, 4, 4, _addr(7), _addr(8), cu_host=[0, 4, 4])
     assert e.value.status_name == "SPR_ERR_INVALID_ARG"
     assert "length 0" in str(e.value)
+
+
+def test_atomic_dq_and_deterministic_flags_conflict(lib):
+    """SPR_ATOMIC_DQ with SPR_DETERMINISTIC is contradictory: INVALID_ARG
+    before anything is launched; either alone passes the dims check."""
+    d = _dims()
+    d.flags = B.SPR_ATOMIC_DQ | B.SPR_DETERMINISTIC
+    assert B.status_string(_call_prefix_fwd(d)) == "SPR_ERR_INVALID_ARG"
+    assert "SPR_ATOMIC_DQ" in B.last_error()
+    for f in (B.SPR_ATOMIC_DQ, B.SPR_DETERMINISTIC):
+        d.flags = f
+        out = ctypes.c_size_t(0)
+        assert B.lib().spr_workspace_size(B.OP_PREFIX_BWD, ctypes.byref(d), 0, 0, 0, ctypes.byref(out)) == 0

@@ -71,28 +71,35 @@ def test_row_shares_match_oracle(gpu, name, shape, mbs):
     _check(grp.fetch("dense"), dense_group_reference(inp), DENSE_KEYS, "dense")
 
 
+@pytest.mark.parametrize("deterministic", [True, False], ids=["deterministic", "atomic_dq"])
 @pytest.mark.parametrize("name,shape,mbs", CASES[:2], ids=[c[0] for c in CASES[:2]])
-def test_row_shares_bitwise_reproducible(gpu, name, shape, mbs):
+def test_row_shares_bitwise_reproducible(gpu, name, shape, mbs, deterministic):
+    """Reruns are bitwise equal: every output under SPR_DETERMINISTIC, every
+    output but dQ in the atomic-dQ mode (dQ to rounding there)."""
     from paper_2606_01143_amd.group import DeviceGroup
-    _announce(f"row shares reruns {name}")
+    _announce(f"row shares reruns {name} deterministic={deterministic}")
     inp = make_group(shape, seed=12)
-    grp = DeviceGroup(inp, dense=False)
+    grp = DeviceGroup(inp, dense=False, atomic_dq=not deterministic)
     grp.run_schedule()
     a = grp.fetch("schedule")
     grp.run_schedule()
     b = grp.fetch("schedule")
     for k in SCHED_KEYS:
-        assert np.array_equal(a[k], b[k]), k
+        if deterministic or not k.startswith("dq"):
+            assert np.array_equal(a[k], b[k]), k
+        else:
+            assert max_abs_rel(a[k], b[k], floor=1e-3) <= TOL, k
 
 
-def test_row_shares_prefix_backward_halves_equal_whole(gpu):
+@pytest.mark.parametrize("deterministic", [True, False], ids=["deterministic", "atomic_dq"])
+def test_row_shares_prefix_backward_halves_equal_whole(gpu, deterministic):
     import torch
     from paper_2606_01143_amd import binding as B
     from paper_2606_01143_amd.group import DeviceGroup
     shape = CASES[0][1]
-    _announce(f"row shares split Phase C {shape}")
+    _announce(f"row shares split Phase C {shape} deterministic={deterministic}")
     inp = make_group(shape, seed=13)
-    grp = DeviceGroup(inp, dense=False)
+    grp = DeviceGroup(inp, dense=False, atomic_dq=not deterministic)
     grp.run_schedule(overlap=False)
     o, d = grp.out, grp.dims
     ws2 = torch.empty_like(grp.ws)
@@ -104,7 +111,11 @@ def test_row_shares_prefix_backward_halves_equal_whole(gpu):
     B.prefix_bwd_dkv(d, grp.q_p, grp.k_p, grp.v_p, o["o_p"], o["lse_p"], grp.g_y, grp.gk, grp.gv,
                      dk, dv, grp.ws)
     torch.cuda.synchronize()
-    assert torch.equal(dq, ref["dq_p"]) and torch.equal(dk, ref["dk_p"]) and torch.equal(dv, ref["dv_p"])
+    assert torch.equal(dk, ref["dk_p"]) and torch.equal(dv, ref["dv_p"])
+    if deterministic:
+        assert torch.equal(dq, ref["dq_p"])
+    else:
+        assert max_abs_rel(dq.float().cpu().numpy(), ref["dq_p"].float().cpu().numpy(), floor=1e-3) <= TOL
 
 
 def test_row_shares_padded_equals_packed(gpu):

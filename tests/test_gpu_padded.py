@@ -32,7 +32,7 @@ def _announce(what):
     print(f"\n[gpu padded] {what}", flush=True)
 
 
-def _run_packed_and_padded(shape, seed, ragged=None):
+def _run_packed_and_padded(shape, seed, ragged=None, deterministic=True):
     import torch
     from paper_2606_01143_amd import binding as B
     inp = make_group(shape, seed=seed, ragged=ragged)
@@ -44,7 +44,7 @@ def _run_packed_and_padded(shape, seed, ragged=None):
     lens = [int(x) for x in inp["suffix_lens"]]
     n, s_max, T = len(lens), max(lens), sum(lens)
     cu_h = [0] + list(np.cumsum(lens))
-    dims = B.make_dims(hq, hkv, d, P, shape.dtype)
+    dims = B.make_dims(hq, hkv, d, P, shape.dtype, atomic_dq=not deterministic)
     k_p, v_p = up(inp["k_p"]), up(inp["v_p"])
     t = {k: up(inp[k]) for k in ("q_s", "k_s", "v_s", "do_s")}
     cu = torch.tensor(cu_h, dtype=torch.int32, device=dev)
@@ -81,10 +81,15 @@ def _run_packed_and_padded(shape, seed, ragged=None):
     torch.cuda.synchronize()
     packed = {"o": o, "lse": lse, "dq": dq, "dk": dk, "dv": dv}
     padded = {"o": po, "lse": plse, "dq": pdq, "dk": pdk, "dv": pdv}
+    exact = deterministic or shape.dtype == "f32"  # dQ of the atomic mode agrees to rounding only
     for key in packed:
         for i in range(n):
             got = padded[key][i, :lens[i]]
-            assert torch.equal(got, packed[key][cu_h[i]:cu_h[i + 1]]), (key, i)
+            want = packed[key][cu_h[i]:cu_h[i + 1]]
+            if exact or key != "dq":
+                assert torch.equal(got, want), (key, i)
+            else:
+                assert max_abs_rel(got.float().cpu().numpy(), want.float().cpu().numpy(), floor=1e-3) <= 2e-2
             assert not padded[key][i, lens[i]:].float().abs().sum().item(), (key, i, "padding not zero")
     assert torch.equal(gk, gk2) and torch.equal(gv, gv2)
     # the padded call's own valid rows and cache against the oracle
@@ -102,10 +107,11 @@ CASES = [
 
 
 @pytest.mark.gpu
+@pytest.mark.parametrize("deterministic", [True, False], ids=["deterministic", "atomic_dq"])
 @pytest.mark.parametrize("name,shape", CASES, ids=[c[0] for c in CASES])
-def test_padded_layout_is_bitwise_the_packed_layout(gpu, name, shape):
-    _announce(f"{name} {shape}")
-    _run_packed_and_padded(shape, seed=31)
+def test_padded_layout_is_bitwise_the_packed_layout(gpu, name, shape, deterministic):
+    _announce(f"{name} {shape} deterministic={deterministic}")
+    _run_packed_and_padded(shape, seed=31, deterministic=deterministic)
 
 
 @pytest.mark.gpu

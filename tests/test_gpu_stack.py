@@ -1,7 +1,8 @@
 """Stacked layers with the prefix-state lifecycle (paper Sec. 3.3, 4.3):
 offloading the dormant prefix state to pinned host memory and restoring it
 for Phase C (prefetched, demand-loaded, or through per-tensor pinned
-fallbacks) changes no result bit, over repeated steps."""
+fallbacks) changes no result bit, over repeated steps (with SPR_DETERMINISTIC,
+so that dQ is bitwise reproducible too)."""
 import pytest
 
 SHAPE_ARGS = dict(layers=3, num_q_heads=4, num_kv_heads=2, head_dim=128, prefix_len=300,

@@ -2,10 +2,13 @@
 sizes the library reports: a backward launch that splits its key tiles'
 row sweeps into R shares reserves R * (P + T) * Hkv * d fp32 partials for
 dK and for dV.  The rule is restated here from its description (work in
-(32-row tile, q head) steps of 64-key tiles; the query-outer role adds 3/4;
-two slots per CU on 256 CUs; split when the longest sweep exceeds the
-average per slot by over 10%, R = ceil(longest / average), 1 <= R <= 8,
-each share >= 16 steps) and compared with the library's choice."""
+(32-row tile, q head) steps of 64-key tiles; by default the query-outer
+role adds 3/4, with SPR_ATOMIC_DQ there is no such role; two slots
+per CU on 256 CUs; split when the longest sweep exceeds the average per slot
+by over 10%, R = ceil(longest / average), 1 <= R <= 8, each share >= 16
+steps) and compared with the library's choice.  The atomic mode also
+reserves the fp32 dQ accumulator of the launch's rows and never splits the
+query-outer keys (it has no query-outer role)."""
 import math
 
 import pytest
@@ -21,25 +24,25 @@ def _causal(length, g):
     return sum(g * ((length - k0 + 31) // 32) for k0 in range(0, length, 64))
 
 
-def _rule(kv_steps, max_steps):
+def _rule(kv_steps, max_steps, atomic):
     if kv_steps <= 0 or max_steps <= 0:
         return 1
-    per_slot = 1.75 * kv_steps / 512.0
+    per_slot = (1.0 if atomic else 1.75) * kv_steps / 512.0
     if max_steps <= 1.1 * per_slot:
         return 1
     return max(1, min(math.ceil(max_steps / per_slot), max_steps // 16, 8))
 
 
-def _suffix_r(hq, hkv, P, n, ml):
+def _suffix_r(hq, hkv, P, n, ml, atomic):
     g, rows = hq // hkv, n * ml
     kv = _tiles(P, 64) * g * ((rows + 31) // 32) + n * _causal(ml, g)
     crit = g * ((rows + 31) // 32) if P > 0 else g * ((ml + 31) // 32)
-    return _rule(kv * hkv, crit)
+    return _rule(kv * hkv, crit, atomic)
 
 
-def _prefix_r(hq, hkv, P):
+def _prefix_r(hq, hkv, P, atomic):
     g = hq // hkv
-    return _rule(_causal(P, g) * hkv, g * ((P + 31) // 32))
+    return _rule(_causal(P, g) * hkv, g * ((P + 31) // 32), atomic)
 
 
 def _qsplit(hq, P, n, ml):
@@ -56,20 +59,25 @@ def _align(x):
     return (x + 255) // 256 * 256
 
 
-def _suffix_ws(hq, hkv, d, P, n, ml, T):
+def _suffix_ws(hq, hkv, d, P, n, ml, T, atomic):
     off = _align(hq * T * 4) + _align(hq * T * 4)  # row statistic, log2 LSE
-    ns = _qsplit(hq, P, n, ml)
-    if ns > 1:
-        off += _align(ns * T * hq * d * 4)
-    r = _suffix_r(hq, hkv, P, n, ml)
+    if atomic:
+        off += _align(T * hq * d * 4)  # fp32 dQ accumulator
+    else:
+        ns = _qsplit(hq, P, n, ml)
+        if ns > 1:
+            off += _align(ns * T * hq * d * 4)
+    r = _suffix_r(hq, hkv, P, n, ml, atomic)
     if r > 1:
         off += 2 * _align(r * (P + T) * hkv * d * 4)
     return off, r
 
 
-def _prefix_ws(hq, hkv, d, P):
+def _prefix_ws(hq, hkv, d, P, atomic):
     off = _align(hq * P * 4) * 2
-    r = _prefix_r(hq, hkv, P)
+    if atomic:
+        off += _align(P * hq * d * 4)
+    r = _prefix_r(hq, hkv, P, atomic)
     if r > 1:
         off += 2 * _align(r * P * hkv * d * 4)
     return off, r
@@ -88,31 +96,39 @@ CASES = [
 ]
 
 
+MODES = pytest.mark.parametrize("atomic", [True, False], ids=["atomic_dq", "deterministic"])
+
+
+@MODES
 @pytest.mark.parametrize("hq,hkv,d,P,n,ml,T", CASES)
-def test_suffix_backward_workspace_follows_the_rule(hq, hkv, d, P, n, ml, T):
-    dims = B.make_dims(hq, hkv, d, P, "bf16")
-    want, r = _suffix_ws(hq, hkv, d, P, n, ml, T)
+def test_suffix_backward_workspace_follows_the_rule(hq, hkv, d, P, n, ml, T, atomic):
+    dims = B.make_dims(hq, hkv, d, P, "bf16", atomic_dq=atomic)
+    want, r = _suffix_ws(hq, hkv, d, P, n, ml, T, atomic)
     assert B.workspace_size(B.OP_SUFFIX_BWD, dims, n, ml, T) == want, r
 
 
+@MODES
 @pytest.mark.parametrize("hq,hkv,d,P", sorted({(c[0], c[1], c[2], c[3]) for c in CASES}))
-def test_prefix_backward_workspace_follows_the_rule(hq, hkv, d, P):
-    dims = B.make_dims(hq, hkv, d, P, "bf16")
-    want, r = _prefix_ws(hq, hkv, d, P)
+def test_prefix_backward_workspace_follows_the_rule(hq, hkv, d, P, atomic):
+    dims = B.make_dims(hq, hkv, d, P, "bf16", atomic_dq=atomic)
+    want, r = _prefix_ws(hq, hkv, d, P, atomic)
     assert B.workspace_size(B.OP_PREFIX_BWD, dims) == want, r
 
 
 def test_rule_decisions_at_named_shapes():
-    # the bench workload: Phase B whole, Phase C in two shares
-    assert _suffix_r(32, 8, 4096, 1, 512) == 1 and _prefix_r(32, 8, 4096) == 2
+    # Llama3-8B group at P = 4096: Phase B whole, Phase C in two shares
+    for atomic in (False, True):
+        assert _suffix_r(32, 8, 4096, 1, 512, atomic) == 1 and _prefix_r(32, 8, 4096, atomic) == 2
+    # the long-context group (P = 28672) fills the GPU without shares
+    assert _prefix_r(32, 8, 28672, True) == 1 and _suffix_r(32, 8, 28672, 1, 128, True) == 1
     # one kv head, short prefix: the sweeps are cut
-    assert _suffix_r(4, 1, 2048, 1, 700) == 5 and _prefix_r(4, 1, 2048) == 8
+    assert _suffix_r(4, 1, 2048, 1, 700, False) == 5 and _prefix_r(4, 1, 2048, False) == 8
     # long prefixes fill the GPU without shares
-    assert _prefix_r(32, 8, 16384) == 1 and _suffix_r(4, 1, 131072, 2, 1000) == 1
+    assert _prefix_r(32, 8, 16384, False) == 1 and _suffix_r(4, 1, 131072, 2, 1000, False) == 1
 
 
 def test_fp32_storage_never_splits():
-    dims = B.make_dims(4, 1, 128, 2048, "f32")
+    dims = B.make_dims(4, 1, 128, 2048, "f32")  # fp32 storage has no atomic mode either
     base = B.workspace_size(B.OP_SUFFIX_BWD, dims, 1, 700, 700)
     # fp32: row statistic, log2 LSE and the fp32 dQ accumulator only
     assert base == _align(4 * 700 * 4) * 2 + _align(700 * 4 * 128 * 4)

@@ -5,11 +5,12 @@
 // What it computes (paper App. A.2-A.5): with P = exp(S - LSE),
 // dP = dO V^T and dS = P * (dP - rowsum(dO * O)) over the joint row,
 //   dV = P^T dO,  dK = dS^T Q / sqrt(d),  dQ = dS K / sqrt(d).
-// Two kernels split the work so that no gradient needs atomics:
+// Two workgroup roles split the work so that, by default, no gradient needs
+// atomics (with SPR_ATOMIC_DQ the key-outer role also adds dQ, see below):
 //
-// bwd_kv (key-outer): one workgroup owns a 128-key tile of one kv head (32
-//   keys per wave) and sweeps every query row that sees it, for all G q
-//   heads of the kv head.  For a prefix key tile in Phase B the rows are all
+// bwd_kv (key-outer): one workgroup owns a 64-key tile of one kv head, as
+//   two wave pairs of 32 keys, and sweeps every query row that sees it, for
+//   all G q heads of the kv head.  For a prefix key tile in Phase B the rows are all
 //   suffix rows of the microbatch, so the tile's dK/dV are exactly
 //   gK_1 = dS_21^T Q_2 / sqrt(d) and gV_1 = P_21^T dO_2; the workgroup adds
 //   them into the fp32 cache G_K/G_V with a plain read-modify-write.  Each
@@ -25,10 +26,11 @@
 //     S^T = K Q^T, dP^T = V dO^T   A = K/V tile rows, B = Q/dO (registers)
 //     dQ^T += K^T dS^T             A = K tile read transposed, B = dS^T registers
 //   and writes dQ once, already scaled and rounded.
-// Both stream their tiles through double-buffered LDS, filled by
-// direct-to-LDS loads issued one tile ahead of the products.  The loads
-// are invisible to the compiler's wait tracking: every tile is read only
-// after tile_barrier (vmcnt(0) + workgroup barrier).
+// Both stream their tiles through LDS (the key-outer role's 32-row Q/dO
+// tiles triple-buffered, the query-outer role's 64-key K/V tiles
+// double-buffered), filled by direct-to-LDS loads issued one tile ahead of
+// the products.  The loads are invisible to the compiler's wait tracking:
+// every tile is read only after tile_barrier (vmcnt(0) + workgroup barrier).
 #include <algorithm>
 #include <cmath>
 

@@ -311,8 +311,8 @@ def main():
     ap.add_argument("--layer", action="store_true",
                     help="a long-context Llama3-8B decoder layer through the schedule vs dense")
     ap.add_argument("--stack", action="store_true",
-                    help="Phase-B HBM with and without dormant-prefix offload over a layer stack")
-    ap.add_argument("--layers", type=int, default=32)
+                    help="Phase-B HBM with and without dormant-prefix offload over a decoder-layer stack")
+    ap.add_argument("--layers", type=int, default=16, help="decoder layers of --stack")
     ap.add_argument("--shard", action="store_true",
                     help="the Qwen3-8B sweep kernels on one GPU's kv-head share (Hkv = 8/g, g = 1, 2, 4, 8)")
     ap.add_argument("--moe-aux", action="store_true",
@@ -618,19 +618,24 @@ def layer_bench(args):
 def stack_bench(args):
     """Phase-B HBM with and without offloading the dormant prefix state (the
     measurement of the paper's Table 6, Sec. 5.5): a stack of Llama3-8B
-    attention layers (GQA 32/8, d = 128), N = 16 suffixes, total length
-    12288 split between prefix and suffix.  One JSON line per split."""
+    decoder layers (hidden 4096, GQA 32/8, d 128, SwiGLU 14336; weights and
+    inputs drawn on the GPU), chained across layers, N = 16 suffixes, total
+    length 12288 split between prefix and suffix.  One JSON line per split:
+    the allocator's peak during Phase B, the step time, and the dormant
+    bytes moved to pinned host memory."""
     import torch
-    from paper_2606_01143_amd.stack import StackedGroup, StackShape
+    from paper_2606_01143_amd.stack import DecoderStack
+    from synthetic.layer import LayerShape
     L = args.layers
     gib = float(1 << 30)
     for P, S in ((2048, 10240), (6144, 6144), (8192, 4096), (10240, 2048)):
-        shape = StackShape(L, 32, 8, 128, P, (S,) * 16)
-        rec = {"workload": f"llama3_8b_attn_stack{L}_p{P}_s{S}_n16", "layers": L, "prefix_len": P,
+        shape = LayerShape(4096, 32, 8, 128, 14336, P, (S,) * 16)
+        rec = {"workload": f"llama3_8b_decoder_stack{L}_p{P}_s{S}_n16", "layers": L, "prefix_len": P,
                "suffix_len": S, "n_suffixes": 16, "dtype": "bf16", "data": "synthetic"}
         for offload in (False, True):
-            sg = StackedGroup(shape, seed=args.seed, offload=offload)
-            sg.run()  # warm: allocator pools, pinned pool, kernels
+            log(f"stack P={P} S={S} offload={offload}")
+            st = DecoderStack(shape=shape, layers=L, seed=args.seed, offload=offload, pool_factor=1.1)
+            st.run_schedule()  # warm: allocator pools, pinned pool, kernels
             torch.cuda.synchronize()
             marks = {}
 
@@ -645,8 +650,9 @@ def stack_bench(args):
 
             start = torch.cuda.Event(enable_timing=True)
             start.record()
-            sg.run(on_phase=mark)
+            out = st.run_schedule(on_phase=mark)
             torch.cuda.synchronize()
+            del out
             key = "offload" if offload else "no_offload"
             rec[f"phase_b_peak_gib_{key}"] = round(marks["peak_b"] / gib, 3)
             rec[f"step_ms_{key}"] = round(start.elapsed_time(marks["C"]), 2)
@@ -654,10 +660,14 @@ def stack_bench(args):
                                       "B": round(marks["A"].elapsed_time(marks["B"]), 2),
                                       "C": round(marks["B"].elapsed_time(marks["C"]), 2)}
             if offload:
-                rec["dormant_gib"] = round(sg.dormant_bytes / gib, 3)
-                rec["restores"] = {k: v for k, v in sg.stats.items()}
-            del sg
+                rec["dormant_gib"] = round(st.dormant_bytes / gib, 3)
+                rec["restores"] = {k: v for k, v in st.stats.items()}
+            del st
             torch.cuda.empty_cache()
+            # pinned host blocks go back to the driver too (the next split's
+            # pool is larger and cannot reuse them)
+            if hasattr(torch._C, "_host_emptyCache"):
+                torch._C._host_emptyCache()
         red = rec["phase_b_peak_gib_no_offload"] - rec["phase_b_peak_gib_offload"]
         rec["reduction_gib"] = round(red, 3)
         rec["reduction_pct"] = round(100 * red / rec["phase_b_peak_gib_no_offload"], 1)

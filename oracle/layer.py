@@ -19,6 +19,15 @@ prefix forward once; Phase B per suffix, forward and backward with the
 prefix K/V as leaves whose gradients accumulate (the gK/gV cache); Phase C
 one prefix backward with G_Y = sum_i dY_P(i) and the accumulated cache
 injected into the prefix K/V.  Both use torch autograd in float64.
+
+``dense_stack_reference`` and ``reordered_stack_reference`` do the same
+for a stack of layers, each with its own weights, the output of layer l
+being the input of layer l + 1 (App. A.7): the reordered stack runs the
+prefix through every layer once (Phase A), each suffix forward through
+every layer against that layer's cached prefix K/V and backward from the
+top (Phase B, one cache per layer), then the prefix backward from the top
+layer down (Phase C), layer l's injected cache and upstream adjoint giving
+the prefix hidden-state adjoint that layer l - 1 receives as its G_Y.
 """
 from __future__ import annotations
 
@@ -156,4 +165,114 @@ def group_loss(inp: Dict) -> float:
             y = _tail(x, attention(q, k, v, torch.tril(torch.ones(L, L, dtype=torch.bool))), W, shp)
             dy = _t(np.concatenate([inp["dy_p"][i], inp["dy_s"][i]], axis=0))
             total += float((y * dy).sum())
+    return total
+
+
+# ---------------------------------------------------------------------------
+# A stack of layers (App. A.7: the schedule extended across layers)
+# ---------------------------------------------------------------------------
+
+def _stack_weights(inp):
+    return [{k: _t(w[k], grad=True) for k in W_KEYS} for w in inp["weights"]]
+
+
+def _layer(x, W, shp, pos, visible, k_extra=None, v_extra=None):
+    """One layer over rows x at positions pos; k_extra/v_extra: cached
+    prefix K/V placed before the rows' own keys.  Returns y, k, v."""
+    q, k, v = _qkv(x, W, shp, pos)
+    kk = k if k_extra is None else torch.cat([k_extra, k])
+    vv = v if v_extra is None else torch.cat([v_extra, v])
+    return _tail(x, attention(q, kk, vv, visible), W, shp), k, v
+
+
+def dense_stack_reference(inp: Dict) -> Dict:
+    """Every trajectory [P||S(i)] through all layers, upstream
+    [dY_P(i); dY_S(i)] at the top; the prefix's and every layer's weight
+    gradients summed over the trajectories."""
+    shp = inp["shape"]
+    P = shp.prefix_len
+    Ws = _stack_weights(inp)
+    y_s, dx_s, y_p = [], [], None
+    dx_p = torch.zeros(P, shp.hidden, dtype=torch.float64)
+    for i in range(shp.n):
+        x0 = _t(np.concatenate([inp["x_p"], inp["x_s"][i]], axis=0), grad=True)
+        L = x0.shape[0]
+        pos = torch.arange(L)
+        vis = torch.tril(torch.ones(L, L, dtype=torch.bool))
+        x = x0
+        for W in Ws:
+            x, _, _ = _layer(x, W, shp, pos, vis)
+        x.backward(_t(np.concatenate([inp["dy_p"][i], inp["dy_s"][i]], axis=0)))
+        dx_p += x0.grad[:P]
+        dx_s.append(x0.grad[P:].numpy())
+        y_s.append(x[P:].detach().numpy())
+        if y_p is None:
+            y_p = x[:P].detach().numpy()
+    return {"y_p": y_p, "y_s": y_s, "dx_p": dx_p.numpy(), "dx_s": dx_s,
+            "dw": [{k: W[k].grad.numpy() for k in W_KEYS} for W in Ws]}
+
+
+def reordered_stack_reference(inp: Dict) -> Dict:
+    """The three-phase schedule over the stack (see the module docstring)."""
+    shp = inp["shape"]
+    P = shp.prefix_len
+    Ws = _stack_weights(inp)
+    pos_p = torch.arange(P)
+    vis_p = torch.tril(torch.ones(P, P, dtype=torch.bool))
+    # Phase A: the prefix through every layer once; layer l's graph (input
+    # leaf, output, K/V) is kept for its Phase C
+    xs, ys, ks, vs = [], [], [], []
+    x = _t(inp["x_p"])
+    for W in Ws:
+        x_in = x.detach().requires_grad_(True)
+        y, k, v = _layer(x_in, W, shp, pos_p, vis_p)
+        xs.append(x_in); ys.append(y); ks.append(k); vs.append(v)
+        x = y
+    # the caches: every layer's prefix K/V as leaves whose gradients accumulate
+    k_c = [k.detach().requires_grad_(True) for k in ks]
+    v_c = [v.detach().requires_grad_(True) for v in vs]
+    # Phase B: each suffix forward through the layers against their cached
+    # prefix K/V, then backward from the top
+    y_s, dx_s = [], []
+    for i in range(shp.n):
+        x0 = _t(inp["x_s"][i], grad=True)
+        s = x0.shape[0]
+        pos = torch.arange(P, P + s)
+        vis = torch.cat([torch.ones(s, P, dtype=torch.bool), torch.tril(torch.ones(s, s, dtype=torch.bool))], dim=1)
+        x = x0
+        for l, W in enumerate(Ws):
+            x, _, _ = _layer(x, W, shp, pos, vis, k_c[l], v_c[l])
+        x.backward(_t(inp["dy_s"][i]))
+        y_s.append(x.detach().numpy())
+        dx_s.append(x0.grad.numpy())
+    # Phase C: from the top layer down, the upstream adjoint of layer l's
+    # prefix output plus its injected cache give the adjoint of its input,
+    # which is layer l - 1's upstream
+    g = _t(np.sum(np.asarray(inp["dy_p"], dtype=np.float64), axis=0))
+    for l in reversed(range(len(Ws))):
+        outs, grads = [ys[l]], [g]
+        for t, leaf in ((ks[l], k_c[l]), (vs[l], v_c[l])):
+            if leaf.grad is not None:
+                outs.append(t)
+                grads.append(leaf.grad)
+        torch.autograd.backward(outs, grads)
+        g = xs[l].grad
+    return {"y_p": ys[-1].detach().numpy(), "y_s": y_s, "dx_p": g.numpy(), "dx_s": dx_s,
+            "dw": [{k: W[k].grad.numpy() for k in W_KEYS} for W in Ws]}
+
+
+def stack_group_loss(inp: Dict) -> float:
+    """L = sum_i <Y(i), dY(i)> over the dense trajectories through the stack."""
+    shp = inp["shape"]
+    Ws = [{k: _t(w[k]) for k in W_KEYS} for w in inp["weights"]]
+    total = 0.0
+    with torch.no_grad():
+        for i in range(shp.n):
+            x = _t(np.concatenate([inp["x_p"], inp["x_s"][i]], axis=0))
+            L = x.shape[0]
+            pos, vis = torch.arange(L), torch.tril(torch.ones(L, L, dtype=torch.bool))
+            for W in Ws:
+                x, _, _ = _layer(x, W, shp, pos, vis)
+            dy = _t(np.concatenate([inp["dy_p"][i], inp["dy_s"][i]], axis=0))
+            total += float((x * dy).sum())
     return total

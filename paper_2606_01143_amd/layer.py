@@ -32,12 +32,9 @@ W_KEYS = ("wq", "wk", "wv", "wo", "wg", "wu", "wd")
 class DecoderLayer:
     def __init__(self, inp: Dict, device="cuda:0"):
         shp = inp["shape"]
-        if shp.dtype != "bf16":
-            raise ValueError("the layer path runs in bf16")
-        self.shape = shp
-        self.dev = torch.device(device)
-        up = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(device=self.dev, dtype=torch.bfloat16)
-        self.w = {k: up(inp["weights"][k]) for k in W_KEYS}
+        dev = torch.device(device)
+        up = lambda x: torch.from_numpy(np.ascontiguousarray(x)).to(device=dev, dtype=torch.bfloat16)
+        self._setup(shp, {k: up(inp["weights"][k]) for k in W_KEYS}, dev, None)
         self.x_p = up(inp["x_p"])
         self.x_s = [up(x) for x in inp["x_s"]]
         self.dy_s = [up(x) for x in inp["dy_s"]]
@@ -45,17 +42,37 @@ class DecoderLayer:
         # G_Y summed in fp32, rounded once
         self.g_y = torch.stack([x.float() for x in self.dy_p]).sum(0).to(torch.bfloat16) if shp.n else \
             torch.zeros_like(self.x_p)
+
+    @classmethod
+    def of_weights(cls, shape, weights: Dict[str, torch.Tensor], device, ws: Optional[torch.Tensor] = None):
+        """A layer of a stack: its bf16 weights on the device, its own gK/gV
+        cache; ``ws`` a workspace shared by the stack's layers."""
+        layer = cls.__new__(cls)
+        layer._setup(shape, weights, torch.device(device), ws)
+        return layer
+
+    def _setup(self, shp, weights, dev, ws):
+        if shp.dtype != "bf16":
+            raise ValueError("the layer path runs in bf16")
+        self.shape = shp
+        self.dev = dev
+        self.w = weights
         hq, hkv, d, P = shp.num_q_heads, shp.num_kv_heads, shp.head_dim, shp.prefix_len
         self.dims = B.make_dims(hq, hkv, d, P, "bf16")
         self.gk = torch.zeros(P, hkv, d, dtype=torch.float32, device=self.dev)
         self.gv = torch.zeros_like(self.gk)
-        mx = max(shp.suffix_lens) if shp.n else 1
-        need = max(B.workspace_size(B.OP_PREFIX_BWD, self.dims),
-                   B.workspace_size(B.OP_SUFFIX_FWD, self.dims, 1, mx, mx),
-                   B.workspace_size(B.OP_SUFFIX_BWD, self.dims, 1, mx, mx), 256)
-        self.ws = torch.empty(need, dtype=torch.uint8, device=self.dev)
+        if ws is None:
+            ws = torch.empty(self.workspace_bytes(shp), dtype=torch.uint8, device=self.dev)
+        self.ws = ws
         self._cu = {}
         self._dense_dims = {}
+
+    @staticmethod
+    def workspace_bytes(shp) -> int:
+        dims = B.make_dims(shp.num_q_heads, shp.num_kv_heads, shp.head_dim, shp.prefix_len, "bf16")
+        mx = max(shp.suffix_lens) if shp.n else 1
+        return max(B.workspace_size(B.OP_PREFIX_BWD, dims), B.workspace_size(B.OP_SUFFIX_FWD, dims, 1, mx, mx),
+                   B.workspace_size(B.OP_SUFFIX_BWD, dims, 1, mx, mx), 256)
 
     # ---------------------------------------------------------- token-wise
     def _forward(self, x: torch.Tensor, pos0: int, attend) -> Dict[str, torch.Tensor]:

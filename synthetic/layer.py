@@ -20,7 +20,7 @@ import numpy as np
 
 from . import round_to_bf16
 
-__all__ = ["LayerShape", "make_layer_group", "LAYER_SHAPES"]
+__all__ = ["LayerShape", "make_layer_group", "make_stack_group", "LAYER_SHAPES"]
 
 
 @dataclass(frozen=True)
@@ -71,6 +71,46 @@ def make_layer_group(shape: LayerShape, seed: int = 0,
         dy_s.append(draw((s, h)))
         dy_p.append(draw((shp.prefix_len, h)))
     return {"shape": shp, "weights": w, "x_p": x_p, "x_s": x_s, "dy_s": dy_s, "dy_p": dy_p}
+
+
+def make_stack_group(shape: LayerShape, layers: int, seed: int = 0,
+                     ragged: Optional[Tuple[int, int]] = None) -> Dict:
+    """A stack of ``layers`` decoder layers of one shape, each with its own
+    weights, and one prompt group of inputs to the bottom layer and upstream
+    adjoints at the top.  Draw order: [ragged groups: the suffix lengths],
+    then for each layer its seven weights in the single-layer order, then
+    X_P, then for each suffix X_S(i), dY_S(i), dY_P(i).  Returns the
+    single-layer dict with ``weights`` a list (bottom layer first)."""
+    rng = np.random.default_rng(seed)
+    lens = tuple(shape.suffix_lens)
+    if ragged is not None:
+        lo, hi = ragged
+        lens = tuple(int(v) for v in rng.integers(lo, hi + 1, size=len(lens)))
+    shp = LayerShape(shape.hidden, shape.num_q_heads, shape.num_kv_heads, shape.head_dim,
+                     shape.intermediate, shape.prefix_len, lens, shape.dtype, shape.rope_theta,
+                     shape.norm_eps, shape.weight_std)
+
+    def draw(shp_, std=1.0):
+        x = rng.standard_normal(size=shp_, dtype=np.float32)
+        if std != 1.0:
+            x = (x * np.float32(std)).astype(np.float32)
+        return round_to_bf16(x) if shp.dtype == "bf16" else x
+
+    h, hq, hkv, d, I = shp.hidden, shp.num_q_heads, shp.num_kv_heads, shp.head_dim, shp.intermediate
+    sd = shp.weight_std
+    ws = []
+    for _ in range(layers):
+        ws.append({"wq": draw((h, hq * d), sd), "wk": draw((h, hkv * d), sd), "wv": draw((h, hkv * d), sd),
+                   "wo": draw((hq * d, h), sd), "wg": draw((h, I), sd), "wu": draw((h, I), sd),
+                   "wd": draw((I, h), sd)})
+    x_p = draw((shp.prefix_len, h))
+    x_s, dy_s, dy_p = [], [], []
+    for s in lens:
+        x_s.append(draw((s, h)))
+        dy_s.append(draw((s, h)))
+        dy_p.append(draw((shp.prefix_len, h)))
+    return {"shape": shp, "layers": layers, "weights": ws, "x_p": x_p, "x_s": x_s, "dy_s": dy_s,
+            "dy_p": dy_p}
 
 
 LAYER_SHAPES: Dict[str, LayerShape] = {

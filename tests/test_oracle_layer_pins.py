@@ -150,3 +150,96 @@ def test_planted_mistakes_are_caught(monkeypatch, mutation):
     except AssertionError:
         caught.append(True)
     assert any(caught), mutation
+
+
+# ---------------------------------------------------------------------------
+# the stack of layers (App. A.7)
+# ---------------------------------------------------------------------------
+from synthetic.layer import make_stack_group  # noqa: E402
+
+
+def pin_stack_reordered(shape, layers, seed, ragged=None):
+    inp = make_stack_group(shape, layers, seed=seed, ragged=ragged)
+    a, b = ol.dense_stack_reference(inp), ol.reordered_stack_reference(inp)
+    errs = [_rel(b["y_p"], a["y_p"]), _rel(b["dx_p"], a["dx_p"])]
+    errs += [_rel(x, y) for x, y in zip(b["y_s"], a["y_s"])] + [_rel(x, y) for x, y in zip(b["dx_s"], a["dx_s"])]
+    errs += [_rel(bw[k], aw[k]) for bw, aw in zip(b["dw"], a["dw"]) for k in ol.W_KEYS]
+    return max(errs)
+
+
+@pytest.mark.parametrize("shape,layers,seed", [
+    (LayerShape(16, 2, 1, 8, 32, 7, (3, 5), "f32"), 2, 1),
+    (LayerShape(32, 4, 2, 8, 48, 12, (4, 1, 9), "f32"), 3, 2),
+    (LayerShape(24, 2, 2, 12, 40, 5, (6,), "f32"), 2, 3),   # N = 1
+])
+def test_stack_reordered_equals_dense(shape, layers, seed):
+    """Prop. 1 across layers: the schedule over the stack (prefix once
+    through every layer, suffixes against each layer's cached prefix K/V,
+    the prefix backward from the top with each layer's cache injected and
+    the adjoint chained downwards) equals the dense per-trajectory stack,
+    every layer's weight gradients included."""
+    assert pin_stack_reordered(shape, layers, seed) < 1e-12
+
+
+def test_stack_of_one_layer_is_the_layer():
+    """One layer's stack is the single-layer reference (same draws up to
+    the weight list)."""
+    shape = LayerShape(16, 2, 1, 8, 32, 7, (3, 5), "f32")
+    st = make_stack_group(shape, 1, seed=6)
+    one = dict(st, weights=st["weights"][0])
+    a, b = ol.dense_stack_reference(st), ol.dense_layer_reference(one)
+    assert _rel(a["dx_p"], b["dx_p"]) < 1e-14 and _rel(a["y_p"], b["y_p"]) < 1e-14
+    for k in ol.W_KEYS:
+        assert _rel(a["dw"][0][k], b["dw"][k]) < 1e-14
+
+
+def test_stack_finite_differences(h=1e-4):
+    """The dense stack's gradients against central differences of the group
+    loss, on the bottom input, a suffix input and weights of both layers
+    (the adjoint chained through the layer above included)."""
+    inp = make_stack_group(LayerShape(8, 2, 1, 4, 16, 3, (2, 3), "f32"), 2, seed=8)
+    ref = ol.dense_stack_reference(inp)
+    probes = [("x_p", None, (1, 2)), ("x_s", 1, (2, 5)), ("wq", 0, (3, 1)), ("wk", 0, (0, 2)),
+              ("wv", 1, (5, 3)), ("wd", 0, (13, 4)), ("wg", 1, (7, 11))]
+    worst = 0.0
+    for key, sel, idx in probes:
+        vals = []
+        for sgn in (1, -1):
+            x = {"shape": inp["shape"], "layers": 2,
+                 "weights": [{k: v.astype(np.float64).copy() for k, v in w.items()} for w in inp["weights"]],
+                 "x_p": inp["x_p"].astype(np.float64).copy(),
+                 "x_s": [v.astype(np.float64).copy() for v in inp["x_s"]],
+                 "dy_s": inp["dy_s"], "dy_p": inp["dy_p"]}
+            if key == "x_p":
+                x["x_p"][idx] += sgn * h
+            elif key == "x_s":
+                x["x_s"][sel][idx] += sgn * h
+            else:
+                x["weights"][sel][key][idx] += sgn * h
+            vals.append(ol.stack_group_loss(x))
+        fd = (vals[0] - vals[1]) / (2 * h)
+        if key == "x_p":
+            an = ref["dx_p"][idx]
+        elif key == "x_s":
+            an = ref["dx_s"][sel][idx]
+        else:
+            an = ref["dw"][sel][key][idx]
+        worst = max(worst, abs(fd - an) / max(abs(an), 1e-3))
+    assert worst < 1e-6, worst
+
+
+def test_stack_planted_mistake_is_caught(monkeypatch):
+    """Dropping the chained adjoint (every layer's Phase C starting from
+    G_Y instead of the adjoint from the layer above) breaks the stack pin."""
+    orig = ol.reordered_stack_reference
+
+    def broken(inp):
+        shp = inp["shape"]
+        out = orig(inp)
+        # recompute Phase C of the bottom layer alone with the top G_Y
+        one = dict(inp, weights=inp["weights"][0], x_s=[np.zeros_like(x) for x in inp["x_s"]])
+        return dict(out, dx_p=ol.reordered_layer_reference(one)["dx_p"])
+
+    monkeypatch.setattr(ol, "reordered_stack_reference", broken)
+    shape = LayerShape(16, 2, 1, 8, 32, 7, (3, 5), "f32")
+    assert pin_stack_reordered(shape, 2, 1) > 1e-6

@@ -248,6 +248,20 @@ def host_facts():
     return facts
 
 
+def gemm_bf16_rate(n: int = 8192, reps: int = 10):
+    """A measured dense bf16 matrix-core rate on this GPU: an n x n x n
+    torch.matmul (served by hipBLASLt), TFLOP/s, as a second denominator
+    beside the published peak."""
+    import torch
+    g = torch.Generator(device="cuda").manual_seed(1)
+    a = torch.randn(n, n, generator=g, device="cuda").to(torch.bfloat16)
+    b = torch.randn(n, n, generator=g, device="cuda").to(torch.bfloat16)
+    st = time_steps_stats(lambda: torch.matmul(a, b), reps, 3)
+    tf = 2.0 * n ** 3 / (st["min"] * 1e-3) / 1e12
+    return {"tflops": round(tf, 1), "shape": f"{n}x{n}x{n} bf16 (torch.matmul, hipBLASLt)",
+            "ms_min": round(st["min"], 4), "frac_of_published_peak": round(tf / BF16_PEAK_TFLOPS, 4)}
+
+
 def cpu_baseline(inp, shape, budget_s: float):
     """The fp64 oracle's three-phase reference on a bounded sample of the same
     group: one q head at a time with its kv head (heads are independent, so
@@ -499,6 +513,9 @@ def main():
                                    "measured": "HIP events around each launch of the last timed step"}}
     del grp
     torch.cuda.empty_cache()
+    gemm = gemm_bf16_rate()
+    out["gemm_bf16_measured"] = gemm
+    out["roofline"]["frac_of_measured_gemm"] = round(iso_achieved / gemm["tflops"], 4)
     if args.cpu_seconds > 0:
         log("cpu baseline (oracle)")
         out["cpu_baseline"] = cpu_baseline(inp, shape, args.cpu_seconds)

@@ -491,6 +491,23 @@ def main():
         out["policy_" + other_name]["speedup_vs_dense"] = round(ms_dense / st_o["mean"], 3)
         out["dense_policy"] = "one trajectory per launch pair (the dense trainer's per-sequence order)"
         log(f"dense {ms_dense:.3f} ms/step, speedup {ms_dense / ms_step:.2f}x")
+        # the dense baseline under the packed policy: the N materialized
+        # trajectories as one varlen microbatch, one launch pair; compared
+        # with the schedule's packed policy
+        log("dense baseline, packed: warmup + timed steps")
+        grp.prepare_dense_packed()
+        st_dp = time_steps_stats(lambda: grp.run_dense_packed(), max(3, args.steps // 2), 1)
+        grp.release_dense_packed()
+        ms_pk = st_o["mean"] if mbs is per_suffix else ms_step
+        out["dense_packed"] = {
+            "ms_per_step": round(st_dp["mean"], 4), "ms_per_step_median": round(st_dp["median"], 4),
+            "ms_per_step_min": round(st_dp["min"], 4),
+            "speedup_of_schedule_packed": round(st_dp["mean"] / ms_pk, 3),
+            "policy": "all N trajectories materialized as one packed varlen microbatch: one forward "
+                      "and one backward launch of causal attention over the N whole sequences; prefix "
+                      "gradients per copy (the N-way sum is not timed)"}
+        log(f"dense packed {st_dp['mean']:.3f} ms/step, schedule packed speedup "
+            f"{st_dp['mean'] / ms_pk:.2f}x")
 
     traffic, traffic_src = (committed_traffic(args.workload) if dominant == "bwd_bf16"
                             else (None, "n/a"))

@@ -864,10 +864,27 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, int head_dim, int n_qz, bool deter
   const long n_kv = n_kt * a.hkv * R;
   const long n_q = (long)(a.n_prefix_q_tiles + a.n_suffix_q_tiles) * a.hq * n_qz * a.n_split;
   if (n_kv + n_q == 0) return hipSuccess;
-  // Phase C / dense prefix: the causal key tiles near the start of the prefix
-  // carry the most rows.  Phase B suffix: every query tile sweeps the prefix,
-  // so the query-outer role goes first unless its keys are split.
-  const int kv_first = (aq || a.prefix_rows || a.n_split > 1) ? 1 : 0;
+  // Which role's blocks start first.  Phase C / dense prefix: the key-outer
+  // role, whose causal key tile 0 sweeps every prefix row.  Phase B: the
+  // query-outer role only when its blocks are much longer (by over 2.5x),
+  // so that they do not start last and end the launch on a tail; where the
+  // lengths are close, the key-outer role (the one with more blocks) leads
+  // and the query-outer blocks fill the slots its last round leaves.  The
+  // longest key-outer block sweeps the G heads of every row of the launch (a
+  // prefix key tile sees all of them; without a prefix, a suffix key tile
+  // sees its own), cut into R shares; the longest query-outer block visits
+  // all prefix key tiles and its own suffix's, cut into n_split ranges.  A
+  // query-outer step (128 rows x 64 keys, three products) costs about two
+  // key-outer steps (32 rows x 64 keys, four products).
+  int kv_first = 1;
+  if (!aq && !a.prefix_rows && n_q > 0) {
+    const long rows = a.n_prefix_k_tiles > 0 ? a.total_len : (long)a.n_suffix_k_tiles * kKvBK;
+    const long kv_len = (long)(a.hq / a.hkv) * ((rows + 31) / 32) / R;
+    const long nkt = (long)a.n_prefix_k_tiles + a.n_suffix_k_tiles;
+    const long ns = a.n_split > 1 ? a.n_split : 1;
+    const long q_len = 2 * ((nkt + ns - 1) / ns);
+    kv_first = 2 * q_len > 5 * kv_len ? 0 : 1;
+  }
   const long first = kv_first ? n_kv : n_q;
   const long n_first = aq ? n_kv : (first + 7) / 8 * 8;
   const long nb = n_first + (kv_first ? n_q : n_kv);

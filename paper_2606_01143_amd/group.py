@@ -318,6 +318,75 @@ class DeviceGroup:
             o["dq_p"], o["dk_p"], o["dv_p"], self.ws, stream)
 
     # ------------------------------------------------------------------
+    def prepare_dense_packed(self) -> None:
+        """Materialize every trajectory [P||S(i)] (Q, K, V and dO = [dO_P(i);
+        dO_S(i)]) as one packed varlen batch of N sequences, as a dense
+        trainer that packs the whole wave into one microbatch holds it.
+        Built once, outside any timed region."""
+        if getattr(self, "_dp", None) is not None:
+            return
+        if self.do_p is None:
+            raise ValueError("the dense baseline needs the group built with dense=True")
+        shp = self.shape
+        hq, hkv, d, P = shp.num_q_heads, shp.num_kv_heads, shp.head_dim, shp.prefix_len
+        seq = [P + L for L in self.lens]
+        cu = [0] + list(np.cumsum(seq))
+        T = int(cu[-1])
+
+        def cat(pre, suf):
+            return torch.cat([t for i in range(shp.n) for t in (pre(i), suf[self.cu_host[i]:self.cu_host[i + 1]])])
+
+        dims = B.make_dims(hq, hkv, d, 0, shp.dtype, self.dims.softmax_scale,
+                           bool(self.dims.flags & B.SPR_DETERMINISTIC), bool(self.dims.flags & B.SPR_ATOMIC_DQ))
+        B.check_cu_seqlens(cu, shp.n, max(seq), T)
+        e = lambda h, dt=None: torch.empty(T, h, d, device=self.device, dtype=dt or self.dtype)
+        none_kv = torch.empty(0, hkv, d, device=self.device, dtype=self.dtype)
+        none_c = torch.empty(0, hkv, d, device=self.device, dtype=torch.float32)
+        dp = {"dims": dims, "cu_host": cu, "max_len": max(seq), "T": T,
+              "cu": torch.tensor(cu, dtype=torch.int32, device=self.device),
+              "q": cat(lambda i: self.q_p, self.q_s), "k": cat(lambda i: self.k_p, self.k_s),
+              "v": cat(lambda i: self.v_p, self.v_s), "do": cat(lambda i: self.do_p[i], self.do_s),
+              "o": e(hq), "lse": torch.empty(T, hq, device=self.device, dtype=torch.float32),
+              "dq": e(hq), "dk": e(hkv), "dv": e(hkv), "none_kv": none_kv, "none_c": none_c}
+        need = max(B.workspace_size(B.OP_SUFFIX_FWD, dims, shp.n, dp["max_len"], T),
+                   B.workspace_size(B.OP_SUFFIX_BWD, dims, shp.n, dp["max_len"], T), 256)
+        dp["ws"] = torch.empty(need, device=self.device, dtype=torch.uint8)
+        self._dp = dp
+
+    def release_dense_packed(self) -> None:
+        self._dp = None
+
+    def run_dense_packed(self, stream=None) -> None:
+        """The dense baseline under the packed batching policy: the N
+        materialized trajectories as one varlen microbatch, one forward and
+        one backward launch pair of causal attention over each whole
+        sequence (the library's suffix calls with no shared prefix).  The
+        prefix gradients stay per copy, as a dense trainer has them;
+        ``fetch_dense_packed`` sums them for comparison."""
+        self.prepare_dense_packed()
+        t = self._dp
+        dims, n, mx, T = t["dims"], self.shape.n, t["max_len"], t["T"]
+        B.suffix_attn_fwd(dims, t["none_kv"], t["none_kv"], t["q"], t["k"], t["v"], t["cu"], n, mx, T,
+                          t["o"], t["lse"], t["ws"], stream)
+        B.suffix_attn_bwd_accum(dims, t["none_kv"], t["none_kv"], t["q"], t["k"], t["v"], t["o"], t["lse"],
+                                t["do"], t["cu"], n, mx, T, t["dq"], t["dk"], t["dv"], t["none_c"],
+                                t["none_c"], t["ws"], stream)
+
+    def fetch_dense_packed(self) -> Dict[str, np.ndarray]:
+        """The packed dense outputs in the layout of ``fetch``: the first
+        copy's prefix outputs, the prefix gradients summed over the copies
+        (in float64), the suffix rows as packed suffixes."""
+        t, P = self._dp, self.shape.prefix_len
+        f64 = lambda x: x.float().cpu().numpy().astype(np.float64)
+        cu = t["cu_host"]
+        res = {"o_p": f64(t["o"][:P]), "lse_p": f64(t["lse"][:P])}
+        for k in ("dq", "dk", "dv"):
+            res[k + "_p"] = sum(f64(t[k][cu[i]:cu[i] + P]) for i in range(self.shape.n))
+        for k in ("o", "lse", "dq", "dk", "dv"):
+            res[k + "_s"] = np.concatenate([f64(t[k][cu[i] + P:cu[i + 1]]) for i in range(self.shape.n)])
+        return res
+
+    # ------------------------------------------------------------------
     def fetch(self, which: str = "schedule") -> Dict[str, np.ndarray]:
         """Outputs as float64 numpy arrays (LSE as [T, Hq])."""
         src = self.out if which == "schedule" else self.dense_out

@@ -117,6 +117,32 @@ def test_dense_baseline_matches_oracle(gpu, name, shape):
     _assert_close(got, ref, DENSE_KEYS, TOL[shape.dtype], f"dense {name}")
 
 
+PACKED_DENSE_SHAPES = [s for s in SHAPES if s[0] in
+                       ("f32_gqa_d128_ragged", "bf16_gqa4_d128_ragged", "bf16_d64", "bf16_split_ragged",
+                        "bf16_qsplit_ragged", "bf16_n1")]
+
+
+@pytest.mark.parametrize("name,shape", PACKED_DENSE_SHAPES, ids=[s[0] for s in PACKED_DENSE_SHAPES])
+def test_packed_dense_baseline_matches_oracle(gpu, name, shape):
+    """The dense baseline under the packed batching policy (every
+    trajectory materialized, one varlen launch pair over the N whole
+    sequences): its outputs and its prefix gradients summed over the copies
+    against the dense definition; every copy's prefix rows bitwise alike."""
+    import torch
+    _announce(f"packed dense {name} {shape}")
+    inp, grp = _group(shape, seed=1)
+    grp.run_dense_packed()
+    torch.cuda.synchronize()
+    got = grp.fetch_dense_packed()
+    ref = dense_group_reference(inp)
+    _assert_close(got, ref, DENSE_KEYS, TOL[shape.dtype], f"packed dense {name}")
+    t, P = grp._dp, shape.prefix_len
+    for i in range(1, shape.n):
+        c0, ci = t["cu_host"][0], t["cu_host"][i]
+        assert torch.equal(t["o"][c0:c0 + P], t["o"][ci:ci + P]), i
+        assert torch.equal(t["lse"][c0:c0 + P], t["lse"][ci:ci + P]), i
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_suffix_only_loss_exact_cache_injection(gpu, dtype):
     """G_Y = NULL: dQ_P = 0 exactly and dK_P/dV_P are the cache rounded once."""

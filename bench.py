@@ -19,7 +19,9 @@ head that the schedule computes (4d forward + 10d backward), divided by the
 mean step time; the median and minimum of the per-step times are reported
 beside it.  The dense baseline's extra work is never counted.  The other
 batching policy (all suffixes packed into one microbatch) is timed on the
-same inputs and reported beside the headline's.
+same inputs and reported beside the headline's, against the dense baseline
+under the same policy (the N materialized trajectories as one varlen launch
+pair).
 
 Also reported: per-phase times of one step, the standalone gK/gV cache
 accumulate (G += g, HBM-bound) against 8 TB/s, and the 12d (no S recompute)
@@ -559,6 +561,14 @@ def sweep_one(name: str, args):
     ms = time_steps(lambda: grp.run_schedule(mbs), steps, max(1, args.warmup))
     phases = phase_times(grp, mbs)
     ms_dense = time_steps(lambda: grp.run_dense(), max(1, steps // 2), 1)
+    # the packed policy on both sides: all suffixes in one microbatch, and
+    # the N materialized trajectories as one varlen launch pair
+    packed = [(0, shape.n)]
+    grp.prepare(packed)
+    ms_pk = time_steps(lambda: grp.run_schedule(packed), steps, 1)
+    grp.prepare_dense_packed()
+    ms_dense_pk = time_steps(lambda: grp.run_dense_packed(), max(1, steps // 2), 1)
+    grp.release_dense_packed()
     value = sched_flops / (ms * 1e-3) / 1e12
     rec = {"workload": name, "num_q_heads": hq, "num_kv_heads": shape.num_kv_heads, "head_dim": d,
            "prefix_len": shape.prefix_len, "n_suffixes": shape.n,
@@ -567,6 +577,8 @@ def sweep_one(name: str, args):
            "pct_mfma_peak": round(100 * value / BF16_PEAK_TFLOPS, 2),
            "dense_ms_per_step": round(ms_dense, 4), "speedup_vs_dense": round(ms_dense / ms, 3),
            "flop_ratio_dense_over_schedule": round(dense_flops / sched_flops, 3),
+           "packed": {"ms_per_step": round(ms_pk, 4), "dense_ms_per_step": round(ms_dense_pk, 4),
+                      "speedup_vs_dense": round(ms_dense_pk / ms_pk, 3)},
            "phases_ms": phases, "steps": steps, "dtype": "bf16", "data": "synthetic"}
     print(json.dumps(rec), flush=True)
     del grp

@@ -42,6 +42,7 @@ namespace spr {
 
 namespace {
 constexpr int kKvBK = 64;   // keys per key-outer workgroup (two 32-key wave pairs)
+constexpr int kKvWidePairs = 6;  // wave pairs of the key-outer-only workgroup
 constexpr int kQBQ = 128;   // rows per bwd_q workgroup (32 per wave)
 }  // namespace
 
@@ -73,17 +74,17 @@ constexpr int kKvBufs = 3;
 
 typedef __attribute__((address_space(1))) float gfloat;  // global memory
 
-template <int D, bool AQ>
+template <int D, bool AQ, int NP = 2>
 struct KvLds {
   static constexpr int TE = kKvBQ * D;  // bf16 elements of one 32-row tile
   bf16 q[kKvBufs][TE];
   bf16 o[kKvBufs][TE];
   float l[kKvBufs][64];  // log2-domain LSE of the tile's rows (32 used)
   float e[kKvBufs][64];  // rowsum(dO * O) of the tile's rows (32 used)
-  bf16x8 p[2][2][2][64];  // P exchange (bf16) [tile parity][key block][k-step v][lane]
+  bf16x8 p[2][NP][2][64];  // P exchange (bf16) [tile parity][key block][k-step v][lane]
 };
 template <int D>
-struct KvLds<D, true> : KvLds<D, false> {
+struct KvLds<D, true, 2> : KvLds<D, false, 2> {
   // dS^T of a tile for the dQ product: 64 keys x 32 rows bf16, [tile parity]
   bf16 ds[2][64 * kKvBQ];
 };
@@ -96,11 +97,16 @@ __device__ __forceinline__ int dst_off(int key, int col) {
   return key * kKvBQ + ((((col >> 3) ^ ((key >> 2) & 3))) << 3) + (col & 7);
 }
 
-template <int D, bool AQ>
-__device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, KvLds<D, AQ>& L) {
+// NP wave pairs (32 keys each) per workgroup: 2 in the launch shared with
+// the query-outer role, kKvWidePairs in the key-outer-only launch of long
+// prefixes.
+template <int D, bool AQ, int NP = 2>
+__device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, KvLds<D, AQ, NP>& L) {
+  static_assert(NP == 2 || !AQ, "the atomic-dQ variant runs two pairs");
   constexpr int NS = D / 16;
   constexpr int NDB = D / 32;
   constexpr int BQ = kKvBQ;
+  constexpr int KB = 32 * NP;  // keys per workgroup
 
   const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
   const int r = lane & 31, h = lane >> 5;
@@ -111,7 +117,7 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
   const int hk = bid % a.hkv, rs = (bid / a.hkv) % R, x = bid / a.hkv / R;
   const int G = a.hq / a.hkv;
 
-  // ---- which 64 keys: a prefix tile, or a tile of suffix s.  Launches
+  // ---- which KB keys: a prefix tile, or a tile of suffix s.  Launches
   // without prefix rows take the suffix key tiles first: the causal tiles at
   // the start of a suffix carry about as many rows as a prefix tile, and the
   // shorter ones should not start last.
@@ -121,13 +127,13 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
   int k0, kseg, kbase;
   if (sfx_first ? x >= n_sfx : x < a.n_prefix_k_tiles) {
     kpre = true;
-    k0 = (sfx_first ? x - n_sfx : x) * kKvBK;
+    k0 = (sfx_first ? x - n_sfx : x) * KB;
     kseg = a.P;
     kbase = 0;
   } else {
     const int y = sfx_first ? x : x - a.n_prefix_k_tiles;
     const int s = a.seq_base + y / a.n_suffix_k_tiles;
-    k0 = (y % a.n_suffix_k_tiles) * kKvBK;
+    k0 = (y % a.n_suffix_k_tiles) * KB;
     const SegRows sg = suffix_rows(a.cu, s, a.total_len);
     kbase = sg.base;
     kseg = sg.len;
@@ -155,7 +161,7 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
   // the block's last key tile of its segment may be partial: keys past the
   // end recompute the last key and their P must be zero wherever dQ sums
   // over keys
-  const bool kpartial = k0 + kKvBK > kseg;
+  const bool kpartial = k0 + KB > kseg;
   const bool key_ok = wave_k0 + r < kseg;
   // atomic dQ: wave w < NDB owns dQ columns 32 w .. 32 w + 31 of every row
   // tile; its B operands K[16 v + k][32 w + r] for the 4 k-steps over the
@@ -233,20 +239,22 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
     return rt;
   };
 
-  // tile t's loads, split over the four waves
+  // tile t's loads, split over waves 0-3
   const bf16 *q_p = in_sgpr((const bf16*)a.q_p), *q_s = in_sgpr((const bf16*)a.q_s);
   const bf16 *do_p = in_sgpr((const bf16*)a.do_p), *do_s = in_sgpr((const bf16*)a.do_s);
   const float *l_p = in_sgpr((const float*)a.lse2_p), *l_s = in_sgpr((const float*)a.lse2_s);
   const float *e_p = in_sgpr((const float*)a.dd_p), *e_s = in_sgpr((const float*)a.dd_s);
   TileLoader<D, 4, BQ> tl;
-  tl.init(a.hq, w, lane);
+  tl.init(a.hq, w & 3, lane);
   RowVecLoader rl;
   rl.init(a.hq, lane);
   auto issue = [&](const Cursor& cur) {
     const RowTile rt = tile_info(cur);
     const int b = cur.buf;
-    tl.load(L.q[b], pick(rt.prefix, q_p, q_s), rt.row0, rt.nr, a.hq, rt.hh);
-    tl.load(L.o[b], pick(rt.prefix, do_p, do_s), rt.row0, rt.nr, a.hq, rt.hh);
+    if (NP == 2 || w < 4) {
+      tl.load(L.q[b], pick(rt.prefix, q_p, q_s), rt.row0, rt.nr, a.hq, rt.hh);
+      tl.load(L.o[b], pick(rt.prefix, do_p, do_s), rt.row0, rt.nr, a.hq, rt.hh);
+    }
     if (w == 0) rl.load(L.l[b], pick(rt.prefix, l_p, l_s) + rt.hh, rt.row0, rt.nr, a.hq);
     if (w == 1) rl.load(L.e[b], pick(rt.prefix, e_p, e_s) + rt.hh, rt.row0, rt.nr, a.hq);
   };
@@ -769,6 +777,20 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_bf16_kernel(AttnArgs a, int n
   }
 }
 
+// The key-outer role alone, kKvWidePairs wave pairs (192 keys) per
+// workgroup and one workgroup per CU: three waves on every SIMD, where the
+// shared launch holds two (the query-outer role needs more registers than a
+// third wave leaves; the key-outer role fits in 168).  Each wave's tile is a
+// chain of dependent steps (LDS reads, a product, the elementwise step, the
+// second product), so a third wave per SIMD fills more of the matrix core's
+// idle cycles; the pairs also share each Q/dO tile load.  Twelve waves keep
+// the SIMDs even (waves w, w + 4, w + 8 share one).
+template <int D>
+__global__ __launch_bounds__(kKvWidePairs * 128, 1) void bwd_kv_wide_kernel(AttnArgs a, int n_kv) {
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[sizeof(KvLds<D, false, kKvWidePairs>)];
+  if ((int)blockIdx.x < n_kv) bwd_kv_body<D, false, kKvWidePairs>(a, blockIdx.x, *(KvLds<D, false, kKvWidePairs>*)lds);
+}
+
 // dQ of every (suffix row, q head) = scale * the sum of the n_split partials
 // in split order.  One group of D / 4 threads per (row, head), 16-byte reads.
 template <int D>
@@ -848,6 +870,48 @@ __global__ __launch_bounds__(256) void bwd_kv_combine_kernel(AttnArgs a, int n_p
   }
 }
 
+namespace {
+// the row shares' partial dK/dV summed in share order, with the epilogue
+hipError_t launch_kv_combine(const AttnArgs& a, int head_dim, hipStream_t st) {
+  const int n_pre = a.n_prefix_k_tiles > 0 ? a.P : 0;
+  const int n_sfx = a.n_seq * a.n_suffix_k_tiles > 0 ? a.total_len : 0;
+  const long kthreads = ((long)n_pre + n_sfx) * a.hkv * (head_dim / 4);
+  const unsigned kb = (unsigned)((kthreads + 255) / 256);
+  ProfileScope pk("bwd_kv_combine", st);
+  if (head_dim == 64)
+    hipLaunchKernelGGL(bwd_kv_combine_kernel<64>, dim3(kb), dim3(256), 0, st, a, n_pre, n_sfx);
+  else
+    hipLaunchKernelGGL(bwd_kv_combine_kernel<128>, dim3(kb), dim3(256), 0, st, a, n_pre, n_sfx);
+  return hipGetLastError();
+}
+}  // namespace
+
+int bwd_bf16_kv_wide_block_k() { return 32 * kKvWidePairs; }
+int bwd_bf16_kv_wide_slots() { return 256; }  // one workgroup per CU
+
+hipError_t launch_bwd_bf16_kv_wide(const AttnArgs& a, int head_dim, hipStream_t st) {
+  // key-outer blocks only, 32 * kKvWidePairs-key tiles, default (non-atomic) mode
+  if (a.dq_atomic || a.n_prefix_q_tiles || a.n_suffix_q_tiles || a.n_split > 1)
+    return hipErrorInvalidValue;
+  const int R = a.kv_rsplit > 1 ? a.kv_rsplit : 1;
+  if (R > 1 && (a.part_dk == nullptr || a.part_dv == nullptr)) return hipErrorInvalidValue;
+  const long n_kt = (long)a.n_prefix_k_tiles + (long)a.n_seq * a.n_suffix_k_tiles;
+  const long n_kv = n_kt * a.hkv * R;
+  if (n_kv == 0) return hipSuccess;
+  {
+    ProfileScope ps("bwd_bf16", st);
+    if (head_dim == 64)
+      hipLaunchKernelGGL(bwd_kv_wide_kernel<64>, dim3((unsigned)n_kv), dim3(kKvWidePairs * 128), 0, st, a,
+                         (int)n_kv);
+    else
+      hipLaunchKernelGGL(bwd_kv_wide_kernel<128>, dim3((unsigned)n_kv), dim3(kKvWidePairs * 128), 0, st, a,
+                         (int)n_kv);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return R > 1 ? launch_kv_combine(a, head_dim, st) : hipSuccess;
+}
+
 hipError_t launch_bwd_bf16(const AttnArgs& a, int head_dim, int n_qz, bool deterministic,
                            hipStream_t st) {
   if (a.n_split > 1 && (a.prefix_rows || a.part_dq == nullptr)) return hipErrorInvalidValue;
@@ -905,18 +969,7 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, int head_dim, int n_qz, bool deter
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (R > 1 && n_kt > 0) {
-    const int n_pre = a.n_prefix_k_tiles > 0 ? a.P : 0;
-    const int n_sfx = a.n_seq * a.n_suffix_k_tiles > 0 ? a.total_len : 0;
-    const long kthreads = ((long)n_pre + n_sfx) * a.hkv * (head_dim / 4);
-    const unsigned kb = (unsigned)((kthreads + 255) / 256);
-    ProfileScope pk("bwd_kv_combine", st);
-    if (head_dim == 64)
-      hipLaunchKernelGGL(bwd_kv_combine_kernel<64>, dim3(kb), dim3(256), 0, st, a, n_pre, n_sfx);
-    else
-      hipLaunchKernelGGL(bwd_kv_combine_kernel<128>, dim3(kb), dim3(256), 0, st, a, n_pre, n_sfx);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-  }
+  if (R > 1 && n_kt > 0 && (e = launch_kv_combine(a, head_dim, st)) != hipSuccess) return e;
   if (a.n_split <= 1) return hipSuccess;
   const long threads = (long)a.total_len * a.hq * (head_dim / 4);
   const unsigned cb = (unsigned)((threads + 255) / 256);
@@ -930,18 +983,20 @@ hipError_t launch_bwd_bf16(const AttnArgs& a, int head_dim, int n_qz, bool deter
 
 int bwd_bf16_block_q() { return kQBQ; }
 
-int bwd_bf16_kvsplit(long kv_tiles, long max_tiles, bool atomic_dq) {
+int bwd_bf16_kvsplit(long kv_tiles, long max_tiles, bool kv_alone, int slots) {
   // kv_tiles: the key-outer role's (32-row tile, q head) steps over all its
   // blocks; max_tiles: the longest block's.  The query-outer role adds about
   // 3/4 of that work (three products per visible block instead of four),
-  // spread over two slots per CU on 256 CUs; with atomic dQ there is no
-  // query-outer role and the dQ product lengthens every step alike.  A
+  // spread over `slots` workgroup slots (two per CU on 256 CUs, one for
+  // the key-outer-only launch); kv_alone: the launch has no
+  // query-outer role (atomic dQ, whose dQ product lengthens every step
+  // alike, or the key-outer-only launch).  A
   // block clearly longer than that average per slot (by over 10%: the
   // shares' partials and combine cost about that much) would end the launch
   // alone: then every key tile's sweep is cut into R contiguous shares,
   // about the average each, at most 8 and at least 16 steps each.
   if (kv_tiles <= 0 || max_tiles <= 0) return 1;
-  const double per_slot = (atomic_dq ? 1.0 : 1.75) * (double)kv_tiles / 512.0;
+  const double per_slot = (kv_alone ? 1.0 : 1.75) * (double)kv_tiles / (double)slots;
   if ((double)max_tiles <= 1.1 * per_slot) return 1;
   long r = (long)std::ceil((double)max_tiles / per_slot);
   r = std::min(r, max_tiles / 16);

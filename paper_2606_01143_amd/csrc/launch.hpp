@@ -55,11 +55,16 @@ int fwd_bf16_block_q();
 // suffix) blocks and a prefix of prefix_len keys
 int fwd_bf16_split(int n_row_blocks, int prefix_len);
 int bwd_bf16_block_k();
+// key-outer role alone with six wave pairs (192 keys) per workgroup, one
+// workgroup per CU, for the prefix backward of long prefixes (default mode)
+hipError_t launch_bwd_bf16_kv_wide(const AttnArgs& a, int head_dim, hipStream_t st);
+int bwd_bf16_kv_wide_block_k();
+int bwd_bf16_kv_wide_slots();
 // key splits of the bf16 suffix backward's query-outer role for
 // n_row_blocks (row tile, q head, suffix) blocks that each sweep
 // n_key_tiles key tiles
 int bwd_bf16_qsplit(int n_row_blocks, int n_key_tiles);
-int bwd_bf16_kvsplit(long kv_tiles, long max_tiles, bool atomic_dq);
+int bwd_bf16_kvsplit(long kv_tiles, long max_tiles, bool kv_alone, int slots = 512);
 int bwd_bf16_block_q();
 int f32_block_q();
 int f32_block_k();

@@ -164,9 +164,9 @@ int suffix_bwd_splits(const spr_dims* d, int32_t n_mb, int32_t max_len) {
 // 64-key tiles, from the sizes alone (so that packed and padded calls of
 // the same sizes agree): a causal key range of len keys costs
 // g * ceil((len - k0) / 32) steps for the tile at k0.
-long causal_steps(long len, long g) {
+long causal_steps(long len, long g, long bk = 64) {
   long s = 0;
-  for (long k0 = 0; k0 < len; k0 += 64) s += g * ((len - k0 + 31) / 32);
+  for (long k0 = 0; k0 < len; k0 += bk) s += g * ((len - k0 + 31) / 32);
   return s;
 }
 // dQ of the bf16 backward: by default a query-outer role recomputes S and
@@ -189,16 +189,38 @@ int suffix_bwd_kv_splits(const spr_dims* d, int32_t n_mb, int32_t max_len) {
   const long kv = pre + (long)n_mb * causal_steps(max_len, g);
   return bwd_kv_splits(d, kv, d->prefix_len > 0 ? g * ((rows + 31) / 32) : g * ((max_len + 31) / 32));
 }
+// Phase C of a long prefix (bf16, default mode) runs the key-outer role
+// alone, six wave pairs (192 keys) per workgroup at three waves per SIMD,
+// then the query-outer role in a launch of its own.  Each launch then fills
+// the GPU many times over; shorter prefixes keep the two roles in one
+// launch, where together they fill it.  The dense baseline's
+// per-trajectory backward does the same for sequences of that length.
+constexpr long kKvWideMin = 16384;
+bool prefix_kv_wide(const spr_dims* d) {
+  return d->dtype == SPR_BF16 && !atomic_dq(d) && d->prefix_len >= kKvWideMin;
+}
+bool dense_kv_wide(const spr_dims* d, int32_t max_len) {
+  return d->dtype == SPR_BF16 && !atomic_dq(d) && (long)d->prefix_len + max_len >= kKvWideMin;
+}
 // Phase C: causal prefix rows; key tile 0 sweeps all P
 int prefix_bwd_kv_splits(const spr_dims* d) {
   const long g = d->num_q_heads / d->num_kv_heads;
-  return bwd_kv_splits(d, causal_steps(d->prefix_len, g), g * ((d->prefix_len + 31) / 32));
+  const long max_steps = g * ((d->prefix_len + 31) / 32);
+  if (prefix_kv_wide(d))  // wide key tiles, one slot per CU, no query-outer role
+    return bwd_bf16_kvsplit(causal_steps(d->prefix_len, g, bwd_bf16_kv_wide_block_k()) * d->num_kv_heads,
+                            max_steps, true, bwd_bf16_kv_wide_slots());
+  return bwd_kv_splits(d, causal_steps(d->prefix_len, g), max_steps);
 }
 // the dense baseline's per-trajectory launch: prefix key tiles see the
 // causal prefix rows and the suffix rows, suffix key tiles their own rows
 int dense_bwd_kv_splits(const spr_dims* d, int32_t max_len) {
   const long g = d->num_q_heads / d->num_kv_heads, P = d->prefix_len;
   const long sr = g * ((max_len + 31) / 32);
+  if (dense_kv_wide(d, max_len)) {  // wide key tiles, one slot per CU, no query-outer role
+    const long bk = bwd_bf16_kv_wide_block_k();
+    const long kv = causal_steps(P, g, bk) + (long)tiles(d->prefix_len, (int)bk) * sr + causal_steps(max_len, g, bk);
+    return bwd_bf16_kvsplit(kv * d->num_kv_heads, g * ((P + 31) / 32) + sr, true, bwd_bf16_kv_wide_slots());
+  }
   const long kv = causal_steps(P, g) + (long)tiles(d->prefix_len, bwd_bf16_block_k()) * sr +
                   causal_steps(max_len, g);
   return bwd_kv_splits(d, kv, g * ((P + 31) / 32) + sr);
@@ -822,18 +844,35 @@ spr_status prefix_bwd_parts(const spr_dims* dims, const void* q_p, const void* k
     else
       a.n_prefix_q_tiles = tiles(dims->prefix_len, block_q(dims->dtype));
   }
+  const bool wide = prefix_kv_wide(dims);
   if (want_dkv) {
     a.pk_mode = kPkInject;
     a.gk = const_cast<float*>(gk_cache); a.gv = const_cast<float*>(gv_cache);
     a.dk_p = dk_p; a.dv_p = dv_p;
-    a.n_prefix_k_tiles = tiles(dims->prefix_len, block_k(dims->dtype));
+    a.n_prefix_k_tiles = tiles(dims->prefix_len, wide ? bwd_bf16_kv_wide_block_k() : block_k(dims->dtype));
     a.kv_rsplit = prefix_bwd_kv_splits(dims);
     if (a.kv_rsplit > 1) {
       a.part_dk = at<float>(ws, w.part_dk);
       a.part_dv = at<float>(ws, w.part_dv);
     }
   }
-  if ((st = hip_check(launch_bwd(dims, a, 1, stream), "prefix backward")) != SPR_OK) return st;
+  if (wide) {
+    // the key-outer role alone, then the query-outer role
+    if (want_dkv) {
+      AttnArgs kv = a;
+      kv.n_prefix_q_tiles = 0;
+      if ((st = hip_check(launch_bwd_bf16_kv_wide(kv, dims->head_dim, stream), "prefix backward, dK/dV")) != SPR_OK)
+        return st;
+    }
+    if (want_dq) {
+      AttnArgs q = a;
+      q.n_prefix_k_tiles = 0;
+      q.kv_rsplit = 1;
+      if ((st = hip_check(launch_bwd(dims, q, 1, stream), "prefix backward, dQ")) != SPR_OK) return st;
+    }
+  } else if ((st = hip_check(launch_bwd(dims, a, 1, stream), "prefix backward")) != SPR_OK) {
+    return st;
+  }
   if (dq_acc && (st = hip_check(launch_convert(dims->dtype, dq_acc, scale, nullptr, dq_p, P * hq * hd,
                                                stream), "dq convert")) != SPR_OK)
     return st;
@@ -954,12 +993,30 @@ spr_status spr_dense_recompute_baseline(
       a.n_prefix_q_tiles = 0;
       a.n_suffix_q_tiles = 0;
     }
+    const bool wide = dense_kv_wide(dims, max_len);
+    if (wide) {
+      a.n_prefix_k_tiles = tiles(dims->prefix_len, bwd_bf16_kv_wide_block_k());
+      a.n_suffix_k_tiles = tiles(max_len, bwd_bf16_kv_wide_block_k());
+    }
     a.kv_rsplit = dense_bwd_kv_splits(dims, max_len);
     if (a.kv_rsplit > 1) {
       a.part_dk = at<float>(ws, w.part_dk);
       a.part_dv = at<float>(ws, w.part_dv);
     }
-    SPR_TRY(launch_bwd(dims, a, 1, stream), "dense backward");
+    if (wide) {
+      // the key-outer role alone, then the query-outer role (as Phase C)
+      AttnArgs kv = a;
+      kv.n_prefix_q_tiles = 0;
+      kv.n_suffix_q_tiles = 0;
+      SPR_TRY(launch_bwd_bf16_kv_wide(kv, dims->head_dim, stream), "dense backward, dK/dV");
+      AttnArgs q = a;
+      q.n_prefix_k_tiles = 0;
+      q.n_suffix_k_tiles = 0;
+      q.kv_rsplit = 1;
+      SPR_TRY(launch_bwd(dims, q, 1, stream), "dense backward, dQ");
+    } else {
+      SPR_TRY(launch_bwd(dims, a, 1, stream), "dense backward");
+    }
   }
   SPR_TRY(launch_convert(dims->dtype, dq_acc_p, scale, nullptr, dq_p, P * hq * hd, stream), "convert");
   SPR_TRY(launch_convert(dims->dtype, dk_acc, 1.f, nullptr, dk_p, P * hkv * hd, stream), "convert");

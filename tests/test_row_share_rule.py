@@ -8,7 +8,11 @@ per CU on 256 CUs; split when the longest sweep exceeds the average per slot
 by over 10%, R = ceil(longest / average), 1 <= R <= 8, each share >= 16
 steps) and compared with the library's choice.  The atomic mode also
 reserves the fp32 dQ accumulator of the launch's rows and never splits the
-query-outer keys (it has no query-outer role)."""
+query-outer keys (it has no query-outer role).  The prefix backward of a
+prefix of 16384 keys or more runs, in the default mode, the key-outer role
+alone with 192-key tiles (six wave pairs per workgroup, one workgroup per
+CU): its steps are counted over 192-key tiles, on 256 slots, and no
+query-outer work is added."""
 import math
 
 import pytest
@@ -20,14 +24,14 @@ def _tiles(n, b):
     return 0 if n <= 0 else (n + b - 1) // b
 
 
-def _causal(length, g):
-    return sum(g * ((length - k0 + 31) // 32) for k0 in range(0, length, 64))
+def _causal(length, g, bk=64):
+    return sum(g * ((length - k0 + 31) // 32) for k0 in range(0, length, bk))
 
 
-def _rule(kv_steps, max_steps, atomic):
+def _rule(kv_steps, max_steps, atomic, slots=512):
     if kv_steps <= 0 or max_steps <= 0:
         return 1
-    per_slot = (1.0 if atomic else 1.75) * kv_steps / 512.0
+    per_slot = (1.0 if atomic else 1.75) * kv_steps / slots
     if max_steps <= 1.1 * per_slot:
         return 1
     return max(1, min(math.ceil(max_steps / per_slot), max_steps // 16, 8))
@@ -42,6 +46,8 @@ def _suffix_r(hq, hkv, P, n, ml, atomic):
 
 def _prefix_r(hq, hkv, P, atomic):
     g = hq // hkv
+    if not atomic and P >= 16384:  # the key-outer role alone, 192-key tiles
+        return _rule(_causal(P, g, 192) * hkv, g * ((P + 31) // 32), True, slots=256)
     return _rule(_causal(P, g) * hkv, g * ((P + 31) // 32), atomic)
 
 

@@ -99,10 +99,14 @@ __device__ __forceinline__ int dst_off(int key, int col) {
 
 // NP wave pairs (32 keys each) per workgroup: 2 in the launch shared with
 // the query-outer role, kKvWidePairs in the key-outer-only launch of long
-// prefixes.
-template <int D, bool AQ, int NP = 2>
+// prefixes.  PC: the launch is a Phase C (prefix key tiles, causal prefix
+// rows only), known at compile time, so the per-tile bookkeeping drops the
+// suffix-row cases; in the key-outer-only launch the twelve waves' scalar
+// instructions compete for the CU's scalar unit.
+template <int D, bool AQ, int NP = 2, bool PC = false>
 __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, KvLds<D, AQ, NP>& L) {
   static_assert(NP == 2 || !AQ, "the atomic-dQ variant runs two pairs");
+  static_assert(!PC || (NP > 2 && !AQ), "the Phase C form is the key-outer-only launch's");
   constexpr int NS = D / 16;
   constexpr int NDB = D / 32;
   constexpr int BQ = kKvBQ;
@@ -121,11 +125,11 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
   // without prefix rows take the suffix key tiles first: the causal tiles at
   // the start of a suffix carry about as many rows as a prefix tile, and the
   // shorter ones should not start last.
-  const int n_sfx = a.n_seq * a.n_suffix_k_tiles;
-  const bool sfx_first = !a.prefix_rows;
+  const int n_sfx = PC ? 0 : a.n_seq * a.n_suffix_k_tiles;
+  const bool sfx_first = !PC && !a.prefix_rows;
   bool kpre;
   int k0, kseg, kbase;
-  if (sfx_first ? x >= n_sfx : x < a.n_prefix_k_tiles) {
+  if (PC || (sfx_first ? x >= n_sfx : x < a.n_prefix_k_tiles)) {
     kpre = true;
     k0 = (sfx_first ? x - n_sfx : x) * KB;
     kseg = a.P;
@@ -141,7 +145,11 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
   }
   if (k0 >= kseg) return;
   const int kb = w >> 1;               // key block of this wave's pair
-  const bool pw = (w & 1) == 0;        // P-wave (dV) or dS-wave (dK)
+  // P-wave (dV) or dS-wave (dK).  A workgroup's waves take the CU's four
+  // SIMDs in a fixed cycle from some starting SIMD, so waves w, w + 4 and
+  // w + 8 share one.  Only the P-waves evaluate exp2: in the twelve-wave
+  // launch pairs 4 and 5 swap roles, and every SIMD holds both kinds.
+  const bool pw = ((w & 1) == 0) != (NP > 2 && w >= 8);
   const int wave_k0 = k0 + 32 * kb;
   const int my_key = min(wave_k0 + r, kseg - 1);  // keys past the end recompute the last one
 
@@ -174,7 +182,9 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
   // of suffixes seq_base .. seq_base + n_seq - 1 (all visible);
   // suffix key tile: the suffix's own rows from k0 on (causal).
   int n_pr = 0, n_sr = 0, sr0 = 0, sr1 = 0;
-  if (kpre) {
+  if (PC) {
+    n_pr = (a.P - k0 + BQ - 1) / BQ;
+  } else if (kpre) {
     if (a.prefix_rows) n_pr = (a.P - k0 + BQ - 1) / BQ;
     if (a.suffix_rows) {
       const SegRows sp = suffix_span(a.cu, a.seq_base, a.seq_base + a.n_seq, a.total_len);
@@ -217,6 +227,14 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
     RowTile rt;
     rt.hh = hk * G + c.g;
     const int j = c.j;
+    if constexpr (PC) {
+      rt.prefix = true;
+      rt.causal = true;
+      rt.lp_first = k0 + (n_pr - 1 - j) * BQ;
+      rt.row0 = rt.lp_first;
+      rt.nr = min(BQ, a.P - rt.lp_first);
+      return rt;
+    }
     if (kpre && j < n_sr) {
       rt.prefix = false;
       rt.causal = false;
@@ -249,14 +267,13 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
   RowVecLoader rl;
   rl.init(a.hq, lane);
   auto issue = [&](const Cursor& cur) {
+    if (NP > 2 && w >= 4) return;  // waves 0-3 load every tile
     const RowTile rt = tile_info(cur);
     const int b = cur.buf;
-    if (NP == 2 || w < 4) {
-      tl.load(L.q[b], pick(rt.prefix, q_p, q_s), rt.row0, rt.nr, a.hq, rt.hh);
-      tl.load(L.o[b], pick(rt.prefix, do_p, do_s), rt.row0, rt.nr, a.hq, rt.hh);
-    }
-    if (w == 0) rl.load(L.l[b], pick(rt.prefix, l_p, l_s) + rt.hh, rt.row0, rt.nr, a.hq);
-    if (w == 1) rl.load(L.e[b], pick(rt.prefix, e_p, e_s) + rt.hh, rt.row0, rt.nr, a.hq);
+    tl.load(L.q[b], PC ? q_p : pick(rt.prefix, q_p, q_s), rt.row0, rt.nr, a.hq, rt.hh);
+    tl.load(L.o[b], PC ? do_p : pick(rt.prefix, do_p, do_s), rt.row0, rt.nr, a.hq, rt.hh);
+    if (w == 0) rl.load(L.l[b], (PC ? l_p : pick(rt.prefix, l_p, l_s)) + rt.hh, rt.row0, rt.nr, a.hq);
+    if (w == 1) rl.load(L.e[b], (PC ? e_p : pick(rt.prefix, e_p, e_s)) + rt.hh, rt.row0, rt.nr, a.hq);
   };
 
   // A tile whose rows all precede this pair's keys (causal) contributes
@@ -785,10 +802,11 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_bf16_kernel(AttnArgs a, int n
 // second product), so a third wave per SIMD fills more of the matrix core's
 // idle cycles; the pairs also share each Q/dO tile load.  Twelve waves keep
 // the SIMDs even (waves w, w + 4, w + 8 share one).
-template <int D>
+template <int D, bool PC>
 __global__ __launch_bounds__(kKvWidePairs * 128, 1) void bwd_kv_wide_kernel(AttnArgs a, int n_kv) {
   __shared__ __attribute__((aligned(1024))) unsigned char lds[sizeof(KvLds<D, false, kKvWidePairs>)];
-  if ((int)blockIdx.x < n_kv) bwd_kv_body<D, false, kKvWidePairs>(a, blockIdx.x, *(KvLds<D, false, kKvWidePairs>*)lds);
+  if ((int)blockIdx.x < n_kv)
+    bwd_kv_body<D, false, kKvWidePairs, PC>(a, blockIdx.x, *(KvLds<D, false, kKvWidePairs>*)lds);
 }
 
 // dQ of every (suffix row, q head) = scale * the sum of the n_split partials
@@ -900,12 +918,19 @@ hipError_t launch_bwd_bf16_kv_wide(const AttnArgs& a, int head_dim, hipStream_t 
   if (n_kv == 0) return hipSuccess;
   {
     ProfileScope ps("bwd_bf16", st);
-    if (head_dim == 64)
-      hipLaunchKernelGGL(bwd_kv_wide_kernel<64>, dim3((unsigned)n_kv), dim3(kKvWidePairs * 128), 0, st, a,
-                         (int)n_kv);
-    else
-      hipLaunchKernelGGL(bwd_kv_wide_kernel<128>, dim3((unsigned)n_kv), dim3(kKvWidePairs * 128), 0, st, a,
-                         (int)n_kv);
+    // Phase C: prefix key tiles and causal prefix rows only
+    const bool pc = a.prefix_rows && !a.suffix_rows && a.n_seq * a.n_suffix_k_tiles == 0;
+    const dim3 grid((unsigned)n_kv), block(kKvWidePairs * 128);
+    if (head_dim == 64) {
+      if (pc)
+        hipLaunchKernelGGL((bwd_kv_wide_kernel<64, true>), grid, block, 0, st, a, (int)n_kv);
+      else
+        hipLaunchKernelGGL((bwd_kv_wide_kernel<64, false>), grid, block, 0, st, a, (int)n_kv);
+    } else if (pc) {
+      hipLaunchKernelGGL((bwd_kv_wide_kernel<128, true>), grid, block, 0, st, a, (int)n_kv);
+    } else {
+      hipLaunchKernelGGL((bwd_kv_wide_kernel<128, false>), grid, block, 0, st, a, (int)n_kv);
+    }
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

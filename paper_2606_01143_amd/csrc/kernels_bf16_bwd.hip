@@ -27,9 +27,9 @@
 //     dQ^T += K^T dS^T             A = K tile read transposed, B = dS^T registers
 //   and writes dQ once, already scaled and rounded.
 // Both stream their tiles through LDS (the key-outer role's 32-row Q/dO
-// tiles triple-buffered, the query-outer role's 64-key K/V tiles
-// double-buffered), filled by direct-to-LDS loads issued one tile ahead of
-// the products.  The loads are invisible to the compiler's wait tracking:
+// tiles triple-buffered, four buffers in its key-outer-only launch; the
+// query-outer role's 64-key K/V tiles double-buffered), filled by
+// direct-to-LDS loads issued one tile ahead of the products.  The loads are invisible to the compiler's wait tracking:
 // every tile is read only after tile_barrier (vmcnt(0) + workgroup barrier).
 #include <algorithm>
 #include <cmath>
@@ -73,14 +73,21 @@ constexpr int kKvBufs = 3;
 }  // namespace
 
 typedef __attribute__((address_space(1))) float gfloat;  // global memory
+template <bool B>
+struct StepOrder {
+  static constexpr bool value = B;
+};
 
+// In the key-outer-only launch a deferring dS-wave (below) still reads tile
+// t - 2 while tile t + 1 loads: a fourth buffer.
 template <int D, bool AQ, int NP = 2>
 struct KvLds {
   static constexpr int TE = kKvBQ * D;  // bf16 elements of one 32-row tile
-  bf16 q[kKvBufs][TE];
-  bf16 o[kKvBufs][TE];
-  float l[kKvBufs][64];  // log2-domain LSE of the tile's rows (32 used)
-  float e[kKvBufs][64];  // rowsum(dO * O) of the tile's rows (32 used)
+  static constexpr int NB = NP > 2 ? 4 : kKvBufs;
+  bf16 q[NB][TE];
+  bf16 o[NB][TE];
+  float l[NB][64];  // log2-domain LSE of the tile's rows (32 used)
+  float e[NB][64];  // rowsum(dO * O) of the tile's rows (32 used)
   bf16x8 p[2][NP][2][64];  // P exchange (bf16) [tile parity][key block][k-step v][lane]
 };
 template <int D>
@@ -107,6 +114,7 @@ template <int D, bool AQ, int NP = 2, bool PC = false>
 __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, KvLds<D, AQ, NP>& L) {
   static_assert(NP == 2 || !AQ, "the atomic-dQ variant runs two pairs");
   static_assert(!PC || (NP > 2 && !AQ), "the Phase C form is the key-outer-only launch's");
+  constexpr int NB = KvLds<D, AQ, NP>::NB;
   constexpr int NS = D / 16;
   constexpr int NDB = D / 32;
   constexpr int BQ = kKvBQ;
@@ -150,6 +158,14 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
   // w + 8 share one.  Only the P-waves evaluate exp2: in the twelve-wave
   // launch pairs 4 and 5 swap roles, and every SIMD holds both kinds.
   const bool pw = ((w & 1) == 0) != (NP > 2 && w >= 8);
+  // Every wave leaves the tile barrier at the same time, so waves taking the
+  // same steps in the same order all want the matrix cores at once, then
+  // all the vector ALU.  In the key-outer-only launch each SIMD holds two
+  // waves of one role and one of the other; that one (waves 8-11) defers
+  // each tile's accumulation to the next barrier interval and runs it first
+  // there, so its matrix work overlaps the other two waves' elementwise
+  // steps.
+  const bool defer = NP > 2 && (w >> 2) == 2;
   const int wave_k0 = k0 + 32 * kb;
   const int my_key = min(wave_k0 + r, kseg - 1);  // keys past the end recompute the last one
 
@@ -221,7 +237,7 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
       c.g = 0;
       ++c.j;
     }
-    c.buf = c.buf == kKvBufs - 1 ? 0 : c.buf + 1;
+    c.buf = c.buf == NB - 1 ? 0 : c.buf + 1;
   };
   auto tile_info = [&](const Cursor& c) {
     RowTile rt;
@@ -300,8 +316,11 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
     __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
     return c;
   };
-  // acc += (dO or Q)^T (P or dS), operands pb[v] (C-order rows)
+  // acc += (dO or Q)^T (P or dS), operands pb[v] (C-order rows).  In the
+  // key-outer-only launch a wave raises its issue priority for these eight
+  // products, so the SIMD's arbiter feeds the matrix core from it first.
   auto accumulate = [&](const bf16* T, const bf16x8 (&pb)[2]) {
+    if constexpr (NP > 2) __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int v = 0; v < 2; ++v) {
       bf16x8 at[NDB];
@@ -317,16 +336,21 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
       }
       __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
     }
+    if constexpr (NP > 2) __builtin_amdgcn_s_setprio(0);
   };
 
-  // this wave's work on tile tc: one product, the role's elementwise step,
-  // one accumulation
-  auto compute = [&](int tc, const RowTile& rt, const int b) {
+  // this wave's work on tile tc: one product and the role's elementwise
+  // step (front), giving the bf16 operands of one accumulation (back)
+  struct Ops {
+    bf16x8 v[2];
+  };
+  auto front = [&](int tc, const RowTile& rt, const int b) {
     const bf16* Qc = L.q[b];
     const bf16* Oc = L.o[b];
     bf16x8* px = &L.p[tc & 1][kb][0][lane];  // k-step v at px[64 v]
     f32x16 c = product(pw ? Qc : Oc);
-    bf16x8 ops[2];
+    Ops res;
+    bf16x8(&ops)[2] = res.v;
     if (pw) {
       const float* Lc = L.l[b];
 #pragma unroll
@@ -380,8 +404,9 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
         }
       }
     }
-    accumulate(pw ? Oc : Qc, ops);
+    return res;
   };
+  auto back = [&](const int b, const Ops& o) { accumulate(pw ? L.o[b] : L.q[b], o.v); };
 
   // dQ of tile tq (atomic variant): dQ[row][32 w + r] += sum over the
   // block's 64 keys of dS[row][key] K[key][32 w + r], A = dS^T read
@@ -471,28 +496,60 @@ __device__ __forceinline__ void bwd_kv_body(const AttnArgs& a, const int bid, Kv
     __syncthreads();  // every wave holds its operands before buffer 1 reloads
   }
   const int t_end = dq_on ? ntiles + 1 : ntiles;
-  for (int t = 0; t <= t_end; ++t) {
-    if (t + 1 < ntiles) {
-      issue(cl);
-      advance(cl);
-    }
-    compiler_fence();
-    const int tc = pw ? t : t - 1;
-    if (tc >= 0 && tc < ntiles) {
-      const RowTile rt = tile_info(cc);
-      if (!hidden(rt)) compute(tc, rt, cc.buf);
-      advance(cc);
-    }
-    if (dq_on) {
-      // the dS-waves published tile t - 2 one barrier ago
-      const int tq = t - 2;
-      if (tq >= 0 && tq < ntiles) {
-        dq_step(tq, tile_info(cq));
-        advance(cq);
+  // The tile loop, in one of two step orders fixed at compile time (the
+  // deferring order carries one tile's operands across the barrier; compiled
+  // as one loop with a runtime order, those registers would stay live through
+  // every wave's products).
+  auto sweep = [&](auto order) {
+    constexpr bool DEFER = decltype(order)::value;
+    // a deferring wave's accumulation still to do: tile buffer and operands
+    bool pend = false;
+    int pend_buf = 0;
+    Ops pend_ops;
+    for (int t = 0; t <= t_end; ++t) {
+      if (t + 1 < ntiles) {
+        issue(cl);
+        advance(cl);
       }
+      compiler_fence();
+      const int tc = pw ? t : t - 1;
+      if constexpr (DEFER) {
+        if (pend) back(pend_buf, pend_ops);
+        pend = false;
+      }
+      if (tc >= 0 && tc < ntiles) {
+        const RowTile rt = tile_info(cc);
+        if (!hidden(rt)) {
+          const Ops o = front(tc, rt, cc.buf);
+          if constexpr (DEFER) {
+            pend_ops = o;
+            pend_buf = cc.buf;
+            pend = true;
+          } else {
+            back(cc.buf, o);
+          }
+        }
+        advance(cc);
+      }
+      if (dq_on) {
+        // the dS-waves published tile t - 2 one barrier ago
+        const int tq = t - 2;
+        if (tq >= 0 && tq < ntiles) {
+          dq_step(tq, tile_info(cq));
+          advance(cq);
+        }
+      }
+      tile_barrier();
     }
-    tile_barrier();
-  }
+    // a dS-wave's last tile (its buffer is no longer reloaded)
+    if constexpr (DEFER) {
+      if (pend) back(pend_buf, pend_ops);
+    }
+  };
+  if (NP > 2 && defer)
+    sweep(StepOrder<true>{});
+  else
+    sweep(StepOrder<false>{});
 
   // ---- epilogue: acc[db][i] is dV^T or dK^T at d = 32 db + c_row0(i) + 4 h,
   // key wave_k0 + r

@@ -27,6 +27,10 @@ namespace spr {
 
 namespace {
 constexpr int kFwdBQ = 128;
+// headroom (log2 domain) of the softmax reference over a row's true running
+// max: P = exp2(s - m) stays below 256, far inside fp32, and bf16 rounds it
+// to the same relative precision as below 1
+constexpr float kFwdSlack = 8.f;
 }  // namespace
 
 int fwd_bf16_block_q() { return kFwdBQ; }
@@ -153,15 +157,19 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(AttnArgs a) {
 #pragma unroll
     for (int e = 0; e < 32; ++e) mt = fmaxf(mt, SC(e));
     mt = fmaxf(mt, __shfl_xor(mt, 32)) * a.scale_log2;
-    const float mn = fmaxf(m, mt);
-    const float mu = mn == -INFINITY ? 0.f : mn;
-    if (__builtin_expect(__any(mn > m), 0)) {  // rescale only when some row's max grew
-      const float corr = fast_exp2(m - mu);
+    // m is the reference the exponents are taken against, not necessarily
+    // the running max: it moves (and O, l are rescaled) only when some row's
+    // max exceeds it by more than kFwdSlack, so P = exp2(s - m) < 2^kFwdSlack.
+    // O / l and m + log2(l) do not depend on the reference.
+    if (__builtin_expect(__any(mt > m + kFwdSlack), 0)) {
+      const float mn = fmaxf(m, mt);
+      const float corr = fast_exp2(m - (mn == -INFINITY ? 0.f : mn));
       l *= corr;
 #pragma unroll
       for (int db = 0; db < NDB; ++db) o[db] *= corr;
+      m = mn;
     }
-    m = mn;
+    const float mu = m == -INFINITY ? 0.f : m;
     float rs = 0.f;
 #pragma unroll
     for (int e = 0; e < 32; ++e) {

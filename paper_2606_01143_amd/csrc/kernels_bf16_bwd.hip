@@ -764,11 +764,17 @@ __device__ __forceinline__ void bwd_q_body(const AttnArgs& a, const int bid, bf1
 
   if (t_begin < t_end) issue(t_begin, Ks[0], Vs[0]);
   tile_barrier();
-  for (int t = t_begin; t < t_end; ++t) {
-    const int cur = (t - t_begin) & 1;
-    if (t + 1 < t_end) issue(t + 1, Ks[cur ^ 1], Vs[cur ^ 1]);
+  // two tiles per pass, so each buffer's LDS address is a constant and goes
+  // into the reads' immediate offsets instead of a per-read address add
+  for (int t = t_begin; t < t_end; t += 2) {
+    if (t + 1 < t_end) issue(t + 1, Ks[1], Vs[1]);
     compiler_fence();
-    compute(t, Ks[cur], Vs[cur]);
+    compute(t, Ks[0], Vs[0]);
+    tile_barrier();
+    if (t + 1 >= t_end) break;
+    if (t + 2 < t_end) issue(t + 2, Ks[0], Vs[0]);
+    compiler_fence();
+    compute(t + 1, Ks[1], Vs[1]);
     tile_barrier();
   }
 

@@ -181,26 +181,38 @@ int bwd_kv_splits(const spr_dims* d, long kv_steps, long max_steps) {
   if (d->dtype != SPR_BF16) return 1;
   return bwd_bf16_kvsplit(kv_steps * d->num_kv_heads, max_steps, atomic_dq(d));
 }
-// Phase B: prefix key tiles see every suffix row (at most n_mb * max_len),
-// suffix key tiles their own causal rows
-int suffix_bwd_kv_splits(const spr_dims* d, int32_t n_mb, int32_t max_len) {
-  const long g = d->num_q_heads / d->num_kv_heads, rows = (long)n_mb * max_len;
-  const long pre = (long)tiles(d->prefix_len, bwd_bf16_block_k()) * g * ((rows + 31) / 32);
-  const long kv = pre + (long)n_mb * causal_steps(max_len, g);
-  return bwd_kv_splits(d, kv, d->prefix_len > 0 ? g * ((rows + 31) / 32) : g * ((max_len + 31) / 32));
-}
 // Phase C of a long prefix (bf16, default mode) runs the key-outer role
 // alone, six wave pairs (192 keys) per workgroup at three waves per SIMD,
 // then the query-outer role in a launch of its own.  Each launch then fills
 // the GPU many times over; shorter prefixes keep the two roles in one
 // launch, where together they fill it.  The dense baseline's
-// per-trajectory backward does the same for sequences of that length.
+// per-trajectory backward does the same for sequences of that length, and
+// the suffix backward for suffixes of that length (the packed dense
+// baseline's whole trajectories among them).
 constexpr long kKvWideMin = 16384;
 bool prefix_kv_wide(const spr_dims* d) {
   return d->dtype == SPR_BF16 && !atomic_dq(d) && d->prefix_len >= kKvWideMin;
 }
 bool dense_kv_wide(const spr_dims* d, int32_t max_len) {
   return d->dtype == SPR_BF16 && !atomic_dq(d) && (long)d->prefix_len + max_len >= kKvWideMin;
+}
+bool suffix_kv_wide(const spr_dims* d, int32_t max_len) {
+  return d->dtype == SPR_BF16 && !atomic_dq(d) && max_len >= kKvWideMin;
+}
+// Phase B: prefix key tiles see every suffix row (at most n_mb * max_len),
+// suffix key tiles their own causal rows
+int suffix_bwd_kv_splits(const spr_dims* d, int32_t n_mb, int32_t max_len) {
+  const long g = d->num_q_heads / d->num_kv_heads, rows = (long)n_mb * max_len;
+  const long max_steps = d->prefix_len > 0 ? g * ((rows + 31) / 32) : g * ((max_len + 31) / 32);
+  if (suffix_kv_wide(d, max_len)) {  // wide key tiles, one slot per CU, no query-outer role
+    const long bk = bwd_bf16_kv_wide_block_k();
+    const long kv = (long)tiles(d->prefix_len, (int)bk) * g * ((rows + 31) / 32) +
+                    (long)n_mb * causal_steps(max_len, g, bk);
+    return bwd_bf16_kvsplit(kv * d->num_kv_heads, max_steps, true, bwd_bf16_kv_wide_slots());
+  }
+  const long pre = (long)tiles(d->prefix_len, bwd_bf16_block_k()) * g * ((rows + 31) / 32);
+  const long kv = pre + (long)n_mb * causal_steps(max_len, g);
+  return bwd_kv_splits(d, kv, max_steps);
 }
 // Phase C: causal prefix rows; key tile 0 sweeps all P
 int prefix_bwd_kv_splits(const spr_dims* d) {
@@ -663,7 +675,26 @@ spr_status spr_suffix_attn_bwd_accum(const spr_dims* dims, const void* k_p, cons
     a.part_dk = at<float>(ws, w.part_dk);
     a.part_dv = at<float>(ws, w.part_dv);
   }
-  if ((st = hip_check(launch_bwd(dims, a, n_mb, stream), "suffix backward")) != SPR_OK) return st;
+  if (suffix_kv_wide(dims, max_len)) {
+    // the key-outer role alone on 192-key tiles, then the query-outer role
+    // (as Phase C of a long prefix)
+    AttnArgs kv = a;
+    kv.n_prefix_k_tiles = tiles(dims->prefix_len, bwd_bf16_kv_wide_block_k());
+    kv.n_suffix_k_tiles = tiles(max_len, bwd_bf16_kv_wide_block_k());
+    kv.n_suffix_q_tiles = 0;
+    kv.n_split = 1;
+    kv.part_dq = nullptr;
+    if ((st = hip_check(launch_bwd_bf16_kv_wide(kv, dims->head_dim, stream), "suffix backward, dK/dV")) != SPR_OK)
+      return st;
+    AttnArgs q = a;
+    q.n_prefix_k_tiles = 0;
+    q.n_suffix_k_tiles = 0;
+    q.kv_rsplit = 1;
+    q.part_dk = q.part_dv = nullptr;
+    if ((st = hip_check(launch_bwd(dims, q, n_mb, stream), "suffix backward, dQ")) != SPR_OK) return st;
+  } else if ((st = hip_check(launch_bwd(dims, a, n_mb, stream), "suffix backward")) != SPR_OK) {
+    return st;
+  }
   if (dq_acc && (st = hip_check(launch_convert(dims->dtype, dq_acc, a.scale, nullptr, dq_s,
                                                T * hq * hd, stream), "dq convert")) != SPR_OK)
     return st;

@@ -2,7 +2,9 @@
 a prefix of 16384 keys or more runs the key-outer role alone, six wave
 pairs (192 keys) per workgroup, then the query-outer role in a launch of its
 own; the dense baseline's per-trajectory backward of sequences that long
-does the same.  Checked at full length on one or two kv heads against the
+does the same, and so does the suffix backward of suffixes that long (the
+packed dense baseline's whole trajectories, or a long suffix behind a short
+prefix in Phase B).  Checked at full length on one or two kv heads against the
 oracle's sampled rows and keys (each from its own sequence; both sampled
 references are pinned to the whole oracle on small groups) and the
 identities that hold at any size, with row shares (3 to 6), head_dim 64,
@@ -111,3 +113,57 @@ def test_long_sequence_dense_baseline_matches_oracle(gpu, name, shape):
         B.profile_enable(False)
     assert n_bwd == 2 * shape.n, n_bwd
     _assert_sampled(inp, grp.fetch("dense"), f"dense {name}", cache=False)
+
+
+@pytest.mark.parametrize("name,shape", CASES[:2], ids=[c[0] for c in CASES[:2]])
+def test_long_sequences_packed_dense_baseline_matches_oracle(gpu, name, shape):
+    """The packed dense baseline's whole trajectories (one varlen microbatch,
+    no shared prefix) are this long: the suffix backward takes the same two
+    launches; its outputs against the sampled oracle."""
+    import torch
+    from paper_2606_01143_amd import binding as B
+    from paper_2606_01143_amd.group import DeviceGroup
+    _announce(f"long-sequence packed dense {name} {shape}")
+    inp = make_group(shape, seed=37)
+    grp = DeviceGroup(inp, dense=True)
+    grp.prepare_dense_packed()
+    B.profile_reset()
+    B.profile_enable(True)
+    try:
+        grp.run_dense_packed()
+        torch.cuda.synchronize()
+        _, n_bwd = B.profile_query("bwd_bf16")
+    finally:
+        B.profile_enable(False)
+    assert n_bwd == 2, n_bwd
+    _assert_sampled(inp, grp.fetch_dense_packed(), f"packed dense {name}", cache=False)
+
+
+LONG_SUFFIX = [
+    # a suffix of 16400 = 85 * 192 + 80 tokens behind a prefix of 512, and a
+    # short one: Phase B takes the two launches for the first microbatch only
+    ("hkv1_gqa4_s16400", GroupShape(4, 1, 128, 512, (16400, 300), "bf16")),
+    ("hkv2_d64_s16500", GroupShape(2, 2, 64, 200, (16500,), "bf16")),
+]
+
+
+@pytest.mark.parametrize("name,shape", LONG_SUFFIX, ids=[c[0] for c in LONG_SUFFIX])
+def test_long_suffix_phase_b_matches_oracle(gpu, name, shape):
+    import torch
+    from paper_2606_01143_amd import binding as B
+    from paper_2606_01143_amd.group import DeviceGroup
+    _announce(f"long-suffix Phase B {name} {shape}")
+    inp = make_group(shape, seed=41)
+    grp = DeviceGroup(inp, dense=False)
+    B.profile_reset()
+    B.profile_enable(True)
+    try:
+        grp.run_schedule(overlap=False)
+        torch.cuda.synchronize()
+        _, n_bwd = B.profile_query("bwd_bf16")
+    finally:
+        B.profile_enable(False)
+    n_long = sum(1 for s in shape.suffix_lens if s >= 16384)
+    # one launch per short suffix, two per long one, one for Phase C
+    assert n_bwd == shape.n + n_long + 1, n_bwd
+    _assert_sampled(inp, grp.fetch("schedule"), f"schedule {name}", cache=True)

@@ -9,10 +9,11 @@ by over 10%, R = ceil(longest / average), 1 <= R <= 8, each share >= 16
 steps) and compared with the library's choice.  The atomic mode also
 reserves the fp32 dQ accumulator of the launch's rows and never splits the
 query-outer keys (it has no query-outer role).  The prefix backward of a
-prefix of 16384 keys or more runs, in the default mode, the key-outer role
-alone with 192-key tiles (six wave pairs per workgroup, one workgroup per
-CU): its steps are counted over 192-key tiles, on 256 slots, and no
-query-outer work is added."""
+prefix of 16384 keys or more, and the suffix backward of suffixes that long
+(the packed dense baseline's whole trajectories among them), run, in the
+default mode, the key-outer role alone with 192-key tiles (six wave pairs
+per workgroup, one workgroup per CU): their steps are counted over 192-key
+tiles, on 256 slots, and no query-outer work is added."""
 import math
 
 import pytest
@@ -39,8 +40,11 @@ def _rule(kv_steps, max_steps, atomic, slots=512):
 
 def _suffix_r(hq, hkv, P, n, ml, atomic):
     g, rows = hq // hkv, n * ml
-    kv = _tiles(P, 64) * g * ((rows + 31) // 32) + n * _causal(ml, g)
     crit = g * ((rows + 31) // 32) if P > 0 else g * ((ml + 31) // 32)
+    if not atomic and ml >= 16384:  # the key-outer role alone, 192-key tiles
+        kv = _tiles(P, 192) * g * ((rows + 31) // 32) + n * _causal(ml, g, 192)
+        return _rule(kv * hkv, crit, True, slots=256)
+    kv = _tiles(P, 64) * g * ((rows + 31) // 32) + n * _causal(ml, g)
     return _rule(kv * hkv, crit, atomic)
 
 
@@ -99,6 +103,9 @@ CASES = [
     (4, 2, 64, 1536, 3, 400, 747),       # ragged microbatch of three
     (4, 1, 128, 16384, 1, 1024, 1024),
     (4, 1, 128, 131072, 2, 1000, 1037),
+    (4, 1, 128, 0, 2, 16500, 32900),     # long whole sequences, no prefix (packed dense)
+    (32, 8, 128, 0, 8, 28800, 230400),   # the long-context group's packed dense baseline
+    (4, 1, 64, 512, 2, 16400, 20000),    # long suffixes behind a prefix
 ]
 
 
@@ -114,7 +121,7 @@ def test_suffix_backward_workspace_follows_the_rule(hq, hkv, d, P, n, ml, T, ato
 
 
 @MODES
-@pytest.mark.parametrize("hq,hkv,d,P", sorted({(c[0], c[1], c[2], c[3]) for c in CASES}))
+@pytest.mark.parametrize("hq,hkv,d,P", sorted({(c[0], c[1], c[2], c[3]) for c in CASES if c[3] > 0}))
 def test_prefix_backward_workspace_follows_the_rule(hq, hkv, d, P, atomic):
     dims = B.make_dims(hq, hkv, d, P, "bf16", atomic_dq=atomic)
     want, r = _prefix_ws(hq, hkv, d, P, atomic)
@@ -131,6 +138,9 @@ def test_rule_decisions_at_named_shapes():
     assert _suffix_r(4, 1, 2048, 1, 700, False) == 5 and _prefix_r(4, 1, 2048, False) == 8
     # long prefixes fill the GPU without shares
     assert _prefix_r(32, 8, 16384, False) == 1 and _suffix_r(4, 1, 131072, 2, 1000, False) == 1
+    # long whole sequences on 192-key tiles: one kv head's two sequences are
+    # cut, the long-context group's eight trajectories are not
+    assert _suffix_r(4, 1, 0, 2, 16500, False) > 1 and _suffix_r(32, 8, 0, 8, 28800, False) == 1
 
 
 def test_fp32_storage_never_splits():

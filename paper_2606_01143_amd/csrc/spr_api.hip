@@ -181,35 +181,60 @@ int bwd_kv_splits(const spr_dims* d, long kv_steps, long max_steps) {
   if (d->dtype != SPR_BF16) return 1;
   return bwd_bf16_kvsplit(kv_steps * d->num_kv_heads, max_steps, atomic_dq(d));
 }
-// Phase C of a long prefix (bf16, default mode) runs the key-outer role
-// alone, six wave pairs (192 keys) per workgroup at three waves per SIMD,
-// then the query-outer role in a launch of its own.  Each launch then fills
-// the GPU many times over; shorter prefixes keep the two roles in one
-// launch, where together they fill it.  The dense baseline's
-// per-trajectory backward does the same for sequences of that length, and
-// the suffix backward for suffixes of that length (the packed dense
-// baseline's whole trajectories among them).
-constexpr long kKvWideMin = 16384;
-bool prefix_kv_wide(const spr_dims* d) {
-  return d->dtype == SPR_BF16 && !atomic_dq(d) && d->prefix_len >= kKvWideMin;
+// The key-outer-only launch (bf16, default mode): the key-outer role alone,
+// six wave pairs (192 keys) per workgroup at three waves per SIMD, then the
+// query-outer role in a launch of its own.  It pays when its own work fills
+// the GPU several times over: at least kKvWideMinSteps (32-row tile, q head)
+// steps of 192-key tiles over all kv heads, 128 per CU.  Below that the two
+// roles share one launch, where together they fill it.  (Phase C measured:
+// 175 steps per CU and more, 8-15% faster; 87 and fewer, 6-42% slower.)  The
+// same rule serves Phase C, the dense baseline's per-trajectory backward and
+// the suffix backward (the packed dense baseline's whole trajectories among
+// them).
+constexpr long kKvWideMinSteps = 32768;
+bool kv_wide(const spr_dims* d, long wide_steps) {
+  return d->dtype == SPR_BF16 && !atomic_dq(d) && wide_steps * d->num_kv_heads >= kKvWideMinSteps;
 }
-bool dense_kv_wide(const spr_dims* d, int32_t max_len) {
-  return d->dtype == SPR_BF16 && !atomic_dq(d) && (long)d->prefix_len + max_len >= kKvWideMin;
+long wide_bk() { return bwd_bf16_kv_wide_block_k(); }
+// Phase C: causal prefix rows
+long prefix_wide_steps(const spr_dims* d) {
+  return causal_steps(d->prefix_len, d->num_q_heads / d->num_kv_heads, wide_bk());
 }
-bool suffix_kv_wide(const spr_dims* d, int32_t max_len) {
-  return d->dtype == SPR_BF16 && !atomic_dq(d) && max_len >= kKvWideMin;
+// the dense per-trajectory launch: prefix key tiles see the causal prefix
+// rows and the suffix rows, suffix key tiles their own rows
+long dense_wide_steps(const spr_dims* d, int32_t max_len) {
+  const long g = d->num_q_heads / d->num_kv_heads, sr = g * ((max_len + 31) / 32);
+  return causal_steps(d->prefix_len, g, wide_bk()) + (long)tiles(d->prefix_len, (int)wide_bk()) * sr +
+         causal_steps(max_len, g, wide_bk());
 }
 // Phase B: prefix key tiles see every suffix row (at most n_mb * max_len),
 // suffix key tiles their own causal rows
+long suffix_wide_steps(const spr_dims* d, int32_t n_mb, int32_t max_len) {
+  const long g = d->num_q_heads / d->num_kv_heads, rows = (long)n_mb * max_len;
+  return (long)tiles(d->prefix_len, (int)wide_bk()) * g * ((rows + 31) / 32) +
+         (long)n_mb * causal_steps(max_len, g, wide_bk());
+}
+bool prefix_kv_wide(const spr_dims* d) { return kv_wide(d, prefix_wide_steps(d)); }
+bool dense_kv_wide(const spr_dims* d, int32_t max_len) { return kv_wide(d, dense_wide_steps(d, max_len)); }
+// In Phase B the prefix key tiles all sweep every suffix row of the
+// microbatch, so their workgroups are equally long; one per CU, they run in
+// rounds of 256, and a last round mostly empty costs more than the launch
+// gains.  With a prefix the key-outer-only launch is taken only when those
+// rounds are at least 85% full (measured: 688 and 1200 tiles, 90% and 94%
+// full, 2-11% faster; 88, 172 and 344 tiles, 34-67%, 4-10% slower).
+bool suffix_kv_wide(const spr_dims* d, int32_t n_mb, int32_t max_len) {
+  if (!kv_wide(d, suffix_wide_steps(d, n_mb, max_len))) return false;
+  if (d->prefix_len == 0) return true;
+  const long n = (long)tiles(d->prefix_len, (int)wide_bk()) * d->num_kv_heads;
+  const long slots = bwd_bf16_kv_wide_slots();
+  return n * 100 >= 85 * slots * ((n + slots - 1) / slots);
+}
 int suffix_bwd_kv_splits(const spr_dims* d, int32_t n_mb, int32_t max_len) {
   const long g = d->num_q_heads / d->num_kv_heads, rows = (long)n_mb * max_len;
   const long max_steps = d->prefix_len > 0 ? g * ((rows + 31) / 32) : g * ((max_len + 31) / 32);
-  if (suffix_kv_wide(d, max_len)) {  // wide key tiles, one slot per CU, no query-outer role
-    const long bk = bwd_bf16_kv_wide_block_k();
-    const long kv = (long)tiles(d->prefix_len, (int)bk) * g * ((rows + 31) / 32) +
-                    (long)n_mb * causal_steps(max_len, g, bk);
-    return bwd_bf16_kvsplit(kv * d->num_kv_heads, max_steps, true, bwd_bf16_kv_wide_slots());
-  }
+  if (suffix_kv_wide(d, n_mb, max_len))  // wide key tiles, one slot per CU, no query-outer role
+    return bwd_bf16_kvsplit(suffix_wide_steps(d, n_mb, max_len) * d->num_kv_heads, max_steps, true,
+                            bwd_bf16_kv_wide_slots());
   const long pre = (long)tiles(d->prefix_len, bwd_bf16_block_k()) * g * ((rows + 31) / 32);
   const long kv = pre + (long)n_mb * causal_steps(max_len, g);
   return bwd_kv_splits(d, kv, max_steps);
@@ -219,8 +244,7 @@ int prefix_bwd_kv_splits(const spr_dims* d) {
   const long g = d->num_q_heads / d->num_kv_heads;
   const long max_steps = g * ((d->prefix_len + 31) / 32);
   if (prefix_kv_wide(d))  // wide key tiles, one slot per CU, no query-outer role
-    return bwd_bf16_kvsplit(causal_steps(d->prefix_len, g, bwd_bf16_kv_wide_block_k()) * d->num_kv_heads,
-                            max_steps, true, bwd_bf16_kv_wide_slots());
+    return bwd_bf16_kvsplit(prefix_wide_steps(d) * d->num_kv_heads, max_steps, true, bwd_bf16_kv_wide_slots());
   return bwd_kv_splits(d, causal_steps(d->prefix_len, g), max_steps);
 }
 // the dense baseline's per-trajectory launch: prefix key tiles see the
@@ -228,11 +252,9 @@ int prefix_bwd_kv_splits(const spr_dims* d) {
 int dense_bwd_kv_splits(const spr_dims* d, int32_t max_len) {
   const long g = d->num_q_heads / d->num_kv_heads, P = d->prefix_len;
   const long sr = g * ((max_len + 31) / 32);
-  if (dense_kv_wide(d, max_len)) {  // wide key tiles, one slot per CU, no query-outer role
-    const long bk = bwd_bf16_kv_wide_block_k();
-    const long kv = causal_steps(P, g, bk) + (long)tiles(d->prefix_len, (int)bk) * sr + causal_steps(max_len, g, bk);
-    return bwd_bf16_kvsplit(kv * d->num_kv_heads, g * ((P + 31) / 32) + sr, true, bwd_bf16_kv_wide_slots());
-  }
+  if (dense_kv_wide(d, max_len))  // wide key tiles, one slot per CU, no query-outer role
+    return bwd_bf16_kvsplit(dense_wide_steps(d, max_len) * d->num_kv_heads, g * ((P + 31) / 32) + sr, true,
+                            bwd_bf16_kv_wide_slots());
   const long kv = causal_steps(P, g) + (long)tiles(d->prefix_len, bwd_bf16_block_k()) * sr +
                   causal_steps(max_len, g);
   return bwd_kv_splits(d, kv, g * ((P + 31) / 32) + sr);
@@ -675,7 +697,7 @@ spr_status spr_suffix_attn_bwd_accum(const spr_dims* dims, const void* k_p, cons
     a.part_dk = at<float>(ws, w.part_dk);
     a.part_dv = at<float>(ws, w.part_dv);
   }
-  if (suffix_kv_wide(dims, max_len)) {
+  if (suffix_kv_wide(dims, n_mb, max_len)) {
     // the key-outer role alone on 192-key tiles, then the query-outer role
     // (as Phase C of a long prefix)
     AttnArgs kv = a;

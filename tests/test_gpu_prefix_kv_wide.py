@@ -1,16 +1,17 @@
-"""Backward launches over long sequences (bf16, default mode): a Phase C of
-a prefix of 16384 keys or more runs the key-outer role alone, six wave
-pairs (192 keys) per workgroup, then the query-outer role in a launch of its
-own; the dense baseline's per-trajectory backward of sequences that long
-does the same, and so does the suffix backward of suffixes that long (the
-packed dense baseline's whole trajectories, or a long suffix behind a short
-prefix in Phase B).  Checked at full length on one or two kv heads against the
-oracle's sampled rows and keys (each from its own sequence; both sampled
-references are pinned to the whole oracle on small groups) and the
-identities that hold at any size, with row shares (3 to 6), head_dim 64,
-and prefixes that are not a multiple of 192 keys (a partial last tile whose
-last pairs have no key); the Phase C halves bitwise equal to the whole
-call; reruns bitwise equal."""
+"""Backward launches whose key-outer work fills the GPU several times over
+(bf16, default mode: at least 32768 (32-row tile, q head) steps of 192-key
+tiles over all kv heads) run the key-outer role alone, six wave pairs (192
+keys) per workgroup, then the query-outer role in a launch of its own:
+Phase C of a long prefix, the dense baseline's per-trajectory backward of
+long sequences, and the suffix backward (the packed dense baseline's whole
+trajectories; Phase B when its prefix key tiles also fill their rounds of
+256 workgroups to 85%).  Checked at full length on one or two kv heads
+against the oracle's sampled rows and keys (each from its own sequence;
+both sampled references are pinned to the whole oracle on small groups) and
+the identities that hold at any size, with row shares (3 to 6), head_dim
+64, and prefixes that are not a multiple of 192 keys (a partial last tile
+whose last pairs have no key); the Phase C halves bitwise equal to the
+whole call; reruns bitwise equal."""
 import sys
 
 import numpy as np
@@ -140,15 +141,15 @@ def test_long_sequences_packed_dense_baseline_matches_oracle(gpu, name, shape):
 
 
 LONG_SUFFIX = [
-    # a suffix of 16400 = 85 * 192 + 80 tokens behind a prefix of 512, and a
-    # short one: Phase B takes the two launches for the first microbatch only
-    ("hkv1_gqa4_s16400", GroupShape(4, 1, 128, 512, (16400, 300), "bf16")),
-    ("hkv2_d64_s16500", GroupShape(2, 2, 64, 200, (16500,), "bf16")),
+    # two kv heads, 21000 keys: 220 prefix key tiles of 192, 86% of one round
+    # of 256 workgroups.  The 3000-token suffix's Phase B takes the two
+    # launches, the 100-token one the shared launch; Phase C two launches.
+    ("hkv2_p21000_s3000", GroupShape(4, 2, 128, 21000, (3000, 100), "bf16"), 5),
+    # d = 64, no GQA, 21100 = 109 * 192 + 172: a partial last prefix tile
+    ("hkv2_d64_p21100_s5000", GroupShape(2, 2, 64, 21100, (5000,), "bf16"), 4),
 ]
-
-
-@pytest.mark.parametrize("name,shape", LONG_SUFFIX, ids=[c[0] for c in LONG_SUFFIX])
-def test_long_suffix_phase_b_matches_oracle(gpu, name, shape):
+@pytest.mark.parametrize("name,shape,launches", LONG_SUFFIX, ids=[c[0] for c in LONG_SUFFIX])
+def test_long_suffix_phase_b_matches_oracle(gpu, name, shape, launches):
     import torch
     from paper_2606_01143_amd import binding as B
     from paper_2606_01143_amd.group import DeviceGroup
@@ -163,7 +164,28 @@ def test_long_suffix_phase_b_matches_oracle(gpu, name, shape):
         _, n_bwd = B.profile_query("bwd_bf16")
     finally:
         B.profile_enable(False)
-    n_long = sum(1 for s in shape.suffix_lens if s >= 16384)
-    # one launch per short suffix, two per long one, one for Phase C
-    assert n_bwd == shape.n + n_long + 1, n_bwd
+    assert n_bwd == launches, n_bwd
     _assert_sampled(inp, grp.fetch("schedule"), f"schedule {name}", cache=True)
+
+
+def test_long_and_short_suffix_in_one_microbatch_matches_oracle(gpu):
+    """Both suffixes of the first long-suffix group as one microbatch: the
+    key-outer-only launch also sweeps the short suffix's keys and rows."""
+    import torch
+    from paper_2606_01143_amd import binding as B
+    from paper_2606_01143_amd.group import DeviceGroup
+    name, shape, _ = LONG_SUFFIX[0]
+    _announce(f"long and short suffix packed {name} {shape}")
+    inp = make_group(shape, seed=43)
+    mb = [(0, shape.n)]
+    grp = DeviceGroup(inp, dense=False, microbatch_splits=[mb])
+    B.profile_reset()
+    B.profile_enable(True)
+    try:
+        grp.run_schedule(microbatches=mb, overlap=False)
+        torch.cuda.synchronize()
+        _, n_bwd = B.profile_query("bwd_bf16")
+    finally:
+        B.profile_enable(False)
+    assert n_bwd == 4, n_bwd  # Phase B and Phase C, two launches each
+    _assert_sampled(inp, grp.fetch("schedule"), f"schedule packed {name}", cache=True)

@@ -8,12 +8,15 @@ per CU on 256 CUs; split when the longest sweep exceeds the average per slot
 by over 10%, R = ceil(longest / average), 1 <= R <= 8, each share >= 16
 steps) and compared with the library's choice.  The atomic mode also
 reserves the fp32 dQ accumulator of the launch's rows and never splits the
-query-outer keys (it has no query-outer role).  The prefix backward of a
-prefix of 16384 keys or more, and the suffix backward of suffixes that long
-(the packed dense baseline's whole trajectories among them), run, in the
-default mode, the key-outer role alone with 192-key tiles (six wave pairs
-per workgroup, one workgroup per CU): their steps are counted over 192-key
-tiles, on 256 slots, and no query-outer work is added."""
+query-outer keys (it has no query-outer role).  A backward launch whose key-outer work, counted in
+steps of 192-key tiles over all kv heads, reaches 32768 (128 per CU) runs,
+in the default mode, the key-outer role alone with 192-key tiles (six wave
+pairs per workgroup, one workgroup per CU): its steps are counted over
+192-key tiles, on 256 slots, and no query-outer work is added.  The same
+rule serves the prefix backward and the suffix backward (the packed dense
+baseline's whole trajectories among them); a suffix backward with a prefix
+also needs its prefix key tiles, one workgroup each, to fill their rounds of
+256 to at least 85%."""
 import math
 
 import pytest
@@ -38,19 +41,26 @@ def _rule(kv_steps, max_steps, atomic, slots=512):
     return max(1, min(math.ceil(max_steps / per_slot), max_steps // 16, 8))
 
 
+def _wide(steps, hkv, atomic):
+    """the key-outer role alone on 192-key tiles"""
+    return not atomic and steps * hkv >= 32768
+
+
 def _suffix_r(hq, hkv, P, n, ml, atomic):
     g, rows = hq // hkv, n * ml
     crit = g * ((rows + 31) // 32) if P > 0 else g * ((ml + 31) // 32)
-    if not atomic and ml >= 16384:  # the key-outer role alone, 192-key tiles
-        kv = _tiles(P, 192) * g * ((rows + 31) // 32) + n * _causal(ml, g, 192)
-        return _rule(kv * hkv, crit, True, slots=256)
+    wide = _tiles(P, 192) * g * ((rows + 31) // 32) + n * _causal(ml, g, 192)
+    nt = _tiles(P, 192) * hkv  # equally long prefix sweeps, rounds of 256
+    full = P == 0 or nt * 100 >= 85 * 256 * ((nt + 255) // 256)
+    if _wide(wide, hkv, atomic) and full:
+        return _rule(wide * hkv, crit, True, slots=256)
     kv = _tiles(P, 64) * g * ((rows + 31) // 32) + n * _causal(ml, g)
     return _rule(kv * hkv, crit, atomic)
 
 
 def _prefix_r(hq, hkv, P, atomic):
     g = hq // hkv
-    if not atomic and P >= 16384:  # the key-outer role alone, 192-key tiles
+    if _wide(_causal(P, g, 192), hkv, atomic):
         return _rule(_causal(P, g, 192) * hkv, g * ((P + 31) // 32), True, slots=256)
     return _rule(_causal(P, g) * hkv, g * ((P + 31) // 32), atomic)
 
@@ -129,9 +139,17 @@ def test_prefix_backward_workspace_follows_the_rule(hq, hkv, d, P, atomic):
 
 
 def test_rule_decisions_at_named_shapes():
-    # Llama3-8B group at P = 4096: Phase B whole, Phase C in two shares
-    for atomic in (False, True):
-        assert _suffix_r(32, 8, 4096, 1, 512, atomic) == 1 and _prefix_r(32, 8, 4096, atomic) == 2
+    # Llama3-8B group at P = 4096: Phase B whole; Phase C in two shares of
+    # the shared launch (atomic mode), or in three shares of the
+    # key-outer-only launch (512 steps for key tile 0 against 179 per slot)
+    assert _suffix_r(32, 8, 4096, 1, 512, True) == 1 and _prefix_r(32, 8, 4096, True) == 2
+    assert _suffix_r(32, 8, 4096, 1, 512, False) == 1 and _prefix_r(32, 8, 4096, False) == 3
+    # the launch choice at the measured points: key-outer-only from 175
+    # steps per CU on, shared at 87 and fewer
+    g = 4
+    assert _wide(_causal(4096, g, 192), 8, False) and _wide(_causal(8192, g, 192), 2, False)
+    assert not _wide(_causal(8192, g, 192), 1, False) and not _wide(_causal(2048, g, 192), 8, False)
+    assert not _wide(_causal(4096, g, 192), 2, False)
     # the long-context group (P = 28672) fills the GPU without shares
     assert _prefix_r(32, 8, 28672, True) == 1 and _suffix_r(32, 8, 28672, 1, 128, True) == 1
     # one kv head, short prefix: the sweeps are cut

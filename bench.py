@@ -84,7 +84,7 @@ def mfma_summary(workload: str) -> str:
     """Committed counter summary of the matrix-core utilisation."""
     return os.path.join(ROOT, "profiles", f"mfma_util_{workload}.md")
 
-BWD_SOURCES = ["kernels_bf16_bwd.hip", "tile.hpp", "common.hpp"]
+BWD_SOURCES = ["kernels_bf16_bwd.hip", "tile.hpp", "common.hpp", "spr_api.hip", "launch.hpp"]
 SWEEPS = {
     "c3": [f"qwen3_8b_p{p}_n{n}" for p in (2048, 8192, 16384) for n in (4, 8, 16)],
     "c4": ["qwen3_moe_p8192_n16_ragged"],

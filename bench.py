@@ -491,10 +491,10 @@ def main():
         out["dense_equiv_tflops"] = round(tf(dense_flops, ms_dense), 3)
         out["flop_ratio_dense_over_schedule"] = round(dense_flops / sched_flops, 3)
         out["policy_" + other_name]["speedup_vs_dense"] = round(ms_dense / st_o["mean"], 3)
-        out["dense_policy"] = "one trajectory per launch pair (the dense trainer's per-sequence order)"
+        out["dense_policy"] = "one trajectory per forward/backward call pair (the dense trainer's per-sequence order)"
         log(f"dense {ms_dense:.3f} ms/step, speedup {ms_dense / ms_step:.2f}x")
         # the dense baseline under the packed policy: the N materialized
-        # trajectories as one varlen microbatch, one launch pair; compared
+        # trajectories as one varlen microbatch, one forward/backward call pair; compared
         # with the schedule's packed policy
         log("dense baseline, packed: warmup + timed steps")
         grp.prepare_dense_packed()
@@ -506,7 +506,7 @@ def main():
             "ms_per_step_min": round(st_dp["min"], 4),
             "speedup_of_schedule_packed": round(st_dp["mean"] / ms_pk, 3),
             "policy": "all N trajectories materialized as one packed varlen microbatch: one forward "
-                      "and one backward launch of causal attention over the N whole sequences; prefix "
+                      "and one backward call of causal attention over the N whole sequences; prefix "
                       "gradients per copy (the N-way sum is not timed)"}
         log(f"dense packed {st_dp['mean']:.3f} ms/step, schedule packed speedup "
             f"{st_dp['mean'] / ms_pk:.2f}x")
@@ -562,7 +562,7 @@ def sweep_one(name: str, args):
     phases = phase_times(grp, mbs)
     ms_dense = time_steps(lambda: grp.run_dense(), max(1, steps // 2), 1)
     # the packed policy on both sides: all suffixes in one microbatch, and
-    # the N materialized trajectories as one varlen launch pair
+    # the N materialized trajectories as one varlen forward/backward call pair
     packed = [(0, shape.n)]
     grp.prepare(packed)
     ms_pk = time_steps(lambda: grp.run_schedule(packed), steps, 1)

@@ -359,8 +359,8 @@ class DeviceGroup:
     def run_dense_packed(self, stream=None) -> None:
         """The dense baseline under the packed batching policy: the N
         materialized trajectories as one varlen microbatch, one forward and
-        one backward launch pair of causal attention over each whole
-        sequence (the library's suffix calls with no shared prefix).  The
+        one backward call of causal attention over each whole sequence
+        (the library's suffix calls with no shared prefix).  The
         prefix gradients stay per copy, as a dense trainer has them;
         ``fetch_dense_packed`` sums them for comparison."""
         self.prepare_dense_packed()

@@ -27,6 +27,7 @@ namespace spr {
 
 namespace {
 constexpr int kFwdBQ = 128;
+constexpr int kFwdWideBQ = 96;  // rows of the twelve-wave prefix launch (per q head)
 // headroom (log2 domain) of the softmax reference over a row's true running
 // max: P = exp2(s - m) stays below 256, far inside fp32, and bf16 rounds it
 // to the same relative precision as below 1
@@ -58,40 +59,68 @@ __device__ __forceinline__ RowBlock decode_row_block(const AttnArgs& a, int ntx)
   return rb;
 }
 
-template <int D>
-__global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(AttnArgs a) {
+// The forward in one of two workgroup forms.  Four waves: 128 rows of one q
+// head, any rows, key splits.  Twelve waves (WIDE, the prefix forward of
+// long prefixes): 96 prefix rows of four q heads of one kv head, wave w on
+// rows 32 (w / 4) .. + 31 of head w % 4, all twelve reading each K/V tile
+// that waves 0-3 load.  Both keep the 64 KB of double-buffered tiles, so
+// only the twelve-wave form holds three waves on every SIMD, which needs
+// the loop to fit in 168 registers.
+template <int D, bool WIDE>
+__device__ __forceinline__ void fwd_body(const AttnArgs& a, bf16 (&Ks)[2][Tile<D>::ELEMS],
+                                         bf16 (&Vs)[2][Tile<D>::ELEMS]) {
   constexpr int NS = D / 16;   // k-steps over d for S^T
   constexpr int NDB = D / 32;  // 32-wide d blocks of O^T
-  constexpr int TE = Tile<D>::ELEMS, BK = kTileRows;
-  // double-buffered key tiles
-  __shared__ __attribute__((aligned(1024))) bf16 Ks[2][TE];
-  __shared__ __attribute__((aligned(1024))) bf16 Vs[2][TE];
+  constexpr int BK = kTileRows;
+  constexpr int BQ = WIDE ? kFwdWideBQ : kFwdBQ;
 
   const int tid = threadIdx.x, lane = tid & 63, w = wave_id();
   const int r = lane & 31, h = lane >> 5;
   FragOffsets<D> fo;
   fo.init(lane);
 
-  // ---- which 128 query rows: prefix rows, or rows of suffix seq_base + z
-  const RowBlock blk = decode_row_block(a, a.n_prefix_q_tiles + a.n_suffix_q_tiles);
-  const int seq = a.seq_base + blk.z;
+  // ---- which BQ query rows: prefix rows, or rows of suffix seq_base + z
   bool prefix_rows;
-  int lp0, seg_len, row_base;
-  if (blk.tile < a.n_prefix_q_tiles) {
+  int lp0, seg_len, row_base, hq, hk, wave_lp0;
+  RowBlock blk;
+  if constexpr (WIDE) {
+    // block b -> (kv head b % Hkv, group of four q heads, 96-row tile),
+    // the rows with the most keys first
+    const int G = a.hq / a.hkv;
+    int b = blockIdx.x;
+    hk = b % a.hkv;
+    b /= a.hkv;
+    const int hg = b % (G / 4);
+    b /= G / 4;
+    blk.tile = a.n_prefix_q_tiles - 1 - b;
+    blk.z = 0;
+    blk.split = 0;
+    hq = hk * G + 4 * hg + (w & 3);
     prefix_rows = true;
-    lp0 = blk.tile * kFwdBQ;
+    lp0 = blk.tile * BQ;
     seg_len = a.P;
     row_base = 0;
+    wave_lp0 = lp0 + 32 * (w >> 2);
   } else {
-    prefix_rows = false;
-    lp0 = (blk.tile - a.n_prefix_q_tiles) * kFwdBQ;
-    const SegRows sg = suffix_rows(a.cu, seq, a.total_len);
-    row_base = sg.base;
-    seg_len = sg.len;
+    blk = decode_row_block(a, a.n_prefix_q_tiles + a.n_suffix_q_tiles);
+    const int seq = a.seq_base + blk.z;
+    if (blk.tile < a.n_prefix_q_tiles) {
+      prefix_rows = true;
+      lp0 = blk.tile * BQ;
+      seg_len = a.P;
+      row_base = 0;
+    } else {
+      prefix_rows = false;
+      lp0 = (blk.tile - a.n_prefix_q_tiles) * BQ;
+      const SegRows sg = suffix_rows(a.cu, seq, a.total_len);
+      row_base = sg.base;
+      seg_len = sg.len;
+    }
+    hq = blk.hq;
+    hk = hq / (a.hq / a.hkv);
+    wave_lp0 = lp0 + 32 * w;  // first row of this wave
   }
   if (lp0 >= seg_len) return;
-  const int hq = blk.hq, hk = hq / (a.hq / a.hkv);
-  const int wave_lp0 = lp0 + 32 * w;  // first row of this wave
   const int row_lp = wave_lp0 + r;    // this lane's query row (segment-local)
   const bool row_valid = row_lp < seg_len;
   const int my_lp = row_valid ? row_lp : seg_len - 1;  // rows past the end recompute the last one
@@ -112,7 +141,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(AttnArgs a) {
   float m = -INFINITY, l = 0.f;  // running max (log2 domain) and sum of row my_lp
 
   // key tiles: prefix keys first (causal for prefix rows), then own suffix keys
-  const int last_lp = min(lp0 + kFwdBQ, seg_len) - 1;
+  const int last_lp = min(lp0 + BQ, seg_len) - 1;
   const int nkeys0 = prefix_rows ? min(a.P, last_lp + 1) : a.P;
   const int nkeys1 = prefix_rows ? 0 : last_lp + 1;
   const int nt0 = (nkeys0 + BK - 1) / BK, nt1 = (nkeys1 + BK - 1) / BK;
@@ -123,8 +152,9 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(AttnArgs a) {
   const bf16 *k_p = in_sgpr((const bf16*)a.k_p), *k_s = in_sgpr((const bf16*)a.k_s);
   const bf16 *v_p = in_sgpr((const bf16*)a.v_p), *v_s = in_sgpr((const bf16*)a.v_s);
   TileLoader<D, 4, BK> tl;
-  tl.init(a.hkv, w, lane);
+  tl.init(a.hkv, w & 3, lane);
   auto issue = [&](int t, bf16* Kd, bf16* Vd) {
+    if (WIDE && w >= 4) return;  // waves 0-3 load every tile
     const int seg = t < nt0 ? 0 : 1;
     const int k0 = (seg == 0 ? t : t - nt0) * BK;
     const int nk = min(BK, (seg == 0 ? nkeys0 : nkeys1) - k0);
@@ -149,7 +179,11 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(AttnArgs a) {
 #define SC(e) st[(e) >> 4][(e) & 15]
     if (nk < BK || (causal && k0 + BK - 1 > wave_lp0)) {  // partial or diagonal tile
       // keys kk = 32 (e / 16) + c_row0(e % 16) + 4 h are visible iff kk < lim
-      const int lim = (causal ? min(nk, my_lp - k0 + 1) : nk) - 4 * h;
+      int lp = my_lp;  // recomputed in the twelve-wave form (registers)
+      if constexpr (WIDE)
+        lp = min(wave_lp0 + (int)(__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u)) & 31),
+                 seg_len - 1);
+      const int lim = (causal ? min(nk, lp - k0 + 1) : nk) - 4 * h;
 #pragma unroll
       for (int e = 0; e < 32; ++e) SC(e) = 32 * (e >> 4) + c_row0(e & 15) < lim ? SC(e) : -INFINITY;
     }
@@ -186,7 +220,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(AttnArgs a) {
 #pragma unroll
       for (int db = 0; db < NDB; ++db) o[db] = mfma32(tr_frag<D>(Vc, fo, 16 * u, db), pb, o[db]);
     }
-    sched_reads_ahead<BK / 16 * NDB, 2, 2>();
+    sched_reads_ahead<BK / 16 * NDB, 2, WIDE ? 1 : 2>();
   };
 
   if (t_begin < t_end) issue(t_begin, Ks[0], Vs[0]);
@@ -205,8 +239,18 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(AttnArgs a) {
     tile_barrier();
   }
 
-  if (!row_valid) return;
-  if (a.n_split > 1) {
+  // (the twelve-wave form recomputes the lane and its row here: at 168
+  // registers, values kept from before the loop would spill)
+  int e_lp = my_lp, e_h = h;
+  bool e_valid = row_valid;
+  if constexpr (WIDE) {
+    const int e_lane = (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+    e_h = e_lane >> 5;
+    e_lp = wave_lp0 + (e_lane & 31);
+    e_valid = e_lp < seg_len;
+  }
+  if (!e_valid) return;
+  if (!WIDE && a.n_split > 1) {
     // partial result of this key range: O / l and log2(sum) + max (a range
     // with no visible key gives l = 0: weight 0 in the combine)
     const size_t prow = ((size_t)blk.split * a.total_len + row_base + my_lp) * a.hq + hq;
@@ -224,7 +268,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(AttnArgs a) {
   // o[db][i] = O^T[d = 32 db + c_row0(i) + 4 h][row my_lp]
   const float inv = 1.f / l;
   bf16* ob = (bf16*)(prefix_rows ? a.o_p : a.o_s);
-  const size_t off = ((size_t)(row_base + my_lp) * a.hq + hq) * D + 4 * h;
+  const size_t off = ((size_t)(row_base + e_lp) * a.hq + hq) * D + 4 * e_h;
 #pragma unroll
   for (int db = 0; db < NDB; ++db)
 #pragma unroll
@@ -233,10 +277,24 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(AttnArgs a) {
                         (bf16)(o[db][4 * g4 + 2] * inv), (bf16)(o[db][4 * g4 + 3] * inv)};
       *(bf16x4*)(ob + off + 32 * db + 8 * g4) = v;
     }
-  if (h == 0) {
+  if (e_h == 0) {
     float* lse = prefix_rows ? a.lse_p : a.lse_s;
-    lse[(size_t)(row_base + my_lp) * a.hq + hq] = (m + log2f(l)) * kLn2;
+    lse[(size_t)(row_base + e_lp) * a.hq + hq] = (m + log2f(l)) * kLn2;
   }
+}
+
+template <int D>
+__global__ __launch_bounds__(kThreads, 2) void fwd_bf16_kernel(AttnArgs a) {
+  __shared__ __attribute__((aligned(1024))) bf16 Ks[2][Tile<D>::ELEMS];
+  __shared__ __attribute__((aligned(1024))) bf16 Vs[2][Tile<D>::ELEMS];
+  fwd_body<D, false>(a, Ks, Vs);
+}
+
+template <int D>
+__global__ __launch_bounds__(3 * kThreads, 1) void fwd_wide_kernel(AttnArgs a) {
+  __shared__ __attribute__((aligned(1024))) bf16 Ks[2][Tile<D>::ELEMS];
+  __shared__ __attribute__((aligned(1024))) bf16 Vs[2][Tile<D>::ELEMS];
+  fwd_body<D, true>(a, Ks, Vs);
 }
 
 // Merge of the n_split partial outputs of every (suffix row, q head):
@@ -289,6 +347,24 @@ hipError_t launch_fwd_bf16(const AttnArgs& a, int head_dim, int n_z, hipStream_t
     hipLaunchKernelGGL(fwd_combine_kernel<128>, dim3(cb), dim3(256), 0, st, a);
   return hipGetLastError();
 }
+
+// The prefix forward in its twelve-wave form: a.n_prefix_q_tiles counts
+// 96-row tiles; prefix rows only, no key splits, four q heads per kv head
+// or a multiple of four.
+hipError_t launch_fwd_bf16_wide(const AttnArgs& a, int head_dim, hipStream_t st) {
+  const int G = a.hq / a.hkv;
+  if (G % 4 != 0 || a.n_suffix_q_tiles != 0 || a.n_split > 1 || a.n_seq > 0) return hipErrorInvalidValue;
+  const long nb = (long)a.n_prefix_q_tiles * a.hkv * (G / 4);
+  if (nb == 0) return hipSuccess;
+  ProfileScope ps("fwd_bf16", st);
+  if (head_dim == 64)
+    hipLaunchKernelGGL(fwd_wide_kernel<64>, dim3((unsigned)nb), dim3(3 * kThreads), 0, st, a);
+  else
+    hipLaunchKernelGGL(fwd_wide_kernel<128>, dim3((unsigned)nb), dim3(3 * kThreads), 0, st, a);
+  return hipGetLastError();
+}
+
+int fwd_bf16_wide_block_q() { return kFwdWideBQ; }
 
 int fwd_bf16_split(int n_row_blocks, int prefix_len) {
   // enough workgroups for two per CU on 256 CUs, each split keeping at

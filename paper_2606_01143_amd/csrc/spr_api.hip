@@ -181,6 +181,16 @@ int bwd_kv_splits(const spr_dims* d, long kv_steps, long max_steps) {
   if (d->dtype != SPR_BF16) return 1;
   return bwd_bf16_kvsplit(kv_steps * d->num_kv_heads, max_steps, atomic_dq(d));
 }
+// The prefix forward in its twelve-wave form (96 rows of four q heads per
+// workgroup, three waves on every SIMD) for bf16 groups of four q heads per
+// kv head (or a multiple), once its workgroups fill the GPU several times.
+constexpr long kFwdWideMinBlocks = 1024;
+bool fwd_wide(const spr_dims* d) {
+  if (d->dtype != SPR_BF16 || d->num_q_heads % (4 * d->num_kv_heads) != 0) return false;
+  const long g4 = d->num_q_heads / d->num_kv_heads / 4;
+  return (long)tiles(d->prefix_len, fwd_bf16_wide_block_q()) * d->num_kv_heads * g4 >= kFwdWideMinBlocks;
+}
+
 // The key-outer-only launch (bf16, default mode): the key-outer role alone,
 // six wave pairs (192 keys) per workgroup at three waves per SIMD, then the
 // query-outer role in a launch of its own.  It pays when its own work fills
@@ -503,6 +513,11 @@ spr_status spr_prefix_fwd(const spr_dims* dims, const void* q_p, const void* k_p
   if (P == 0) return ok();
   AttnArgs a = base_args(dims);
   a.q_p = q_p; a.k_p = k_p; a.v_p = v_p; a.o_p = o_p; a.lse_p = lse_p;
+  if (fwd_wide(dims)) {
+    a.n_prefix_q_tiles = tiles(dims->prefix_len, fwd_bf16_wide_block_q());
+    if ((st = hip_check(launch_fwd_bf16_wide(a, dims->head_dim, stream), "prefix forward")) != SPR_OK) return st;
+    return ok();
+  }
   a.n_prefix_q_tiles = tiles(dims->prefix_len, block_q(dims->dtype));
   if ((st = hip_check(launch_fwd(dims, a, 1, stream), "prefix forward")) != SPR_OK) return st;
   return ok();

@@ -50,7 +50,8 @@ def _functions(text, pattern):
 
 @pytest.mark.parametrize("src,pattern", [("kernels_bf16_bwd.hip", "bwd_bf16_kernel"),
                                          ("kernels_bf16_bwd.hip", "bwd_kv_wide_kernel"),
-                                         ("kernels_bf16_fwd.hip", "fwd_bf16_kernel")])
+                                         ("kernels_bf16_fwd.hip", "fwd_bf16_kernel"),
+                                         ("kernels_bf16_fwd.hip", "fwd_wide_kernel")])
 def test_kernels_do_not_spill_copy_or_serialize(src, pattern):
     funcs = _functions(_compile_to_asm(src), pattern)
     assert funcs, f"{pattern} not found in the assembly"

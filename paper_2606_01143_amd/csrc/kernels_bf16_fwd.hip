@@ -60,12 +60,12 @@ __device__ __forceinline__ RowBlock decode_row_block(const AttnArgs& a, int ntx)
 }
 
 // The forward in one of two workgroup forms.  Four waves: 128 rows of one q
-// head, any rows, key splits.  Twelve waves (WIDE, the prefix forward of
-// long prefixes): 96 prefix rows of four q heads of one kv head, wave w on
-// rows 32 (w / 4) .. + 31 of head w % 4, all twelve reading each K/V tile
-// that waves 0-3 load.  Both keep the 64 KB of double-buffered tiles, so
-// only the twelve-wave form holds three waves on every SIMD, which needs
-// the loop to fit in 168 registers.
+// head, key splits allowed.  Twelve waves (WIDE, launches whose workgroups
+// fill the GPU several times over): 96 rows of four q heads of one kv head,
+// wave w on rows 32 (w / 4) .. + 31 of head w % 4, all twelve reading each
+// K/V tile that waves 0-3 load, no key splits.  Both keep the 64 KB of
+// double-buffered tiles, so only the twelve-wave form holds three waves on
+// every SIMD, which needs the loop to fit in 168 registers.
 template <int D, bool WIDE>
 __device__ __forceinline__ void fwd_body(const AttnArgs& a, bf16 (&Ks)[2][Tile<D>::ELEMS],
                                          bf16 (&Vs)[2][Tile<D>::ELEMS]) {
@@ -80,47 +80,44 @@ __device__ __forceinline__ void fwd_body(const AttnArgs& a, bf16 (&Ks)[2][Tile<D
   fo.init(lane);
 
   // ---- which BQ query rows: prefix rows, or rows of suffix seq_base + z
-  bool prefix_rows;
-  int lp0, seg_len, row_base, hq, hk, wave_lp0;
+  const int ntx = a.n_prefix_q_tiles + a.n_suffix_q_tiles;
+  int hq, hk;
   RowBlock blk;
   if constexpr (WIDE) {
-    // block b -> (kv head b % Hkv, group of four q heads, 96-row tile),
-    // the rows with the most keys first
+    // block b -> (kv head b % Hkv, group of four q heads, 96-row tile,
+    // suffix), the rows with the most keys first
     const int G = a.hq / a.hkv;
     int b = blockIdx.x;
     hk = b % a.hkv;
     b /= a.hkv;
     const int hg = b % (G / 4);
     b /= G / 4;
-    blk.tile = a.n_prefix_q_tiles - 1 - b;
-    blk.z = 0;
+    blk.tile = ntx - 1 - b % ntx;
+    blk.z = b / ntx;
     blk.split = 0;
     hq = hk * G + 4 * hg + (w & 3);
+  } else {
+    blk = decode_row_block(a, ntx);
+    hq = blk.hq;
+    hk = hq / (a.hq / a.hkv);
+  }
+  const int seq = a.seq_base + blk.z;
+  bool prefix_rows;
+  int lp0, seg_len, row_base;
+  if (blk.tile < a.n_prefix_q_tiles) {
     prefix_rows = true;
     lp0 = blk.tile * BQ;
     seg_len = a.P;
     row_base = 0;
-    wave_lp0 = lp0 + 32 * (w >> 2);
   } else {
-    blk = decode_row_block(a, a.n_prefix_q_tiles + a.n_suffix_q_tiles);
-    const int seq = a.seq_base + blk.z;
-    if (blk.tile < a.n_prefix_q_tiles) {
-      prefix_rows = true;
-      lp0 = blk.tile * BQ;
-      seg_len = a.P;
-      row_base = 0;
-    } else {
-      prefix_rows = false;
-      lp0 = (blk.tile - a.n_prefix_q_tiles) * BQ;
-      const SegRows sg = suffix_rows(a.cu, seq, a.total_len);
-      row_base = sg.base;
-      seg_len = sg.len;
-    }
-    hq = blk.hq;
-    hk = hq / (a.hq / a.hkv);
-    wave_lp0 = lp0 + 32 * w;  // first row of this wave
+    prefix_rows = false;
+    lp0 = (blk.tile - a.n_prefix_q_tiles) * BQ;
+    const SegRows sg = suffix_rows(a.cu, seq, a.total_len);
+    row_base = sg.base;
+    seg_len = sg.len;
   }
   if (lp0 >= seg_len) return;
+  const int wave_lp0 = lp0 + 32 * (WIDE ? w >> 2 : w);  // first row of this wave
   const int row_lp = wave_lp0 + r;    // this lane's query row (segment-local)
   const bool row_valid = row_lp < seg_len;
   const int my_lp = row_valid ? row_lp : seg_len - 1;  // rows past the end recompute the last one
@@ -348,13 +345,13 @@ hipError_t launch_fwd_bf16(const AttnArgs& a, int head_dim, int n_z, hipStream_t
   return hipGetLastError();
 }
 
-// The prefix forward in its twelve-wave form: a.n_prefix_q_tiles counts
-// 96-row tiles; prefix rows only, no key splits, four q heads per kv head
-// or a multiple of four.
-hipError_t launch_fwd_bf16_wide(const AttnArgs& a, int head_dim, hipStream_t st) {
+// The forward in its twelve-wave form: a.n_prefix_q_tiles and
+// a.n_suffix_q_tiles count 96-row tiles; no key splits, four q heads per kv
+// head or a multiple of four.
+hipError_t launch_fwd_bf16_wide(const AttnArgs& a, int head_dim, int n_z, hipStream_t st) {
   const int G = a.hq / a.hkv;
-  if (G % 4 != 0 || a.n_suffix_q_tiles != 0 || a.n_split > 1 || a.n_seq > 0) return hipErrorInvalidValue;
-  const long nb = (long)a.n_prefix_q_tiles * a.hkv * (G / 4);
+  if (G % 4 != 0 || a.n_split > 1) return hipErrorInvalidValue;
+  const long nb = (long)(a.n_prefix_q_tiles + a.n_suffix_q_tiles) * n_z * a.hkv * (G / 4);
   if (nb == 0) return hipSuccess;
   ProfileScope ps("fwd_bf16", st);
   if (head_dim == 64)

@@ -47,7 +47,7 @@ hipError_t launch_bwd_f32(const AttnArgs& a, int head_dim, int n_qz, hipStream_t
 
 // --- bf16 storage path, MFMA (kernels_bf16_fwd.hip, kernels_bf16_bwd.hip) --
 hipError_t launch_fwd_bf16(const AttnArgs& a, int head_dim, int n_z, hipStream_t st);
-hipError_t launch_fwd_bf16_wide(const AttnArgs& a, int head_dim, hipStream_t st);
+hipError_t launch_fwd_bf16_wide(const AttnArgs& a, int head_dim, int n_z, hipStream_t st);
 int fwd_bf16_wide_block_q();
 hipError_t launch_bwd_bf16(const AttnArgs& a, int head_dim, int n_qz, bool deterministic,
                            hipStream_t st);

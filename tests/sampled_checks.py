@@ -15,8 +15,8 @@ def rel(got, ref):
 
 def sample_rows(P, lens, rng):
     n = len(lens)
-    prefix = sorted({r for r in (0, 1, 63, 64, 127, 128, 255, 256, P // 2, P - 2, P - 1,
-                                 *rng.integers(0, P, 5).tolist()) if 0 <= r < P})
+    rand = rng.integers(0, P, 5).tolist() if P > 0 else []
+    prefix = sorted({r for r in (0, 1, 63, 64, 127, 128, 255, 256, P // 2, P - 2, P - 1, *rand) if 0 <= r < P})
     suffix = sorted({(i, t) for i in (0, n // 2, n - 1)
                      for t in (0, 31, 32, 127, 128, lens[i] // 2, lens[i] - 1) if t < lens[i]})
     return prefix, suffix
@@ -33,8 +33,9 @@ def sample_keys(P, lens, rng):
                   *rng.integers(lo, P, 3).tolist()}
     else:
         last = (P - 1) // 192 * 192  # first key of the last 192-key tile
+        rand = rng.integers(0, P, 4).tolist() if P > 0 else []
         prefix = {0, 1, 63, 64, 127, 128, 191, 192, 383, 384, P // 2 - 1, P // 2, last - 1, last,
-                  P - 65, P - 64, P - 2, P - 1, *rng.integers(0, P, 4).tolist()}
+                  P - 65, P - 64, P - 2, P - 1, *rand}
     prefix = sorted(k for k in prefix if 0 <= k < P)
     suffix = sorted({(i, t) for i in (0, n // 2, n - 1)
                      for t in (0, 1, 63, 64, lens[i] // 2, lens[i] - 1) if t < lens[i]})
@@ -52,6 +53,8 @@ def sampled_errors(inp, got, rng, cache=True):
     prefix_rows, suffix_rows = sample_rows(P, lens, rng)
     ref = sampled_rows_reference(inp, prefix_rows, suffix_rows)
     for key, rows, sfx in (("prefix", prefix_rows, "_p"), ("suffix", suffix_rows, "_s")):
+        if not rows:  # no prefix (P = 0)
+            continue
         for f in ("o", "dq", "lse"):
             g, r = [], []
             for row in rows:
@@ -62,7 +65,7 @@ def sampled_errors(inp, got, rng, cache=True):
     prefix_keys, suffix_keys = sample_keys(P, lens, rng)
     kref = sampled_keys_reference(inp, prefix_keys, suffix_keys)
     fams = (("dk", "dk_p"), ("dv", "dv_p")) + ((("g_k", "g_k"), ("g_v", "g_v")) if cache else ())
-    for f, gk in fams:
+    for f, gk in fams if prefix_keys else ():
         errs[gk + "@keys"] = rel([got[gk][j] for j in prefix_keys], [kref["prefix"][j][f] for j in prefix_keys])
     for f in ("dk", "dv"):
         errs[f + "_s@keys"] = rel([got[f + "_s"][int(cu[i]) + t] for i, t in suffix_keys],

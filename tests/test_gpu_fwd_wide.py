@@ -14,10 +14,11 @@ sampled rows of every q head (the first rows, both sides of the 64-key and
 96-row tile edges, the middle, the first row of the last partial row tile,
 the last rows, random rows) at prefix lengths that are multiples of
 neither tile, d = 128 and 64, four and eight q heads per kv head (eight:
-two workgroups per row tile); then whole schedules whose suffix forward,
-and a dense baseline whose per-trajectory forward, take the twelve-wave
-form, on sampled rows and keys (O, LSE, dQ, dK, dV and the cache), as the
-full-length tests check them."""
+two workgroups per row tile); then whole schedules whose suffix forward
+takes the twelve-wave form (with and without a prefix; d = 128 and 64;
+four and eight q heads per kv head), and a dense baseline whose
+per-trajectory forward takes it, on sampled rows and keys (O, LSE, dQ, dK,
+dV and the cache), as the full-length tests check them."""
 import numpy as np
 import pytest
 
@@ -58,6 +59,7 @@ PREFIX_CASES = [
 SUFFIX_CASES = [
     ("p0_two_sequences_6200", GroupShape(32, 8, 128, 0, (6200, 6131), "bf16")),
     ("p1000_three_ragged_suffixes", GroupShape(32, 8, 128, 1000, (6000, 4999, 5537), "bf16")),
+    ("p0_g8_d64_two_sequences", GroupShape(32, 4, 64, 0, (6200, 6100), "bf16")),
 ]
 # the dense baseline: each trajectory's forward over P + S rows
 DENSE_CASE = ("dense_p12300_n2", GroupShape(32, 8, 128, 12300, (64, 37), "bf16"))

@@ -6,9 +6,11 @@
 // joint softmax across the prefix keys and the row's own causal suffix keys
 // (H_2 = P_21 V_1 + P_22 V_2), plus the row's natural-log LSE.
 //
-// Structure: one workgroup = 4 waves = 128 query rows of one q head; each
-// wave owns 32 rows.  Keys stream through LDS in 64-row tiles, first the
-// prefix tiles (read in place from K_P/V_P), then the suffix's own tiles.
+// Structure: one workgroup = 4 waves = 128 query rows of one q head (or, in
+// the twelve-wave form of large unsplit launches, 12 waves = 96 rows of the
+// four q heads of one kv head); each wave owns 32 rows of one head.  Keys
+// stream through LDS in 64-row tiles, first the prefix tiles (read in place
+// from K_P/V_P), then the suffix's own tiles.
 // Tiles are double-buffered: the next tile's direct-to-LDS loads are issued
 // before the current tile's products.  Per tile and wave
 // (v_mfma_f32_32x32x16_bf16, operand conventions in tile.hpp):
